@@ -1,0 +1,215 @@
+"""fp64 CPU oracle of the ALS half-sweep -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package. It shares no code with the HIP library
+(``paper_1108_2580_amd``) and neither imports the other; the only common
+dependency is the seeded input generator in ``workload``.
+
+Method (paper Sec. 2.2): with one side of the factorisation fixed, each row s of
+the other side is the regularised least-squares solution
+    x_s = (sum_j f_j f_j^T + lambda n_s I)^{-1} sum_j r_sj f_j,
+computed in fp64 by Cholesky (the per-update "matrix inversion" of Sec. 4.1).
+A prediction is u_u . v_i (Sec. 2.2); RMSE (Sec. 4.1) is taken over the stored
+ratings. One sweep solves the items with the users fixed, then the users with
+the items fixed (the order of Sec. 2.2).
+
+Pins (tests/test_oracle_pins.py) tie every function here to something other
+than itself: ridge least squares, stationarity, a monotone objective, closed
+forms, the SVD soft-threshold optimum of the dense case, exact low-rank
+recovery, symmetry, linearity, thread invariance, an independent transpose
+and hand-derived rational worked examples.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_SRC = os.path.join(_HERE, "als_oracle.c")
+
+
+def build(verbose: bool = False) -> str:
+    """Compile als_oracle.c into liboracle.so (gcc -O2, OpenMP, strict IEEE fp64)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def _configure(lib):
+    """Declare the C signatures on a loaded oracle library."""
+    P, i64, i32, f64, c_int = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
+                               ctypes.c_int)
+    lib.orc_transpose.argtypes = [i64, i64, P, P, P, P, P, P]
+    lib.orc_transpose.restype = c_int
+    lib.orc_normal_equations.argtypes = [i32, i64, P, P, P, f64, P, P]
+    lib.orc_normal_equations.restype = None
+    lib.orc_cholesky_solve.argtypes = [i32, P, P, P, P]
+    lib.orc_cholesky_solve.restype = c_int
+    lib.orc_half_sweep.argtypes = [i64, P, P, P, i32, P, f64, P, P, c_int]
+    lib.orc_half_sweep.restype = i64
+    lib.orc_solve_rows.argtypes = [i64, P, P, P, P, i32, P, f64, P, P, c_int]
+    lib.orc_solve_rows.restype = i64
+    lib.orc_sse.argtypes = [i64, P, P, P, i32, P, P, P, c_int]
+    lib.orc_sse.restype = f64
+    lib.orc_weighted_norm.argtypes = [i64, P, i32, P]
+    lib.orc_weighted_norm.restype = f64
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build()
+    _lib = _configure(ctypes.CDLL(_LIB_PATH))
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i64(a):
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def transpose(ptr, idx, val, n_cols):
+    """Compressed rows -> compressed columns (rows ascending inside each column)."""
+    ptr, idx, val = _i64(ptr), _i32(idx), _f64(val)
+    n_rows = ptr.size - 1
+    out_ptr = np.empty(n_cols + 1, dtype=np.int64)
+    out_idx = np.empty(idx.size, dtype=np.int32)
+    out_val = np.empty(idx.size, dtype=np.float64)
+    if _load().orc_transpose(n_rows, n_cols, _p(ptr), _p(idx), _p(val), _p(out_ptr), _p(out_idx),
+                             _p(out_val)) != 0:
+        raise ValueError("column index out of range")
+    return out_ptr, out_idx, out_val
+
+
+def normal_equations(row, ptr, idx, val, F, lam):
+    """(A, b) of one row: A = sum f f^T + lam n I, b = sum r f (fp64, rating order)."""
+    ptr, idx, val, F = _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    D = F.shape[1]
+    s, e = int(ptr[row]), int(ptr[row + 1])
+    A = np.empty((D, D))
+    b = np.empty(D)
+    _load().orc_normal_equations(D, e - s, _p(idx[s:e]), _p(val[s:e]), _p(F), float(lam), _p(A),
+                                 _p(b))
+    return A, b
+
+
+def cholesky_solve(A, b):
+    """x = A^{-1} b by Cholesky; returns None when A is not numerically SPD."""
+    A, b = _f64(A), _f64(b)
+    D = b.size
+    W = np.zeros((D, D))
+    x = np.empty(D)
+    if _load().orc_cholesky_solve(D, _p(A), _p(b), _p(W), _p(x)) != 0:
+        return None
+    return x
+
+
+def half_sweep(ptr, idx, val, F, lam, X_prev, threads=0):
+    """One half-sweep. Returns (X_new, flags) with flags 0 solved / 1 not SPD / 2 empty.
+
+    Rows that are empty or flagged keep their value from X_prev."""
+    ptr, idx, val, F = _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    X = np.array(X_prev, dtype=np.float64, order="C", copy=True)
+    n_rows = ptr.size - 1
+    D = F.shape[1]
+    assert X.shape == (n_rows, D)
+    flags = np.empty(n_rows, dtype=np.int8)
+    _load().orc_half_sweep(n_rows, _p(ptr), _p(idx), _p(val), D, _p(F), float(lam), _p(X),
+                           _p(flags), int(threads))
+    return X, flags
+
+
+def solve_rows(rows, ptr, idx, val, F, lam, threads=0):
+    """The half-sweep update of the listed rows only: (X_sel, flags)."""
+    rows, ptr, idx, val, F = _i64(rows), _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    D = F.shape[1]
+    X = np.empty((rows.size, D))
+    flags = np.empty(rows.size, dtype=np.int8)
+    _load().orc_solve_rows(rows.size, _p(rows), _p(ptr), _p(idx), _p(val), D, _p(F), float(lam),
+                           _p(X), _p(flags), int(threads))
+    return X, flags
+
+
+def sse(ptr, idx, val, X, F, threads=0, per_row=False):
+    """Sum of squared residuals over the stored ratings of the rows of X."""
+    ptr, idx, val, X, F = _i64(ptr), _i32(idx), _f64(val), _f64(X), _f64(F)
+    n_rows = ptr.size - 1
+    rs = np.empty(n_rows) if per_row else None
+    tot = _load().orc_sse(n_rows, _p(ptr), _p(idx), _p(val), F.shape[1], _p(X), _p(F), _p(rs),
+                          int(threads))
+    return (tot, rs) if per_row else tot
+
+
+def rmse(ptr, idx, val, X, F, threads=0):
+    nnz = int(ptr[-1])
+    return float(np.sqrt(sse(ptr, idx, val, X, F, threads) / nnz)) if nnz else 0.0
+
+
+def weighted_norm(ptr, X):
+    ptr, X = _i64(ptr), _f64(X)
+    return _load().orc_weighted_norm(ptr.size - 1, _p(ptr), X.shape[1], _p(X))
+
+
+def objective(csr, csc, U, V, lam, threads=0):
+    """L(U,V) = sum (r - u.v)^2 + lam (sum_u n_u ||u||^2 + sum_i n_i ||v_i||^2)."""
+    ptr, col, val = csr
+    cptr = csc[0]
+    return (sse(ptr, col, val, U, V, threads)
+            + lam * (weighted_norm(ptr, U) + weighted_norm(cptr, V)))
+
+
+class Trajectory:
+    """Free-running fp64 ALS from the given (fp32) initial factors.
+
+    ``step(side)`` performs one half-sweep: side "items" solves V with U fixed,
+    side "users" solves U with V fixed."""
+
+    def __init__(self, M, N, row_ptr, col, val, U0, V0, lam, threads=0):
+        self.csr = (_i64(row_ptr), _i32(col), _f64(val))
+        self.csc = transpose(self.csr[0], self.csr[1], self.csr[2], N)
+        self.U = _f64(U0).copy()
+        self.V = _f64(V0).copy()
+        self.lam = float(lam)
+        self.threads = threads
+        self.nflag = 0
+
+    def step(self, side):
+        if side == "items":
+            self.V, fl = half_sweep(*self.csc, self.U, self.lam, self.V, self.threads)
+        else:
+            self.U, fl = half_sweep(*self.csr, self.V, self.lam, self.U, self.threads)
+        self.nflag = int((fl == 1).sum())
+        return self
+
+    def sweep(self):
+        return self.step("items").step("users")
+
+    def rmse(self):
+        return rmse(*self.csr, self.U, self.V, self.threads)
+
+    def objective(self):
+        return objective(self.csr, self.csc, self.U, self.V, self.lam, self.threads)

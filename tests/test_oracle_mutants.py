@@ -1,0 +1,66 @@
+"""The oracle pins must be sensitive: plant plausible mistakes in a copy of the
+oracle's C source (on the CPU only), rebuild it, and check that the pins catch
+every one of them."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
+
+# (name, original text, mutated text)
+MUTANTS = [
+    ("unweighted_lambda", "A[a * D + a] += lambda * (double)n;", "A[a * D + a] += lambda;"),
+    ("rhs_without_rating", "b[a] += r * f[a];", "b[a] += f[a];"),
+    ("first_rating_dropped", "for (int64_t k = 0; k < n; ++k) {", "for (int64_t k = 1; k < n; ++k) {"),
+    ("backsolve_transposed", "s -= W[m * D + i] * x[m];", "s -= W[i * D + m] * x[m];"),
+    ("cholesky_sign", "s -= W[i * D + m] * W[j * D + m];", "s += W[i * D + m] * W[j * D + m];"),
+    ("forward_solve_no_update", "s -= W[i * D + m] * y[m];", "s -= 0.0 * y[m];"),
+    ("prediction_wrong_index", "pred += x[a] * f[a];", "pred += x[a] * f[0];"),
+    ("transpose_rows_reversed", "for (int64_t r = 0; r < n_rows; ++r) {\n    for (int64_t p = ptr[r];",
+     "for (int64_t r = n_rows - 1; r >= 0; --r) {\n    for (int64_t p = ptr[r];"),
+    ("norm_unweighted", "total += (double)(ptr[s + 1] - ptr[s]) * q;", "total += q;"),
+    ("zero_degree_overwritten", "if (n == 0) return 2;", "if (n < 0) return 2;"),
+]
+
+PIN_TESTS = [
+    pins.test_golden_worked_solves,
+    pins.test_golden_worked_rmse,
+    lambda: pins.test_brute_force_rational(3, 5),
+    lambda: pins.test_p1_matches_lstsq(3),
+    pins.test_p2_gradient_zero,
+    pins.test_p4_single_rating_sherman_morrison,
+    pins.test_p4_one_factor,
+    pins.test_p4_orthogonal_rows,
+    pins.test_p5_dense_soft_threshold,
+    pins.test_p7_symmetry,
+    pins.test_p10_transpose,
+    pins.test_p11_rmse_gram_identity,
+    pins.test_empty_row_unchanged_and_zero_ratings_counted,
+]
+
+
+@pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, orig, mut):
+    src = open(SRC).read()
+    assert src.count(orig) == 1, f"mutation anchor not unique for {name}"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(orig, mut))
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", str(so), str(path), "-lm"])
+    saved = oracle._lib
+    oracle._lib = oracle._configure(ctypes.CDLL(str(so)))
+    caught = []
+    try:
+        for t in PIN_TESTS:
+            try:
+                t()
+            except (AssertionError, ValueError, StopIteration, IndexError, ZeroDivisionError):
+                caught.append(getattr(t, "__name__", "lambda"))
+    finally:
+        oracle._lib = saved
+    assert caught, f"no pin caught mutant {name}"

@@ -1,0 +1,338 @@
+"""Seeded synthetic rating matrices and factor initialisation for the ALS workloads.
+
+This module manufactures inputs only. It holds none of the ALS arithmetic and
+is the one piece shared by the fp64 oracle (``oracle/``) and the HIP library
+(``paper_1108_2580_amd``): both read the bytes it produces.
+
+The shapes follow the paper's data set (Yahoo! Music, Sec. 1: 1,000,990 users,
+624,961 items, 262,810,175 ratings; ratings are integers 0..100, Sec. 3). The
+data set itself is not available, so the full-scale workloads are synthetic
+stand-ins with that shape; degree distributions and rating mixtures follow the
+recipes below (see ``CONFIGS``).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsynth.so")
+_SRC = os.path.join(_HERE, "synth.c")
+
+
+def build(verbose: bool = False) -> str:
+    """Compile synth.c into libsynth.so (gcc, OpenMP)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i64, u64, i32, f64 = ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_double
+    lib.synth_sample_rows.argtypes = [i64, P, i64, P, u64, P]
+    lib.synth_sample_rows.restype = ctypes.c_int
+    lib.synth_ratings_mixture.argtypes = [i64, u64, P]
+    lib.synth_ratings_mixture.restype = None
+    lib.synth_lowrank_scores.argtypes = [i64, P, P, i32, P, P, P]
+    lib.synth_lowrank_scores.restype = None
+    lib.synth_quantise.argtypes = [i64, P, f64, f64, f64, f64, f64, u64, P]
+    lib.synth_quantise.restype = None
+    lib.synth_transpose.argtypes = [i64, i64, P, P, P, P, P, P]
+    lib.synth_transpose.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+@dataclasses.dataclass
+class Ratings:
+    """A rating matrix in CSR by user: row_ptr int64[M+1], col int32[nnz], val uint8[nnz]."""
+
+    name: str
+    M: int
+    N: int
+    row_ptr: np.ndarray
+    col: np.ndarray
+    val: np.ndarray
+    D: int
+    lam: float
+    sweeps: int
+    data_seed: int
+    init_seed: int
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1])
+
+
+# data_seed = 11082580 + k, init_seed = data_seed + 1000; the two full-scale
+# configurations (D=20 and D=100) share one matrix, generated from the D=20 seed.
+CONFIGS = {
+    1: dict(name="tiny_2000x1000_d10", M=2000, N=1000, nnz=50_000, D=10, lam=0.05, sweeps=5,
+            kind="uniform", rank=10, noise=5.0),
+    2: dict(name="mid_100000x50000_d20", M=100_000, N=50_000, nnz=10_000_000, D=20, lam=0.065,
+            sweeps=10, kind="zipf", rank=20, noise=10.0),
+    3: dict(name="full_1000990x624961_d20", M=1_000_990, N=624_961, nnz=262_810_175, D=20,
+            lam=0.065, sweeps=5, kind="kddcup"),
+    4: dict(name="full_1000990x624961_d100", M=1_000_990, N=624_961, nnz=262_810_175, D=100,
+            lam=0.065, sweeps=3, kind="kddcup", matrix_of=3),
+    5: dict(name="hub_500000x200000_d128", M=500_000, N=200_000, nnz=150_000_000, D=128,
+            lam=0.05, sweeps=3, kind="itemhub", rank=32, noise=10.0),
+}
+
+# Zipf-Mandelbrot offset of the full-scale item popularity (weights (r+q)^-1.1);
+# chosen so that the most-rated item lands near 500k ratings after sampling.
+KDD_ITEM_Q = 32.0
+
+
+def data_seed(k: int) -> int:
+    return 11082580 + k
+
+
+def exact_degrees(raw: np.ndarray, lo: int, hi: int, total: int) -> np.ndarray:
+    """Integer degrees proportional to ``raw``, clamped to [lo, hi], summing exactly to ``total``.
+
+    A common scale s is found by bisection so that sum(clip(s*raw, lo, hi)) = total;
+    the real values are then floored and the remainder handed out one by one to the
+    largest fractional parts (ties by index), never beyond ``hi``.
+    """
+    raw = np.asarray(raw, dtype=np.float64)
+    n = raw.size
+    if not (lo * n <= total <= hi * n):
+        raise ValueError("infeasible degree total")
+    a, b = 0.0, 1.0
+    while np.clip(b * raw, lo, hi).sum() < total:
+        b *= 2.0
+    for _ in range(200):
+        m = 0.5 * (a + b)
+        if np.clip(m * raw, lo, hi).sum() < total:
+            a = m
+        else:
+            b = m
+    x = np.clip(b * raw, lo, hi)
+    f = np.floor(x)
+    rem = int(total - f.sum())
+    if rem < 0:
+        raise RuntimeError("degree bisection overshoot")
+    frac = np.where(f < hi, x - f, -1.0)
+    order = np.argsort(-frac, kind="stable")
+    f[order[:rem]] += 1
+    out = f.astype(np.int64)
+    assert int(out.sum()) == total and out.min() >= lo and out.max() <= hi
+    return out
+
+
+def _ptr_from_degrees(deg: np.ndarray) -> np.ndarray:
+    ptr = np.zeros(deg.size + 1, dtype=np.int64)
+    np.cumsum(deg, out=ptr[1:])
+    return ptr
+
+
+def _sample(ptr: np.ndarray, n_cols: int, weights: np.ndarray, seed: int) -> np.ndarray:
+    lib = _load()
+    nnz = int(ptr[-1])
+    col = np.empty(nnz, dtype=np.int32)
+    w = np.ascontiguousarray(weights, dtype=np.float64)
+    rc = lib.synth_sample_rows(ptr.size - 1, _p(ptr), n_cols, _p(w), seed, _p(col))
+    if rc != 0:
+        raise RuntimeError("synth_sample_rows failed")
+    return col
+
+
+def _lowrank_ratings(M, N, ptr, col, rank, noise, seed, rng) -> np.ndarray:
+    """Rank-k ground truth U*.V*^T standardised over the stored entries to mean 50, sd 20,
+    plus N(0, noise) noise, rounded and clipped to 0..100."""
+    lib = _load()
+    A = rng.standard_normal((M, rank))
+    B = rng.standard_normal((N, rank))
+    nnz = int(ptr[-1])
+    score = np.empty(nnz, dtype=np.float64)
+    lib.synth_lowrank_scores(M, _p(ptr), _p(col), rank, _p(A), _p(B), _p(score))
+    mu = float(score.mean())
+    sigma = float(score.std())
+    val = np.empty(nnz, dtype=np.uint8)
+    lib.synth_quantise(nnz, _p(score), mu, sigma, 50.0, 20.0, float(noise), seed ^ 0x5EED, _p(val))
+    return val
+
+
+def _rank_weights(n: int, f, rng) -> np.ndarray:
+    """Popularity weight f(rank) (rank 1 = most popular) assigned to ids by a seeded permutation."""
+    ranks = np.arange(1, n + 1, dtype=np.float64)
+    w_by_rank = f(ranks)
+    perm = rng.permutation(n)
+    w = np.empty(n, dtype=np.float64)
+    w[perm] = w_by_rank
+    return w
+
+
+def _make_uniform(cfg, seed):
+    rng = np.random.default_rng(seed)
+    M, N, nnz = cfg["M"], cfg["N"], cfg["nnz"]
+    pos = np.sort(rng.choice(M * N, size=nnz, replace=False))
+    row = pos // N
+    col = (pos % N).astype(np.int32)
+    ptr = np.zeros(M + 1, dtype=np.int64)
+    np.add.at(ptr, row + 1, 1)
+    np.cumsum(ptr, out=ptr)
+    val = _lowrank_ratings(M, N, ptr, col, cfg["rank"], cfg["noise"], seed, rng)
+    return ptr, col, val
+
+
+def _make_zipf(cfg, seed):
+    """Users: d(r) = clamp(C/r, 5, 50000) over a random rank order, C fitted to nnz exactly.
+    Items: weights max(1/r, f) (Zipf 1.0 with a floor f that gives ~5 expected ratings)."""
+    rng = np.random.default_rng(seed)
+    M, N, nnz = cfg["M"], cfg["N"], cfg["nnz"]
+    ranks = np.arange(1, M + 1, dtype=np.float64)
+    deg_by_rank = exact_degrees(1.0 / ranks, 5, 50_000, nnz)
+    perm = rng.permutation(M)
+    deg = np.empty(M, dtype=np.int64)
+    deg[perm] = deg_by_rank
+    ptr = _ptr_from_degrees(deg)
+    r = np.arange(1, N + 1, dtype=np.float64)
+    lo_f, hi_f = 0.0, 1.0
+    for _ in range(100):
+        f = 0.5 * (lo_f + hi_f)
+        expect = nnz * f / np.maximum(1.0 / r, f).sum()
+        if expect < 5.0:
+            lo_f = f
+        else:
+            hi_f = f
+    fl = hi_f
+    w = _rank_weights(N, lambda x: np.maximum(1.0 / x, fl), rng)
+    col = _sample(ptr, N, w, seed)
+    val = _lowrank_ratings(M, N, ptr, col, cfg["rank"], cfg["noise"], seed, rng)
+    return ptr, col, val
+
+
+def _make_kddcup(cfg, seed):
+    """Users: lognormal degrees (median 120, sigma fitted so the mean is nnz/M), min 10,
+    cap 62,500, exact total. Items: Zipf-Mandelbrot weights (r+q)^-1.1.
+    Ratings: 30 % at 0, 20 % uniform on 90..100, 50 % uniform on 1..89."""
+    from scipy.special import ndtri
+
+    rng = np.random.default_rng(seed)
+    M, N, nnz = cfg["M"], cfg["N"], cfg["nnz"]
+    median = 120.0
+    sigma = math.sqrt(2.0 * math.log((nnz / M) / median))
+    q = (np.arange(M, dtype=np.float64) + 0.5) / M
+    raw = np.exp(math.log(median) + sigma * ndtri(q))
+    deg_sorted = exact_degrees(raw, 10, 62_500, nnz)
+    perm = rng.permutation(M)
+    deg = np.empty(M, dtype=np.int64)
+    deg[perm] = deg_sorted
+    ptr = _ptr_from_degrees(deg)
+    w = _rank_weights(N, lambda x: (x + KDD_ITEM_Q) ** -1.1, rng)
+    col = _sample(ptr, N, w, seed)
+    val = np.empty(nnz, dtype=np.uint8)
+    _load().synth_ratings_mixture(nnz, seed ^ 0xBEEF, _p(val))
+    return ptr, col, val
+
+
+def _make_itemhub(cfg, seed):
+    """Items prescribed: d(r) = clamp(C r^-1.5, 1, M) (the top items are rated by every
+    user), exact total. Users: weights r^-1.2. Rank-32 ratings with N(0,10) noise."""
+    rng = np.random.default_rng(seed)
+    M, N, nnz = cfg["M"], cfg["N"], cfg["nnz"]
+    ranks = np.arange(1, N + 1, dtype=np.float64)
+    deg_by_rank = exact_degrees(ranks ** -1.5, 1, M, nnz)
+    perm = rng.permutation(N)
+    deg = np.empty(N, dtype=np.int64)
+    deg[perm] = deg_by_rank
+    cptr = _ptr_from_degrees(deg)
+    w = _rank_weights(M, lambda x: x ** -1.2, rng)
+    rows = _sample(cptr, M, w, seed)
+    lib = _load()
+    ptr = np.empty(M + 1, dtype=np.int64)
+    col = np.empty(nnz, dtype=np.int32)
+    dummy = np.zeros(nnz, dtype=np.uint8)
+    outv = np.empty(nnz, dtype=np.uint8)
+    if lib.synth_transpose(N, M, _p(cptr), _p(rows), _p(dummy), _p(ptr), _p(col), _p(outv)) != 0:
+        raise RuntimeError("transpose failed")
+    del rows, dummy, outv
+    val = _lowrank_ratings(M, N, ptr, col, cfg["rank"], cfg["noise"], seed, rng)
+    return ptr, col, val
+
+
+_MAKERS = {"uniform": _make_uniform, "zipf": _make_zipf, "kddcup": _make_kddcup,
+           "itemhub": _make_itemhub}
+
+
+def make_config(k: int) -> Ratings:
+    """Generate configuration k (1..5) deterministically."""
+    cfg = CONFIGS[k]
+    mk = cfg.get("matrix_of", k)
+    seed = data_seed(mk)
+    cache = os.environ.get("ALS_WORKLOAD_CACHE")
+    path = os.path.join(cache, f"matrix_{mk}.npz") if cache else None
+    if path and os.path.exists(path):
+        z = np.load(path)
+        ptr, col, val = z["row_ptr"], z["col"], z["val"]
+    else:
+        ptr, col, val = _MAKERS[CONFIGS[mk]["kind"]](CONFIGS[mk], seed)
+        if path:
+            os.makedirs(cache, exist_ok=True)
+            np.savez(path, row_ptr=ptr, col=col, val=val)
+    return Ratings(name=cfg["name"], M=cfg["M"], N=cfg["N"], row_ptr=ptr, col=col, val=val,
+                   D=cfg["D"], lam=cfg["lam"], sweeps=cfg["sweeps"], data_seed=seed,
+                   init_seed=data_seed(k) + 1000)
+
+
+def make_custom(M: int, N: int, deg_users: np.ndarray, seed: int, item_weights=None,
+                ratings: str = "mixture") -> tuple:
+    """A small matrix with prescribed user degrees (for edge-case tests)."""
+    deg = np.asarray(deg_users, dtype=np.int64)
+    ptr = _ptr_from_degrees(deg)
+    w = np.ones(N) if item_weights is None else np.asarray(item_weights, dtype=np.float64)
+    col = _sample(ptr, N, w, seed) if ptr[-1] > 0 else np.zeros(0, dtype=np.int32)
+    val = np.empty(int(ptr[-1]), dtype=np.uint8)
+    if ptr[-1] > 0:
+        _load().synth_ratings_mixture(int(ptr[-1]), seed ^ 0xBEEF, _p(val))
+    return ptr, col, val
+
+
+def init_factors(M: int, N: int, D: int, seed: int) -> tuple:
+    """U0 (M x D) then V0 (N x D), fp32, N(0, sd 0.1), from one PCG64 stream."""
+    rng = np.random.default_rng(seed)
+    U = rng.standard_normal((M, D), dtype=np.float32)
+    U *= np.float32(0.1)
+    V = rng.standard_normal((N, D), dtype=np.float32)
+    V *= np.float32(0.1)
+    return U, V
+
+
+def degree_stats(ptr: np.ndarray) -> dict:
+    d = np.diff(ptr)
+    return dict(n=int(d.size), total=int(d.sum()), max=int(d.max()), p99=float(np.percentile(d, 99)),
+                median=float(np.median(d)), min=int(d.min()), frac_lt20=float((d < 20).mean()))
+
+
+def realised_stats(r: Ratings) -> dict:
+    """Degree statistics of both sides and the rating histogram summary."""
+    item_deg = np.bincount(r.col, minlength=r.N)
+    iptr = _ptr_from_degrees(item_deg)
+    v = r.val
+    return dict(users=degree_stats(r.row_ptr), items=degree_stats(iptr),
+                ratings=dict(mean=float(v.mean()), frac0=float((v == 0).mean()),
+                             frac_ge90=float((v >= 90).mean())))
