@@ -1,0 +1,155 @@
+/*
+ * als.h -- C ABI of the MI355X (gfx950) alternating-least-squares half-sweep.
+ *
+ * The method (paper Sec. 2.2, "ALS and BPTF"): the observed ratings form a
+ * sparse M x N matrix A (users x items); A ~= U V with U (M x D) and V
+ * (D x N). Starting from an initial guess, each iteration fixes U and solves
+ * V by least squares, then fixes V and solves U the same way. A prediction is
+ * the dot product of the user and item vectors. One such least-squares pass
+ * over one side is a "half-sweep":
+ *
+ *   for every row s of the solved side with n_s = |Omega_s| > 0 ratings,
+ *     x_s = (sum_{j in Omega_s} f_j f_j^T + lambda * n_s * I)^{-1}
+ *           * sum_{j in Omega_s} r_sj f_j,
+ *
+ * where f_j are the fixed side's rows. The per-update "matrix inversion"
+ * (Sec. 4.1) is done by Cholesky. The quality measure is RMSE (Sec. 4.1),
+ * here the training RMSE over all stored ratings.
+ *
+ * Conventions
+ *  - Layout: U is stored [n_users x D] and V is stored [n_items x D], both
+ *    row-major fp32 (V transposed relative to the paper's D x N, so that one
+ *    item's vector is contiguous).
+ *  - The rating matrix is given once, as host CSR by user; every stored
+ *    position is an observed rating, including explicit zeros.
+ *  - Ownership: the library copies the CSR to the device and owns it, the
+ *    device-built CSC, the row schedules and all workspace. The caller owns
+ *    every factor buffer (device memory, e.g. torch tensors).
+ *  - Execution: work is enqueued on the HIP stream given at creation. A call
+ *    synchronises that stream only where stated (RMSE read-back, flag count).
+ *  - Errors: every call returns an als_status; nothing is thrown across the
+ *    ABI. als_last_error() gives a message for the last failing call.
+ *  - Threading: calls on one context must not overlap.
+ *  - Determinism: results are bitwise reproducible run to run (fixed
+ *    reduction orders, no floating-point atomics).
+ */
+#ifndef ALS_MI355X_H
+#define ALS_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct als_ctx als_ctx;
+
+typedef enum {
+  ALS_OK = 0,
+  ALS_ERR_INVALID_ARG = 1,   /* bad pointer, size, D, lambda, side, aliasing */
+  ALS_ERR_BAD_MATRIX = 2,    /* CSR fails validation (see als_create) */
+  ALS_ERR_OUT_OF_MEMORY = 3, /* device or host allocation failed */
+  ALS_ERR_HIP = 4,           /* a HIP runtime call failed (message has details) */
+  ALS_ERR_NOT_SPD = 5        /* half-sweep completed; >= 1 row flagged and left unchanged */
+} als_status;
+
+typedef enum {
+  ALS_ROWS_USERS = 0, /* solve U (rows of the CSR) with V fixed */
+  ALS_ROWS_ITEMS = 1  /* solve V (rows of the CSC) with U fixed */
+} als_side;
+
+/* Tunables of the degree-bucketed schedule. Zero fields select defaults. */
+typedef struct {
+  int32_t hub_threshold;   /* rows with more ratings are split into chunks (default 8192) */
+  int32_t chunk;           /* ratings per chunk of a split row (default 4096) */
+  int64_t workspace_bytes; /* cap on the partial-Gram workspace; larger half-sweeps run in
+                              several batches (default 48 GiB) */
+} als_tuning;
+
+/*
+ * Create a context for one rating matrix and one factor width D.
+ *   n_users, n_items  matrix shape (M, N); each >= 1 and < 2^31.
+ *   nnz               number of stored ratings; 0 <= nnz < 2^31.
+ *   row_ptr           host int64[n_users + 1]: row_ptr[0] = 0, non-decreasing,
+ *                     row_ptr[n_users] = nnz.
+ *   col_idx           host int32[nnz]: item of each rating, in [0, n_items),
+ *                     strictly increasing within each row (no duplicates).
+ *   ratings           host uint8[nnz]: the rating values (0..255 accepted).
+ *   D                 factor width, 1 <= D <= 128.
+ *   hip_stream        hipStream_t to enqueue on (NULL = default stream).
+ *   tuning            nullable; see als_tuning.
+ * Validation failures return ALS_ERR_BAD_MATRIX or ALS_ERR_INVALID_ARG and
+ * set *out = NULL. On success the host arrays may be freed by the caller.
+ * The call builds the item-major layout (CSC) on the device and the per-side
+ * row schedules; it synchronises the stream before returning.
+ */
+als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t nnz,
+                      const int64_t *row_ptr, const int32_t *col_idx, const uint8_t *ratings,
+                      int32_t D, void *hip_stream, const als_tuning *tuning);
+
+/*
+ * One half-sweep (paper Sec. 2.2).
+ *   side           ALS_ROWS_USERS: fixed = V [n_items x D], out = U [n_users x D].
+ *                  ALS_ROWS_ITEMS: fixed = U [n_users x D], out = V [n_items x D].
+ *   fixed_factors  device fp32, row-major, read only.
+ *   lambda         regularisation weight, finite and >= 0; the diagonal gets
+ *                  lambda * n_s for a row with n_s ratings.
+ *   out_factors    device fp32, row-major, must not overlap fixed_factors.
+ *                  The caller pre-fills it with the previous iterate: rows with
+ *                  no ratings and flagged rows (pivot <= 0 or non-finite in the
+ *                  Cholesky) keep that content.
+ *   rmse_out       host, nullable. If non-NULL the call synchronises the stream
+ *                  and writes the training RMSE of the new state (out_factors
+ *                  against fixed_factors over all ratings), and returns
+ *                  ALS_ERR_NOT_SPD if any row was flagged.
+ */
+als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
+                          float *out_factors, double *rmse_out);
+
+/*
+ * Training RMSE of (U, V): sqrt(sum over stored ratings of (r - u_u . v_i)^2 / nnz).
+ * U, V: device fp32 [n_users x D], [n_items x D]. Synchronises the stream.
+ * An empty matrix gives 0.
+ */
+als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
+
+/* Rows flagged (not SPD / non-finite) by the last half-sweep; synchronises the
+ * stream. Returns -1 for a NULL context. */
+int64_t als_flagged_rows(als_ctx *ctx);
+
+/*
+ * Copy the device-built CSC (rows ascending within each column) to host
+ * buffers: col_ptr int64[n_items + 1], row_idx int32[nnz], ratings uint8[nnz].
+ * Synchronises the stream.
+ */
+als_status als_get_csc(als_ctx *ctx, int64_t *col_ptr, int32_t *row_idx, uint8_t *ratings);
+
+/*
+ * Schedule statistics of one side, for tests and reports. out receives up to
+ * n values in this order: rows with ratings, rows split into chunks, work
+ * items (rows + chunks), batches, largest degree, workspace bytes per batch.
+ */
+als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
+
+/*
+ * Optional per-phase timing with HIP events recorded on the context's stream
+ * around each kernel launch. When enabled, every half-sweep synchronises the
+ * stream at its end to collect the event times. Phases: 0 = Gram (partial
+ * normal equations), 1 = Cholesky + solve, 2 = residual, 3 = reduction.
+ */
+als_status als_set_profiling(als_ctx *ctx, int32_t enable);
+als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches);
+
+void als_destroy(als_ctx *ctx);
+
+const char *als_status_str(als_status s);
+
+/* Message of the last failing call on ctx (or of the last failed
+ * als_create when ctx is NULL); valid until the next call on ctx. */
+const char *als_last_error(const als_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALS_MI355X_H */

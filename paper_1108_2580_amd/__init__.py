@@ -1,0 +1,193 @@
+"""Python binding of libals, the MI355X ALS half-sweep (C ABI in include/als.h).
+
+Argument marshalling only: every step of the half-sweep runs in the HIP
+kernels of ``csrc/``. PyTorch supplies device memory (fp32 tensors on
+``cuda:0``) and the current HIP stream. There is no CPU path: if the compiled
+library is missing, importing this package raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libals.so")
+
+ALS_OK, ALS_ERR_INVALID_ARG, ALS_ERR_BAD_MATRIX, ALS_ERR_OUT_OF_MEMORY, ALS_ERR_HIP, \
+    ALS_ERR_NOT_SPD = range(6)
+ALS_ROWS_USERS, ALS_ROWS_ITEMS = 0, 1
+_SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
+          ALS_ROWS_USERS: ALS_ROWS_USERS, ALS_ROWS_ITEMS: ALS_ROWS_ITEMS}
+
+EXPORTS = ("als_create", "als_half_sweep", "als_rmse", "als_flagged_rows", "als_get_csc",
+           "als_plan_stats", "als_set_profiling", "als_get_profile", "als_destroy",
+           "als_status_str", "als_last_error")
+
+PHASES = ("gram", "cholesky", "residual", "reduce")
+
+
+class ALSError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class Tuning(ctypes.Structure):
+    _fields_ = [("hub_threshold", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+    st = ctypes.c_int
+    lib.als_create.argtypes = [ctypes.POINTER(P), i64, i64, i64, P, P, P, i32, P,
+                               ctypes.POINTER(Tuning)]
+    lib.als_create.restype = st
+    lib.als_half_sweep.argtypes = [P, st, P, f32, P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_half_sweep.restype = st
+    lib.als_rmse.argtypes = [P, P, P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_rmse.restype = st
+    lib.als_flagged_rows.argtypes = [P]
+    lib.als_flagged_rows.restype = i64
+    lib.als_get_csc.argtypes = [P, P, P, P]
+    lib.als_get_csc.restype = st
+    lib.als_plan_stats.argtypes = [P, st, P, i32]
+    lib.als_plan_stats.restype = st
+    lib.als_set_profiling.argtypes = [P, i32]
+    lib.als_set_profiling.restype = st
+    lib.als_get_profile.argtypes = [P, i32, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_int64)]
+    lib.als_get_profile.restype = st
+    lib.als_destroy.argtypes = [P]
+    lib.als_destroy.restype = None
+    lib.als_status_str.argtypes = [st]
+    lib.als_status_str.restype = ctypes.c_char_p
+    lib.als_last_error.argtypes = [P]
+    lib.als_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load_library()
+
+
+def _np_ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dev_ptr(t, D, rows, name):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous float32")
+    if tuple(t.shape) != (rows, D):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {(rows, D)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class ALS:
+    """One rating matrix (CSR by user) and one factor width D on the current HIP device."""
+
+    def __init__(self, n_users, n_items, row_ptr, col, val, D, stream=None, tuning=None):
+        import torch
+
+        row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int64)
+        col = np.ascontiguousarray(col, dtype=np.int32)
+        val = np.ascontiguousarray(val, dtype=np.uint8)
+        self.M, self.N, self.D = int(n_users), int(n_items), int(D)
+        self.nnz = int(col.size)
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        tun = None
+        if tuning is not None:
+            tun = Tuning(int(tuning.get("hub_threshold", 0)), int(tuning.get("chunk", 0)),
+                         int(tuning.get("workspace_bytes", 0)))
+        h = ctypes.c_void_p()
+        s = lib.als_create(ctypes.byref(h), self.M, self.N, self.nnz, _np_ptr(row_ptr),
+                           _np_ptr(col), _np_ptr(val), self.D, ctypes.c_void_p(stream.cuda_stream),
+                           ctypes.byref(tun) if tun is not None else None)
+        if s != ALS_OK:
+            raise ALSError(s, lib.als_last_error(None).decode())
+        self._h = h
+
+    def _check(self, s):
+        if s != ALS_OK:
+            raise ALSError(s, lib.als_last_error(self._h).decode())
+
+    def half_sweep(self, side, fixed, lam, out, rmse=False, allow_flagged=False):
+        """Solve the rows of ``side`` ("users" or "items") into ``out`` with ``fixed`` held.
+
+        ``out`` must hold the previous iterate (rows without ratings and flagged rows
+        keep it). Returns the RMSE of the new state if ``rmse`` else None."""
+        sd = _SIDES[side]
+        users = sd == ALS_ROWS_USERS
+        n_rows, n_fixed = (self.M, self.N) if users else (self.N, self.M)
+        fp = _dev_ptr(fixed, self.D, n_fixed, "fixed")
+        op = _dev_ptr(out, self.D, n_rows, "out")
+        r = ctypes.c_double(0.0)
+        s = lib.als_half_sweep(self._h, sd, fp, float(lam), op, ctypes.byref(r) if rmse else None)
+        if s == ALS_ERR_NOT_SPD and allow_flagged:
+            return r.value
+        self._check(s)
+        return r.value if rmse else None
+
+    def rmse(self, U, V):
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        r = ctypes.c_double(0.0)
+        self._check(lib.als_rmse(self._h, up, vp, ctypes.byref(r)))
+        return r.value
+
+    def flagged_rows(self):
+        return int(lib.als_flagged_rows(self._h))
+
+    def csc(self):
+        col_ptr = np.empty(self.N + 1, dtype=np.int64)
+        row_idx = np.empty(max(self.nnz, 1), dtype=np.int32)
+        vt = np.empty(max(self.nnz, 1), dtype=np.uint8)
+        self._check(lib.als_get_csc(self._h, _np_ptr(col_ptr), _np_ptr(row_idx), _np_ptr(vt)))
+        return col_ptr, row_idx[: self.nnz], vt[: self.nnz]
+
+    def plan_stats(self, side):
+        out = np.zeros(6, dtype=np.int64)
+        self._check(lib.als_plan_stats(self._h, _SIDES[side], _np_ptr(out), 6))
+        keys = ("rows_with_ratings", "split_rows", "work_items", "batches", "max_degree",
+                "workspace_bytes")
+        return dict(zip(keys, (int(v) for v in out)))
+
+    def set_profiling(self, on=True):
+        self._check(lib.als_set_profiling(self._h, 1 if on else 0))
+
+    def profile(self):
+        res = {}
+        for i, name in enumerate(PHASES):
+            ms = ctypes.c_double(0.0)
+            n = ctypes.c_int64(0)
+            self._check(lib.als_get_profile(self._h, i, ctypes.byref(ms), ctypes.byref(n)))
+            res[name] = (ms.value, n.value)
+        return res
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib.als_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()

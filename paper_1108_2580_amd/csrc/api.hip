@@ -1,0 +1,595 @@
+// Host side of libals: the C ABI declared in include/als.h.
+//
+// als_create validates the user-major CSR, copies it to the device, builds the
+// item-major copy on the device (layout.hip) and plans both sides: rows with
+// ratings are ordered by descending degree (largest work first), rows above
+// the hub threshold are cut into fixed-size chunks, and every row or chunk
+// becomes a work item with its own workspace slot. A half-sweep then runs, per
+// batch of slots, the Gram kernel over the batch's items and the Cholesky
+// kernel over the batch's rows, followed by the residual and reduction
+// kernels for the RMSE of the new state.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/als.h"
+#include "internal.h"
+
+using als::RowTask;
+using als::WorkItem;
+
+namespace {
+
+constexpr int32_t kDefaultHubThreshold = 8192;
+constexpr int32_t kDefaultChunk = 4096;
+constexpr int64_t kDefaultWorkspace = 48LL << 30;
+// cap on the block-by-column count table of the device transpose
+constexpr int64_t kCscTableEntries = 1LL << 29;
+
+struct Batch {
+  int64_t item_off, n_items, row_off, n_rows, n_slots;
+};
+
+struct SidePlan {
+  int64_t n_rows = 0;          // rows of this side
+  int64_t rows_with = 0;       // rows with at least one rating
+  int64_t split_rows = 0;      // rows cut into chunks
+  int64_t max_deg = 0;
+  int64_t max_slots = 0;       // largest batch, in slots
+  std::vector<Batch> batches;
+  std::vector<WorkItem> items;  // host copy, batch-major
+  std::vector<RowTask> rows;
+  WorkItem *d_items = nullptr;
+  RowTask *d_rows = nullptr;
+};
+
+struct ProfEvent {
+  int phase;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct als_ctx {
+  int64_t M = 0, N = 0, nnz = 0;
+  int32_t D = 0, DP = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  als_tuning tune{};
+  std::vector<int64_t> h_row_ptr, h_col_ptr;
+  int64_t *d_row_ptr = nullptr;
+  int32_t *d_col = nullptr;
+  uint8_t *d_val = nullptr;
+  int64_t *d_col_ptr = nullptr;
+  int32_t *d_row_idx = nullptr;
+  uint8_t *d_val_t = nullptr;
+  SidePlan plan[2];
+  float *d_ws = nullptr;
+  size_t ws_bytes = 0;
+  double *d_sse_items = nullptr;
+  double *d_partials = nullptr;
+  double *d_sse_total = nullptr;
+  int32_t *d_flag = nullptr;
+  double *h_sse = nullptr;   // pinned
+  int32_t *h_flag = nullptr; // pinned
+  std::string err;
+  bool profiling = false;
+  std::vector<ProfEvent> prof_pending;
+  std::vector<hipEvent_t> ev_pool;
+  double prof_ms[4] = {0, 0, 0, 0};
+  int64_t prof_n[4] = {0, 0, 0, 0};
+};
+
+namespace {
+
+thread_local std::string g_create_err;
+
+als_status fail(als_ctx *ctx, als_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf; else g_create_err = buf;
+  return st;
+}
+
+#define HIP_OR_FAIL(ctx, call)                                                              \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail((ctx), e_ == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP,    \
+                  "%s failed: %s", #call, hipGetErrorString(e_));                           \
+  } while (0)
+
+template <typename T>
+hipError_t dalloc(T **p, int64_t n) {
+  *p = nullptr;
+  return hipMalloc((void **)p, sizeof(T) * (size_t)std::max<int64_t>(n, 1));
+}
+
+template <typename T>
+void dfree(T *&p) {
+  if (p) (void)hipFree((void *)p);
+  p = nullptr;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) == hipSuccess && prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+// Degree-ordered schedule of one side with hub rows split into chunks.
+als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr) {
+  const int64_t n_rows = (int64_t)ptr.size() - 1;
+  P = SidePlan();
+  P.n_rows = n_rows;
+  std::vector<int32_t> order;
+  order.reserve(n_rows);
+  for (int64_t s = 0; s < n_rows; ++s) {
+    const int64_t d = ptr[s + 1] - ptr[s];
+    if (d > 0) order.push_back((int32_t)s);
+    P.max_deg = std::max(P.max_deg, d);
+  }
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return ptr[a + 1] - ptr[a] > ptr[b + 1] - ptr[b];
+  });
+  P.rows_with = (int64_t)order.size();
+  const int64_t hub = ctx->tune.hub_threshold, chunk = ctx->tune.chunk;
+  const size_t slot_bytes = als::slot_floats_rt(ctx->DP) * sizeof(float);
+  const int64_t cap = std::max<int64_t>(1, ctx->tune.workspace_bytes / (int64_t)slot_bytes);
+  const int64_t max_chunks = P.max_deg > hub ? (P.max_deg + chunk - 1) / chunk : 1;
+  if (max_chunks > cap)
+    return fail(ctx, ALS_ERR_INVALID_ARG,
+                "workspace of %lld bytes holds %lld slots; a split row needs %lld",
+                (long long)ctx->tune.workspace_bytes, (long long)cap, (long long)max_chunks);
+  Batch cur{0, 0, 0, 0, 0};
+  for (int32_t s : order) {
+    const int64_t d = ptr[s + 1] - ptr[s];
+    const int64_t nch = d > hub ? (d + chunk - 1) / chunk : 1;
+    if (nch > 1) ++P.split_rows;
+    if (cur.n_slots + nch > cap) {
+      P.batches.push_back(cur);
+      cur = Batch{(int64_t)P.items.size(), 0, (int64_t)P.rows.size(), 0, 0};
+    }
+    RowTask rt;
+    rt.slot0 = cur.n_slots;
+    rt.deg = d;
+    rt.row = s;
+    rt.nslots = (int32_t)nch;
+    P.rows.push_back(rt);
+    for (int64_t k = 0; k < nch; ++k) {
+      WorkItem it;
+      it.start = ptr[s] + k * (nch > 1 ? chunk : 0);
+      it.len = (int32_t)(nch > 1 ? std::min<int64_t>(chunk, d - k * chunk) : d);
+      it.row = s;
+      it.slot = cur.n_slots + k;
+      P.items.push_back(it);
+    }
+    cur.n_items += nch;
+    cur.n_rows += 1;
+    cur.n_slots += nch;
+  }
+  if (cur.n_rows > 0) P.batches.push_back(cur);
+  for (const Batch &b : P.batches) P.max_slots = std::max(P.max_slots, b.n_slots);
+  HIP_OR_FAIL(ctx, dalloc(&P.d_items, (int64_t)P.items.size()));
+  HIP_OR_FAIL(ctx, dalloc(&P.d_rows, (int64_t)P.rows.size()));
+  if (!P.items.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_items, P.items.data(), sizeof(WorkItem) * P.items.size(),
+                               hipMemcpyHostToDevice));
+  if (!P.rows.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_rows, P.rows.data(), sizeof(RowTask) * P.rows.size(),
+                               hipMemcpyHostToDevice));
+  return ALS_OK;
+}
+
+void free_ctx(als_ctx *c) {
+  if (!c) return;
+  DeviceGuard g(c->device);
+  dfree(c->d_row_ptr);
+  dfree(c->d_col);
+  dfree(c->d_val);
+  dfree(c->d_col_ptr);
+  dfree(c->d_row_idx);
+  dfree(c->d_val_t);
+  for (auto &P : c->plan) {
+    dfree(P.d_items);
+    dfree(P.d_rows);
+  }
+  dfree(c->d_ws);
+  dfree(c->d_sse_items);
+  dfree(c->d_partials);
+  dfree(c->d_sse_total);
+  dfree(c->d_flag);
+  if (c->h_sse) (void)hipHostFree(c->h_sse);
+  if (c->h_flag) (void)hipHostFree(c->h_flag);
+  for (auto &pe : c->prof_pending) {
+    (void)hipEventDestroy(pe.a);
+    (void)hipEventDestroy(pe.b);
+  }
+  for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+  delete c;
+}
+
+// ---- optional per-phase timing -------------------------------------------------------
+
+hipEvent_t take_event(als_ctx *c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct PhaseTimer {
+  als_ctx *c;
+  int phase;
+  hipEvent_t a = nullptr;
+  PhaseTimer(als_ctx *ctx, int ph) : c(ctx), phase(ph) {
+    if (c->profiling && (a = take_event(c))) (void)hipEventRecord(a, c->stream);
+  }
+  ~PhaseTimer() {
+    if (!a) return;
+    hipEvent_t b = take_event(c);
+    if (!b) return;
+    (void)hipEventRecord(b, c->stream);
+    c->prof_pending.push_back(ProfEvent{phase, a, b});
+  }
+};
+
+als_status collect_profile(als_ctx *c) {
+  if (c->prof_pending.empty()) return ALS_OK;
+  HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+  for (auto &pe : c->prof_pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, pe.a, pe.b) == hipSuccess) {
+      c->prof_ms[pe.phase] += ms;
+      c->prof_n[pe.phase] += 1;
+    }
+    c->ev_pool.push_back(pe.a);
+    c->ev_pool.push_back(pe.b);
+  }
+  c->prof_pending.clear();
+  return ALS_OK;
+}
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+  const char *pa = (const char *)a, *pb = (const char *)b;
+  return pa < pb + nb && pb < pa + na;
+}
+
+// Residual pass over a side's items + fixed-order reduction into d_sse_total.
+als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, const uint8_t *val,
+                         const float *F, const float *X) {
+  const int64_t n_items = (int64_t)P.items.size();
+  {
+    PhaseTimer t(c, 2);
+    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_items, n_items, idx, val, F, X, c->D,
+                                     c->d_sse_items, c->stream));
+  }
+  {
+    PhaseTimer t(c, 3);
+    HIP_OR_FAIL(c, als::launch_reduce(c->d_sse_items, n_items, c->d_partials, c->d_sse_total,
+                                      c->stream));
+  }
+  return ALS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *als_status_str(als_status s) {
+  switch (s) {
+    case ALS_OK: return "ok";
+    case ALS_ERR_INVALID_ARG: return "invalid argument";
+    case ALS_ERR_BAD_MATRIX: return "invalid rating matrix";
+    case ALS_ERR_OUT_OF_MEMORY: return "out of memory";
+    case ALS_ERR_HIP: return "HIP runtime error";
+    case ALS_ERR_NOT_SPD: return "some rows were not positive definite and were left unchanged";
+  }
+  return "unknown status";
+}
+
+const char *als_last_error(const als_ctx *ctx) {
+  return ctx ? ctx->err.c_str() : g_create_err.c_str();
+}
+
+als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t nnz,
+                      const int64_t *row_ptr, const int32_t *col_idx, const uint8_t *ratings,
+                      int32_t D, void *hip_stream, const als_tuning *tuning) {
+  g_create_err.clear();
+  if (!out) return fail(nullptr, ALS_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (n_users < 1 || n_items < 1 || n_users >= (1LL << 31) || n_items >= (1LL << 31))
+    return fail(nullptr, ALS_ERR_INVALID_ARG, "matrix shape %lld x %lld out of range",
+                (long long)n_users, (long long)n_items);
+  if (nnz < 0 || nnz >= (1LL << 31))
+    return fail(nullptr, ALS_ERR_INVALID_ARG, "nnz %lld out of range", (long long)nnz);
+  if (D < 1 || D > 128) return fail(nullptr, ALS_ERR_INVALID_ARG, "D = %d outside [1, 128]", D);
+  if (!row_ptr || (nnz > 0 && (!col_idx || !ratings)))
+    return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL host array");
+  // ---- A1: validation of the CSR ----
+  if (row_ptr[0] != 0) return fail(nullptr, ALS_ERR_BAD_MATRIX, "row_ptr[0] = %lld, expected 0",
+                                   (long long)row_ptr[0]);
+  if (row_ptr[n_users] != nnz)
+    return fail(nullptr, ALS_ERR_BAD_MATRIX, "row_ptr[n_users] = %lld, expected nnz = %lld",
+                (long long)row_ptr[n_users], (long long)nnz);
+  for (int64_t u = 0; u < n_users; ++u) {
+    if (row_ptr[u + 1] < row_ptr[u] || row_ptr[u + 1] > nnz)
+      return fail(nullptr, ALS_ERR_BAD_MATRIX, "row_ptr decreases or exceeds nnz at row %lld",
+                  (long long)u);
+  }
+  for (int64_t u = 0; u < n_users; ++u) {
+    const int64_t a = row_ptr[u], b = row_ptr[u + 1];
+    int64_t prev = -1;
+    for (int64_t p = a; p < b; ++p) {
+      const int64_t cidx = col_idx[p];
+      if (cidx < 0 || cidx >= n_items)
+        return fail(nullptr, ALS_ERR_BAD_MATRIX, "column %lld out of range at position %lld",
+                    (long long)cidx, (long long)p);
+      if (cidx <= prev)
+        return fail(nullptr, ALS_ERR_BAD_MATRIX,
+                    "columns not strictly increasing in row %lld (duplicate or unsorted)",
+                    (long long)u);
+      prev = cidx;
+    }
+  }
+  als_ctx *c = new (std::nothrow) als_ctx();
+  if (!c) return fail(nullptr, ALS_ERR_OUT_OF_MEMORY, "host allocation failed");
+  c->M = n_users;
+  c->N = n_items;
+  c->nnz = nnz;
+  c->D = D;
+  c->DP = als::padded_width(D);
+  c->stream = (hipStream_t)hip_stream;
+  c->tune.hub_threshold = kDefaultHubThreshold;
+  c->tune.chunk = kDefaultChunk;
+  c->tune.workspace_bytes = kDefaultWorkspace;
+  if (tuning) {
+    if (tuning->hub_threshold < 0 || tuning->chunk < 0 || tuning->workspace_bytes < 0) {
+      delete c;
+      return fail(nullptr, ALS_ERR_INVALID_ARG, "negative tuning value");
+    }
+    if (tuning->hub_threshold) c->tune.hub_threshold = tuning->hub_threshold;
+    if (tuning->chunk) c->tune.chunk = tuning->chunk;
+    if (tuning->workspace_bytes) c->tune.workspace_bytes = tuning->workspace_bytes;
+  }
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return fail(nullptr, ALS_ERR_HIP, "no HIP device");
+  }
+  auto bail = [&](als_status st) {
+    g_create_err = c->err;
+    free_ctx(c);
+    return st;
+  };
+#define CK(call)                                                                            \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) {                                                                 \
+      fail(c, e_ == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP,              \
+           "%s failed: %s", #call, hipGetErrorString(e_));                                  \
+      return bail(e_ == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP);         \
+    }                                                                                       \
+  } while (0)
+
+  c->h_row_ptr.assign(row_ptr, row_ptr + n_users + 1);
+  CK(dalloc(&c->d_row_ptr, n_users + 1));
+  CK(dalloc(&c->d_col, nnz));
+  CK(dalloc(&c->d_val, nnz));
+  CK(dalloc(&c->d_col_ptr, n_items + 1));
+  CK(dalloc(&c->d_row_idx, nnz));
+  CK(dalloc(&c->d_val_t, nnz));
+  CK(hipMemcpyAsync(c->d_row_ptr, row_ptr, sizeof(int64_t) * (n_users + 1),
+                    hipMemcpyHostToDevice, c->stream));
+  if (nnz > 0) {
+    CK(hipMemcpyAsync(c->d_col, col_idx, sizeof(int32_t) * nnz, hipMemcpyHostToDevice,
+                      c->stream));
+    CK(hipMemcpyAsync(c->d_val, ratings, nnz, hipMemcpyHostToDevice, c->stream));
+  }
+  // ---- A2: device transpose ----
+  {
+    int64_t max_blk = std::max<int64_t>(1, kCscTableEntries / n_items);
+    int64_t rows_per_blk = std::max<int64_t>(16, (n_users + max_blk - 1) / max_blk);
+    int64_t nblk = (n_users + rows_per_blk - 1) / rows_per_blk;
+    int32_t *cnt = nullptr;
+    int64_t *tot = nullptr;
+    CK(dalloc(&cnt, nblk * n_items));
+    CK(dalloc(&tot, n_items));
+    hipError_t e = als::launch_csc_build(c->d_row_ptr, c->d_col, c->d_val, n_users, n_items,
+                                         rows_per_blk, nblk, cnt, tot, c->d_col_ptr,
+                                         c->d_row_idx, c->d_val_t, c->stream);
+    hipError_t e2 = hipStreamSynchronize(c->stream);
+    (void)hipFree(cnt);
+    (void)hipFree(tot);
+    CK(e);
+    CK(e2);
+  }
+  c->h_col_ptr.resize(n_items + 1);
+  CK(hipMemcpy(c->h_col_ptr.data(), c->d_col_ptr, sizeof(int64_t) * (n_items + 1),
+               hipMemcpyDeviceToHost));
+  if (c->h_col_ptr[n_items] != nnz) {
+    fail(c, ALS_ERR_HIP, "device transpose produced %lld entries, expected %lld",
+         (long long)c->h_col_ptr[n_items], (long long)nnz);
+    return bail(ALS_ERR_HIP);
+  }
+  // ---- A3: schedules ----
+  als_status st = build_plan(c, c->plan[ALS_ROWS_USERS], c->h_row_ptr);
+  if (st != ALS_OK) return bail(st);
+  st = build_plan(c, c->plan[ALS_ROWS_ITEMS], c->h_col_ptr);
+  if (st != ALS_OK) return bail(st);
+  int64_t max_slots = 0, max_items = 0;
+  for (auto &P : c->plan) {
+    max_slots = std::max(max_slots, P.max_slots);
+    max_items = std::max(max_items, (int64_t)P.items.size());
+  }
+  c->ws_bytes = (size_t)max_slots * als::slot_floats_rt(c->DP) * sizeof(float);
+  CK(dalloc(&c->d_ws, (int64_t)(c->ws_bytes / sizeof(float))));
+  CK(dalloc(&c->d_sse_items, max_items));
+  CK(dalloc(&c->d_partials, als::reduce_partials(max_items)));
+  CK(dalloc(&c->d_sse_total, 1));
+  CK(dalloc(&c->d_flag, 1));
+  CK(hipHostMalloc((void **)&c->h_sse, sizeof(double), hipHostMallocDefault));
+  CK(hipHostMalloc((void **)&c->h_flag, sizeof(int32_t), hipHostMallocDefault));
+  *c->h_flag = 0;
+  *c->h_sse = 0.0;
+  CK(als::launch_fill_i32(c->d_flag, 1, 0, c->stream));
+  CK(hipStreamSynchronize(c->stream));
+#undef CK
+  *out = c;
+  return ALS_OK;
+}
+
+als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
+                          float *out_factors, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "side %d is not ALS_ROWS_USERS or ALS_ROWS_ITEMS",
+                (int)side);
+  if (!fixed_factors || !out_factors) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL factor buffer");
+  if (!std::isfinite(lambda) || lambda < 0.f)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (((uintptr_t)fixed_factors & 15) || ((uintptr_t)out_factors & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  const bool users = side == ALS_ROWS_USERS;
+  const int64_t n_rows = users ? ctx->M : ctx->N, n_fixed = users ? ctx->N : ctx->M;
+  if (overlap(fixed_factors, sizeof(float) * n_fixed * ctx->D, out_factors,
+              sizeof(float) * n_rows * ctx->D))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "out_factors overlaps fixed_factors");
+  DeviceGuard g(ctx->device);
+  const SidePlan &P = ctx->plan[side];
+  const int32_t *idx = users ? ctx->d_col : ctx->d_row_idx;
+  const uint8_t *val = users ? ctx->d_val : ctx->d_val_t;
+  HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
+  for (const Batch &b : P.batches) {
+    {
+      PhaseTimer t(ctx, 0);
+      HIP_OR_FAIL(ctx, als::launch_gram(ctx->DP, P.d_items + b.item_off, b.n_items, idx, val,
+                                        fixed_factors, ctx->D, ctx->d_ws, ctx->stream));
+    }
+    {
+      PhaseTimer t(ctx, 1);
+      HIP_OR_FAIL(ctx, als::launch_chol(ctx->DP, P.d_rows + b.row_off, b.n_rows, ctx->d_ws,
+                                        ctx->D, lambda, out_factors, ctx->d_flag, ctx->stream));
+    }
+  }
+  als_status st = residual_pass(ctx, P, idx, val, fixed_factors, out_factors);
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
+                                  hipMemcpyDeviceToHost, ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, ctx->stream));
+  if (ctx->profiling && (st = collect_profile(ctx)) != ALS_OK) return st;
+  if (rmse_out) {
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
+    if (*ctx->h_flag > 0)
+      return fail(ctx, ALS_ERR_NOT_SPD, "%d rows were flagged and left unchanged",
+                  (int)*ctx->h_flag);
+  }
+  return ALS_OK;
+}
+
+als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!U || !V || !rmse_out) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  DeviceGuard g(ctx->device);
+  const SidePlan &P = ctx->plan[ALS_ROWS_USERS];
+  als_status st = residual_pass(ctx, P, ctx->d_col, ctx->d_val, V, U);
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
+                                  hipMemcpyDeviceToHost, ctx->stream));
+  if (ctx->profiling && (st = collect_profile(ctx)) != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
+  return ALS_OK;
+}
+
+int64_t als_flagged_rows(als_ctx *ctx) {
+  if (!ctx) return -1;
+  DeviceGuard g(ctx->device);
+  if (hipStreamSynchronize(ctx->stream) != hipSuccess) return -1;
+  return *ctx->h_flag;
+}
+
+als_status als_get_csc(als_ctx *ctx, int64_t *col_ptr, int32_t *row_idx, uint8_t *ratings) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!col_ptr || (ctx->nnz > 0 && (!row_idx || !ratings)))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL host buffer");
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpy(col_ptr, ctx->d_col_ptr, sizeof(int64_t) * (ctx->N + 1),
+                             hipMemcpyDeviceToHost));
+  if (ctx->nnz > 0) {
+    HIP_OR_FAIL(ctx, hipMemcpy(row_idx, ctx->d_row_idx, sizeof(int32_t) * ctx->nnz,
+                               hipMemcpyDeviceToHost));
+    HIP_OR_FAIL(ctx, hipMemcpy(ratings, ctx->d_val_t, ctx->nnz, hipMemcpyDeviceToHost));
+  }
+  return ALS_OK;
+}
+
+als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  if ((side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS) || !out || n < 0)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "bad argument");
+  const SidePlan &P = ctx->plan[side];
+  const int64_t v[6] = {P.rows_with, P.split_rows, (int64_t)P.items.size(),
+                        (int64_t)P.batches.size(), P.max_deg, (int64_t)ctx->ws_bytes};
+  for (int32_t i = 0; i < n && i < 6; ++i) out[i] = v[i];
+  return ALS_OK;
+}
+
+als_status als_set_profiling(als_ctx *ctx, int32_t enable) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->profiling = enable != 0;
+  if (enable) {
+    for (int i = 0; i < 4; ++i) {
+      ctx->prof_ms[i] = 0.0;
+      ctx->prof_n[i] = 0;
+    }
+  }
+  return ALS_OK;
+}
+
+als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  if (phase < 0 || phase > 3 || !total_ms || !launches)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "bad argument");
+  als_status st = collect_profile(ctx);
+  if (st != ALS_OK) return st;
+  *total_ms = ctx->prof_ms[phase];
+  *launches = ctx->prof_n[phase];
+  return ALS_OK;
+}
+
+void als_destroy(als_ctx *ctx) {
+  if (!ctx) return;
+  {
+    DeviceGuard g(ctx->device);
+    (void)hipStreamSynchronize(ctx->stream);
+  }
+  free_ctx(ctx);
+}
+
+}  // extern "C"

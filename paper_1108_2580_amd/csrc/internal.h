@@ -1,0 +1,66 @@
+// Internal declarations shared by the HIP translation units of libals.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace als {
+
+// One unit of Gram work: a whole row, or one chunk of a split ("hub") row.
+struct WorkItem {
+  int64_t start;  // first rating of the item, offset into the side's idx/val arrays
+  int64_t slot;   // workspace slot of the item's partial normal equations (batch local)
+  int32_t len;    // ratings in the item
+  int32_t row;    // solved-side row the item belongs to
+};
+static_assert(sizeof(WorkItem) == 24, "WorkItem layout");
+
+// One row to factor and solve: sums nslots consecutive workspace slots.
+struct RowTask {
+  int64_t slot0;  // batch-local slot of the row's first item
+  int64_t deg;    // n_s, number of ratings of the row
+  int32_t row;
+  int32_t nslots;
+};
+static_assert(sizeof(RowTask) == 24, "RowTask layout");
+
+// Padded factor width: D rounded up to the 16-wide MFMA tile.
+inline int padded_width(int D) { return ((D + 15) / 16) * 16; }
+// Upper-triangle 16x16 tiles of a DP x DP Gram matrix.
+constexpr int num_tiles(int dp) { return (dp / 16) * (dp / 16 + 1) / 2; }
+// Floats per workspace slot: the tiles in MFMA register order, then the right-hand side.
+constexpr size_t slot_floats(int dp) { return (size_t)num_tiles(dp) * 256 + (size_t)dp; }
+inline size_t slot_floats_rt(int dp) { int t = dp / 16; return (size_t)(t * (t + 1) / 2) * 256 + dp; }
+
+// ---- launchers (each returns the launch's hipError_t) ----------------------------------
+
+// Column-major copy of a CSR matrix, built on the device (layout.hip).
+// scratch_cnt: int32[nblk * n_cols]; tot: int64[n_cols]; col_ptr: int64[n_cols + 1].
+hipError_t launch_csc_build(const int64_t *row_ptr, const int32_t *col, const uint8_t *val,
+                            int64_t n_rows, int64_t n_cols, int64_t rows_per_blk, int64_t nblk,
+                            int32_t *scratch_cnt, int64_t *tot, int64_t *col_ptr,
+                            int32_t *row_idx, uint8_t *val_t, hipStream_t s);
+
+// Partial normal equations of each work item into its workspace slot (gram.hip).
+hipError_t launch_gram(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
+                       const uint8_t *val, const float *F, int D, float *ws, hipStream_t s);
+
+// Sum of a row's slots + lambda*n_s*I, Cholesky, two triangular solves (cholesky.hip).
+hipError_t launch_chol(int dp, const RowTask *rows, int64_t n_rows, const float *ws, int D,
+                       float lam, float *out, int32_t *flag_count, hipStream_t s);
+
+// Per-item sums of squared residuals with the rows of X against F (residual.hip).
+hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
+                        const uint8_t *val, const float *F, const float *X, int D,
+                        double *sse_items, hipStream_t s);
+
+// Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].
+int64_t reduce_partials(int64_t n);
+hipError_t launch_reduce(const double *v, int64_t n, double *partials, double *out,
+                         hipStream_t s);
+
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+
+}  // namespace als
