@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""ALS half-sweep throughput on one MI355X.
+
+One step = one ALS sweep of the paper's order (Sec. 2.2): the item half-sweep
+(solve V with U fixed) then the user half-sweep (solve U with V fixed), each
+with its residual pass for the training RMSE. The metric is ratings per
+second per half-sweep, 2 * nnz * steps / elapsed, with the rating matrix and
+factors resident in HBM before the timed region.
+
+Default workload: the full-scale synthetic stand-in for the paper's data set
+(1,000,990 users x 624,961 items x 262,810,175 ratings, Sec. 1), D = 20,
+lambda = 0.065 weighted by n_s. --config 4 selects the same matrix at D = 100.
+
+Besides the JSON line's throughput, the script reports the roofline position
+of the dominant kernel (HIP-event timing of every launch over the timed
+region) and the fp64 CPU oracle's throughput on a bounded sample of the same
+half-sweep on this host's cores.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+MFMA_F32_PEAK_TFS = 157.3  # MI355X dense fp32 matrix
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gram_traffic.txt")
+GRAM_SRC = os.path.join(ROOT, "paper_1108_2580_amd", "csrc", "gram.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target duration of the CPU oracle sample (0 disables it)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def copy_calibration():
+    import torch
+
+    n = 1 << 30  # 1 Gi floats = 4 GiB each way
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 copies of {4 * n} bytes")
+
+
+def gram_source_hash():
+    return hashlib.sha256(open(GRAM_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per Gram launch from the committed rocprofv3 counter summary, if it was
+    taken on the current Gram kernel source for this workload; else None."""
+    try:
+        for line in open(TRAFFIC_FILE):
+            if line.startswith("TRAFFIC_JSON "):
+                rec = json.loads(line[len("TRAFFIC_JSON "):])
+                if rec.get("gram_src_sha256_16") == gram_source_hash() and \
+                        rec.get("workload") == workload_name:
+                    return rec.get("bytes_per_launch")
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(r, side_fixed, target_s):
+    """fp64 oracle on a seeded random sample of the user half-sweep's rows."""
+    import numpy as np
+
+    import oracle
+
+    deg = np.diff(r.row_ptr)
+    rows = np.flatnonzero(deg > 0)
+    rng = np.random.default_rng(12345)
+    perm = rows[rng.permutation(rows.size)]
+    csum = np.cumsum(deg[perm])
+    val = r.val.astype(np.float64)
+    fixed = side_fixed.astype(np.float64)
+    threads = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+
+    def run(n_ratings):
+        k = int(np.searchsorted(csum, n_ratings)) + 1
+        k = min(k, perm.size)
+        sel = np.sort(perm[:k])
+        t0 = time.perf_counter()
+        oracle.solve_rows(sel, r.row_ptr, r.col, val, fixed, r.lam, threads=threads)
+        dt = time.perf_counter() - t0
+        return int(deg[sel].sum()), k, dt
+
+    n0, k0, t0 = run(max(1, r.nnz // 500))
+    rate0 = n0 / max(t0, 1e-9)
+    target = min(r.nnz, int(rate0 * target_s))
+    n1, k1, t1 = run(target)
+    return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
+                sample=(f"user half-sweep of {r.name}: {k1} of {rows.size} rows (seeded random), "
+                        f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the half-sweep would shard by rows with an all-gather of the solved side).",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    import workload
+    from paper_1108_2580_amd import ALS
+
+    t_gen = time.perf_counter()
+    r = workload.make_config(args.config)
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    log(f"generated {r.name}: nnz={r.nnz} in {time.perf_counter() - t_gen:.1f} s")
+    dev = torch.device("cuda:0")
+    t_c = time.perf_counter()
+    als = ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D)
+    log(f"als_create (validation, upload, device CSC, schedules): "
+        f"{time.perf_counter() - t_c:.1f} s; users {als.plan_stats('users')} "
+        f"items {als.plan_stats('items')}")
+    U = torch.from_numpy(U0).to(dev)
+    V = torch.from_numpy(V0).to(dev)
+    for w in range(args.warmup):
+        als.half_sweep("items", U, r.lam, V)
+        als.half_sweep("users", V, r.lam, U)
+        torch.cuda.synchronize()
+        log(f"warmup {w + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    als.set_profiling(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        als.half_sweep("items", U, r.lam, V)
+        als.half_sweep("users", V, r.lam, U)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = als.profile()
+    als.set_profiling(False)
+    elapsed = t1 - t0
+    rmse = als.rmse(U, V)
+    log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
+        f"rmse {rmse:.6f}")
+
+    value = 2.0 * r.nnz * args.steps / elapsed
+    halves = 2 * args.steps
+    rows_with = als.plan_stats("users")["rows_with_ratings"] + \
+        als.plan_stats("items")["rows_with_ratings"]
+    gram_ms, gram_n = prof["gram"]
+    dominant = max(prof, key=lambda k: prof[k][0])
+    if r.D <= 32:
+        # gathered bytes per rating (index, rating, fixed row) and 8 B per solved row
+        alg = halves * r.nnz * (5 + 4 * r.D) + args.steps * rows_with * 8
+        achieved = alg / (gram_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=achieved / HBM_PEAK_GBS)
+    else:
+        # SYRK-convention Gram flops plus the right-hand side
+        alg = halves * r.nnz * (r.D * (r.D + 1) + 2 * r.D)
+        achieved = alg / (gram_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=achieved, peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s",
+                    frac=achieved / MFMA_F32_PEAK_TFS)
+    roof.update(kernel="k_gram", launches=gram_n, avg_launch_ms=gram_ms / max(gram_n, 1),
+                alg_per_launch=alg / max(gram_n, 1),
+                traffic=measured_traffic(r.name), dominant_phase=dominant)
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
+        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds)
+        log(f"cpu baseline: {cpu}")
+
+    out = {
+        "metric": "ALS ratings/sec per half-sweep",
+        "value": value,
+        "unit": "ratings/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": r.name, "n_users": r.M, "n_items": r.N, "nnz": r.nnz, "D": r.D,
+                   "lambda": r.lam, "step": "item half-sweep + user half-sweep",
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
+        "rmse": rmse,
+    }
+    print(json.dumps(out), flush=True)
+    als.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -133,9 +133,11 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
 
 /*
  * Optional per-phase timing with HIP events recorded on the context's stream
- * around each kernel launch. When enabled, every half-sweep synchronises the
- * stream at its end to collect the event times. Phases: 0 = Gram (partial
- * normal equations), 1 = Cholesky + solve, 2 = residual, 3 = reduction.
+ * around each kernel launch (no synchronisation while enabled). Phases:
+ * 0 = Gram (partial normal equations), 1 = Cholesky + solve, 2 = residual,
+ * 3 = reduction. als_set_profiling(ctx, 1) resets the totals;
+ * als_get_profile synchronises the stream, folds the recorded events into the
+ * totals and returns the summed milliseconds and launch count of one phase.
  */
 als_status als_set_profiling(als_ctx *ctx, int32_t enable);
 als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches);

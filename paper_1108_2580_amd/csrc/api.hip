@@ -496,7 +496,6 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
                                   hipMemcpyDeviceToHost, ctx->stream));
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, ctx->stream));
-  if (ctx->profiling && (st = collect_profile(ctx)) != ALS_OK) return st;
   if (rmse_out) {
     HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
     *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
@@ -519,7 +518,6 @@ als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_o
   if (st != ALS_OK) return st;
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
-  if (ctx->profiling && (st = collect_profile(ctx)) != ALS_OK) return st;
   HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
   *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
   return ALS_OK;
@@ -562,6 +560,8 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) 
 
 als_status als_set_profiling(als_ctx *ctx, int32_t enable) {
   if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  als_status st = collect_profile(ctx);
+  if (st != ALS_OK) return st;
   ctx->profiling = enable != 0;
   if (enable) {
     for (int i = 0; i < 4; ++i) {

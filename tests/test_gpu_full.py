@@ -1,0 +1,95 @@
+"""Full-size workloads (the half-sweep at the shapes bench.py times), checked against the
+fp64 oracle on sampled rows (the oracle solves them one by one) and on properties that
+hold at any size.
+
+Sampled rows per side: the 16 largest (split rows included), the 16 smallest and 224
+seeded random rows. Bars as in the small tests: relative row error <= 1e-4 after one
+half-sweep from the seeded initial factors; the RMSE returned with the half-sweep equals
+the fp64 residual of the GPU state within 1e-5; no row flagged; every factor finite.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workload
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+ROW_TOL = 1e-4
+RMSE_TOL = 1e-5
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda:0")
+
+
+def sample_rows(ptr, seed):
+    deg = np.diff(ptr)
+    rows = np.flatnonzero(deg > 0)
+    order = rows[np.argsort(-deg[rows], kind="stable")]
+    rng = np.random.default_rng(seed)
+    pick = np.concatenate([order[:16], order[-16:], rng.choice(rows, 224, replace=False)])
+    return np.unique(pick)
+
+
+@pytest.mark.parametrize("k", [3, 4, 5])
+def test_full_first_half_sweep_sampled(k):
+    from paper_1108_2580_amd import ALS
+
+    r = workload.make_config(k)
+    log(f"{r.name}: nnz={r.nnz} D={r.D}")
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    val = r.val.astype(np.float64)
+    csc = oracle.transpose(r.row_ptr, r.col, val, r.N)
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        log(f"  plans users {als.plan_stats('users')} items {als.plan_stats('items')}")
+        for side, fixed, prev, (p, i, v) in (("items", U0, V0, csc),
+                                             ("users", V0, U0, (r.row_ptr, r.col, val))):
+            out = dev(prev)
+            rm = als.half_sweep(side, dev(fixed), r.lam, out, rmse=True)
+            assert als.flagged_rows() == 0
+            xg = out.cpu().numpy()
+            assert np.isfinite(xg).all()
+            rows = sample_rows(p, seed=k)
+            xo, fl = oracle.solve_rows(rows, p, i, v, fixed, r.lam)
+            assert (fl == 0).all()
+            rel = np.linalg.norm(xg[rows] - xo, axis=1) / np.linalg.norm(xo, axis=1)
+            log(f"  {side}: {rows.size} sampled rows (max degree {np.diff(p)[rows].max()}), "
+                f"rel p50={np.median(rel):.2e} max={rel.max():.2e}")
+            assert rel.max() <= ROW_TOL
+            if side == "items":
+                ro = oracle.rmse(r.row_ptr, r.col, val, U0, xg)
+            else:
+                ro = oracle.rmse(r.row_ptr, r.col, val, xg, V0)
+            log(f"  {side}: rmse gpu {rm:.9f} oracle on the GPU state {ro:.9f}")
+            assert abs(rm - ro) <= RMSE_TOL
+
+
+@pytest.mark.skipif(os.environ.get("ALS_FULL_TRAJECTORY") != "1",
+                    reason="several minutes of host fp64 work; set ALS_FULL_TRAJECTORY=1")
+@pytest.mark.timeout(1500)
+def test_full_d20_free_running_rmse():
+    """Five free-running sweeps at full size, D = 20: GPU fp32 vs oracle fp64 trajectory."""
+    from paper_1108_2580_amd import ALS
+
+    r = workload.make_config(3)
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    t = oracle.Trajectory(r.M, r.N, r.row_ptr, r.col, r.val, U0, V0, r.lam)
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        U, V = dev(U0), dev(V0)
+        for sweep in range(1, r.sweeps + 1):
+            als.half_sweep("items", U, r.lam, V)
+            rm = als.half_sweep("users", V, r.lam, U, rmse=True)
+            t.sweep()
+            ro = t.rmse()
+            log(f"  sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
+        assert abs(rm - ro) <= RMSE_TOL

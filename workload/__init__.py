@@ -279,14 +279,22 @@ _MAKERS = {"uniform": _make_uniform, "zipf": _make_zipf, "kddcup": _make_kddcup,
            "itemhub": _make_itemhub}
 
 
-def make_config(k: int) -> Ratings:
-    """Generate configuration k (1..5) deterministically."""
+_MEMO = {}
+
+
+def make_config(k: int, memo: bool = True) -> Ratings:
+    """Generate configuration k (1..5) deterministically.
+
+    With ``memo`` the matrix is kept for the life of the process (the two
+    full-scale configurations share one matrix)."""
     cfg = CONFIGS[k]
     mk = cfg.get("matrix_of", k)
     seed = data_seed(mk)
     cache = os.environ.get("ALS_WORKLOAD_CACHE")
     path = os.path.join(cache, f"matrix_{mk}.npz") if cache else None
-    if path and os.path.exists(path):
+    if memo and mk in _MEMO:
+        ptr, col, val = _MEMO[mk]
+    elif path and os.path.exists(path):
         z = np.load(path)
         ptr, col, val = z["row_ptr"], z["col"], z["val"]
     else:
@@ -294,6 +302,9 @@ def make_config(k: int) -> Ratings:
         if path:
             os.makedirs(cache, exist_ok=True)
             np.savez(path, row_ptr=ptr, col=col, val=val)
+    if memo:
+        _MEMO.clear()
+        _MEMO[mk] = (ptr, col, val)
     return Ratings(name=cfg["name"], M=cfg["M"], N=cfg["N"], row_ptr=ptr, col=col, val=val,
                    D=cfg["D"], lam=cfg["lam"], sweeps=cfg["sweeps"], data_seed=seed,
                    init_seed=data_seed(k) + 1000)
