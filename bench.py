@@ -29,8 +29,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 MFMA_F32_PEAK_TFS = 157.3  # MI355X dense fp32 matrix
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gram_traffic.txt")
-GRAM_SRC = os.path.join(ROOT, "paper_1108_2580_amd", "csrc", "gram.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rows_traffic.txt")
+GRAM_SRC = os.path.join(ROOT, "paper_1108_2580_amd", "csrc", "rowsolve.hip")
 
 
 def parse():
@@ -67,13 +67,13 @@ def gram_source_hash():
 
 
 def measured_traffic(workload_name):
-    """HBM bytes per Gram launch from the committed rocprofv3 counter summary, if it was
-    taken on the current Gram kernel source for this workload; else None."""
+    """HBM bytes per row-kernel launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source for this workload; else None."""
     try:
         for line in open(TRAFFIC_FILE):
             if line.startswith("TRAFFIC_JSON "):
                 rec = json.loads(line[len("TRAFFIC_JSON "):])
-                if rec.get("gram_src_sha256_16") == gram_source_hash() and \
+                if rec.get("src_sha256_16") == gram_source_hash() and \
                         rec.get("workload") == workload_name:
                     return rec.get("bytes_per_launch")
     except OSError:
@@ -158,30 +158,37 @@ def main():
     prof = als.profile()
     als.set_profiling(False)
     elapsed = t1 - t0
+    rmse_in = als.rmse_in()
     rmse = als.rmse(U, V)
     log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
-        f"rmse {rmse:.6f}")
+        f"rmse entering last half-sweep {rmse_in:.6f}, final {rmse:.6f}")
 
     value = 2.0 * r.nnz * args.steps / elapsed
     halves = 2 * args.steps
     rows_with = als.plan_stats("users")["rows_with_ratings"] + \
         als.plan_stats("items")["rows_with_ratings"]
-    gram_ms, gram_n = prof["gram"]
+    # the fused row kernel and the chunk kernel of split rows share the gather work
+    k_ms = prof["rows"][0] + prof["chunks"][0]
+    k_n = prof["rows"][1]
     dominant = max(prof, key=lambda k: prof[k][0])
-    if r.D <= 32:
-        # gathered bytes per rating (index, rating, fixed row) and 8 B per solved row
-        alg = halves * r.nnz * (5 + 4 * r.D) + args.steps * rows_with * 8
-        achieved = alg / (gram_ms * 1e-3) / 1e9
+    D = r.D
+    if D <= 32:
+        # per rating: index, rating and the gathered fixed row; per solved row: the row
+        # pointer, the entering value and the written solution
+        alg = halves * r.nnz * (5 + 4 * D) + args.steps * rows_with * (8 + 8 * D)
+        achieved = alg / (k_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=achieved / HBM_PEAK_GBS)
     else:
-        # SYRK-convention Gram flops plus the right-hand side
-        alg = halves * r.nnz * (r.D * (r.D + 1) + 2 * r.D)
-        achieved = alg / (gram_ms * 1e-3) / 1e12
+        # SYRK-convention Gram flops, right-hand side and residual dot per rating, plus the
+        # Cholesky factorisation and two triangular solves per row
+        alg = halves * r.nnz * (D * (D + 1) + 4 * D) + \
+            args.steps * rows_with * (D ** 3 / 3.0 + 2.0 * D * D)
+        achieved = alg / (k_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=achieved, peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s",
                     frac=achieved / MFMA_F32_PEAK_TFS)
-    roof.update(kernel="k_gram", launches=gram_n, avg_launch_ms=gram_ms / max(gram_n, 1),
-                alg_per_launch=alg / max(gram_n, 1),
+    roof.update(kernel="k_rows+k_gram_chunks", launches=k_n, avg_launch_ms=k_ms / max(k_n, 1),
+                alg_per_launch=alg / max(k_n, 1),
                 traffic=measured_traffic(r.name), dominant_phase=dominant)
 
     cpu = None
@@ -210,6 +217,7 @@ def main():
         "cpu_baseline": cpu,
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
         "rmse": rmse,
+        "rmse_entering_last_half_sweep": rmse_in,
     }
     print(json.dumps(out), flush=True)
     als.close()

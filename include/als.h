@@ -88,7 +88,10 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
                       int32_t D, void *hip_stream, const als_tuning *tuning);
 
 /*
- * One half-sweep (paper Sec. 2.2).
+ * One half-sweep (paper Sec. 2.2). The pass that gathers each row's fixed
+ * vectors also accumulates the squared residuals of the state entering the
+ * half-sweep (out_factors' previous content against fixed_factors); that
+ * training RMSE (Sec. 4.1) is read back with als_last_rmse_in.
  *   side           ALS_ROWS_USERS: fixed = V [n_items x D], out = U [n_users x D].
  *                  ALS_ROWS_ITEMS: fixed = U [n_users x D], out = V [n_items x D].
  *   fixed_factors  device fp32, row-major, read only.
@@ -105,6 +108,13 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
  */
 als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
                           float *out_factors, double *rmse_out);
+
+/*
+ * Training RMSE of the state that entered the most recent half-sweep (for a
+ * sweep items-then-users: the RMSE after the previous half-sweep).
+ * Synchronises the stream. ALS_ERR_INVALID_ARG if no half-sweep has run.
+ */
+als_status als_last_rmse_in(als_ctx *ctx, double *rmse_in);
 
 /*
  * Training RMSE of (U, V): sqrt(sum over stored ratings of (r - u_u . v_i)^2 / nnz).
@@ -126,16 +136,17 @@ als_status als_get_csc(als_ctx *ctx, int64_t *col_ptr, int32_t *row_idx, uint8_t
 
 /*
  * Schedule statistics of one side, for tests and reports. out receives up to
- * n values in this order: rows with ratings, rows split into chunks, work
- * items (rows + chunks), batches, largest degree, workspace bytes per batch.
+ * n values in this order: rows with ratings, rows split into chunks, chunks,
+ * batches, largest degree, workspace bytes per batch.
  */
 als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
 
 /*
  * Optional per-phase timing with HIP events recorded on the context's stream
  * around each kernel launch (no synchronisation while enabled). Phases:
- * 0 = Gram (partial normal equations), 1 = Cholesky + solve, 2 = residual,
- * 3 = reduction. als_set_profiling(ctx, 1) resets the totals;
+ * 0 = staging of the fixed side, 1 = normal equations of split-row chunks,
+ * 2 = fused row solve (normal equations, Cholesky, solves), 3 = new-state
+ * residual pass, 4 = reductions. als_set_profiling(ctx, 1) resets the totals;
  * als_get_profile synchronises the stream, folds the recorded events into the
  * totals and returns the summed milliseconds and launch count of one phase.
  */

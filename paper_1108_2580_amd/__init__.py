@@ -21,11 +21,12 @@ ALS_ROWS_USERS, ALS_ROWS_ITEMS = 0, 1
 _SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
           ALS_ROWS_USERS: ALS_ROWS_USERS, ALS_ROWS_ITEMS: ALS_ROWS_ITEMS}
 
-EXPORTS = ("als_create", "als_half_sweep", "als_rmse", "als_flagged_rows", "als_get_csc",
+EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_flagged_rows",
+           "als_get_csc",
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_destroy",
            "als_status_str", "als_last_error")
 
-PHASES = ("gram", "cholesky", "residual", "reduce")
+PHASES = ("stage", "chunks", "rows", "residual", "reduce")
 
 
 class ALSError(RuntimeError):
@@ -51,6 +52,8 @@ def _load_library():
     lib.als_create.restype = st
     lib.als_half_sweep.argtypes = [P, st, P, f32, P, ctypes.POINTER(ctypes.c_double)]
     lib.als_half_sweep.restype = st
+    lib.als_last_rmse_in.argtypes = [P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_last_rmse_in.restype = st
     lib.als_rmse.argtypes = [P, P, P, ctypes.POINTER(ctypes.c_double)]
     lib.als_rmse.restype = st
     lib.als_flagged_rows.argtypes = [P]
@@ -139,6 +142,12 @@ class ALS:
         self._check(s)
         return r.value if rmse else None
 
+    def rmse_in(self):
+        """RMSE of the state that entered the last half-sweep (computed in its gather pass)."""
+        r = ctypes.c_double(0.0)
+        self._check(lib.als_last_rmse_in(self._h, ctypes.byref(r)))
+        return r.value
+
     def rmse(self, U, V):
         up = _dev_ptr(U, self.D, self.M, "U")
         vp = _dev_ptr(V, self.D, self.N, "V")
@@ -159,7 +168,7 @@ class ALS:
     def plan_stats(self, side):
         out = np.zeros(6, dtype=np.int64)
         self._check(lib.als_plan_stats(self._h, _SIDES[side], _np_ptr(out), 6))
-        keys = ("rows_with_ratings", "split_rows", "work_items", "batches", "max_degree",
+        keys = ("rows_with_ratings", "split_rows", "chunks", "batches", "max_degree",
                 "workspace_bytes")
         return dict(zip(keys, (int(v) for v in out)))
 

@@ -2,12 +2,12 @@
 //
 // als_create validates the user-major CSR, copies it to the device, builds the
 // item-major copy on the device (layout.hip) and plans both sides: rows with
-// ratings are ordered by descending degree (largest work first), rows above
-// the hub threshold are cut into fixed-size chunks, and every row or chunk
-// becomes a work item with its own workspace slot. A half-sweep then runs, per
-// batch of slots, the Gram kernel over the batch's items and the Cholesky
-// kernel over the batch's rows, followed by the residual and reduction
-// kernels for the RMSE of the new state.
+// ratings are ordered by descending degree (largest work first); rows above
+// the hub threshold are cut into fixed-size chunks whose partial normal
+// equations go to workspace slots. A half-sweep stages the fixed side into a
+// padded copy, then runs per batch the chunk kernel and the fused row kernel
+// (rowsolve.hip), and reduces the entering-state squared residuals; the
+// new-state RMSE is an extra residual pass (residual.hip), run on request.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -33,21 +33,28 @@ constexpr int64_t kDefaultWorkspace = 48LL << 30;
 constexpr int64_t kCscTableEntries = 1LL << 29;
 
 struct Batch {
-  int64_t item_off, n_items, row_off, n_rows, n_slots;
+  int64_t chunk_off, n_chunks;  // chunks of split rows
+  int64_t row_off, n_rows;      // row tasks
+  int64_t n_slots;              // workspace slots used by the batch's chunks
 };
 
 struct SidePlan {
-  int64_t n_rows = 0;          // rows of this side
-  int64_t rows_with = 0;       // rows with at least one rating
-  int64_t split_rows = 0;      // rows cut into chunks
+  int64_t n_rows = 0;       // rows of this side
+  int64_t rows_with = 0;    // rows with at least one rating
+  int64_t split_rows = 0;   // rows cut into chunks
   int64_t max_deg = 0;
-  int64_t max_slots = 0;       // largest batch, in slots
+  int64_t max_slots = 0;    // largest batch, in slots
   std::vector<Batch> batches;
-  std::vector<WorkItem> items;  // host copy, batch-major
-  std::vector<RowTask> rows;
-  WorkItem *d_items = nullptr;
+  std::vector<WorkItem> chunks;  // chunks of split rows, batch-major
+  std::vector<RowTask> rows;     // every row with ratings, batch-major, descending degree
+  std::vector<WorkItem> pieces;  // residual work: the chunks, then whole unsplit rows
+  WorkItem *d_chunks = nullptr;
   RowTask *d_rows = nullptr;
+  WorkItem *d_pieces = nullptr;
+  int64_t n_sse() const { return (int64_t)(chunks.size() + rows.size()); }
 };
+
+constexpr int kPhases = 5;  // stage, chunks, rows, residual, reduce
 
 struct ProfEvent {
   int phase;
@@ -72,18 +79,22 @@ struct als_ctx {
   SidePlan plan[2];
   float *d_ws = nullptr;
   size_t ws_bytes = 0;
-  double *d_sse_items = nullptr;
+  float *d_fpad = nullptr;       // staged fixed side [max(M, N) x DP]
+  double *d_sse_items = nullptr; // per chunk / row / piece squared residuals
   double *d_partials = nullptr;
-  double *d_sse_total = nullptr;
+  double *d_sse_in = nullptr;    // entering-state SSE of the last half-sweep
+  double *d_sse_total = nullptr; // SSE of the last residual pass
   int32_t *d_flag = nullptr;
-  double *h_sse = nullptr;   // pinned
-  int32_t *h_flag = nullptr; // pinned
+  double *h_sse = nullptr;    // pinned
+  double *h_sse_in = nullptr; // pinned
+  int32_t *h_flag = nullptr;  // pinned
+  int last_side = -1;
   std::string err;
   bool profiling = false;
   std::vector<ProfEvent> prof_pending;
   std::vector<hipEvent_t> ev_pool;
-  double prof_ms[4] = {0, 0, 0, 0};
-  int64_t prof_n[4] = {0, 0, 0, 0};
+  double prof_ms[kPhases] = {0, 0, 0, 0, 0};
+  int64_t prof_n[kPhases] = {0, 0, 0, 0, 0};
 };
 
 namespace {
@@ -150,7 +161,7 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   const int64_t hub = ctx->tune.hub_threshold, chunk = ctx->tune.chunk;
   const size_t slot_bytes = als::slot_floats_rt(ctx->DP) * sizeof(float);
   const int64_t cap = std::max<int64_t>(1, ctx->tune.workspace_bytes / (int64_t)slot_bytes);
-  const int64_t max_chunks = P.max_deg > hub ? (P.max_deg + chunk - 1) / chunk : 1;
+  const int64_t max_chunks = P.max_deg > hub ? (P.max_deg + chunk - 1) / chunk : 0;
   if (max_chunks > cap)
     return fail(ctx, ALS_ERR_INVALID_ARG,
                 "workspace of %lld bytes holds %lld slots; a split row needs %lld",
@@ -158,39 +169,55 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   Batch cur{0, 0, 0, 0, 0};
   for (int32_t s : order) {
     const int64_t d = ptr[s + 1] - ptr[s];
-    const int64_t nch = d > hub ? (d + chunk - 1) / chunk : 1;
-    if (nch > 1) ++P.split_rows;
+    const int64_t nch = d > hub ? (d + chunk - 1) / chunk : 0;
+    if (nch > 0) ++P.split_rows;
     if (cur.n_slots + nch > cap) {
       P.batches.push_back(cur);
-      cur = Batch{(int64_t)P.items.size(), 0, (int64_t)P.rows.size(), 0, 0};
+      cur = Batch{(int64_t)P.chunks.size(), 0, (int64_t)P.rows.size(), 0, 0};
     }
     RowTask rt;
+    rt.start = ptr[s];
     rt.slot0 = cur.n_slots;
-    rt.deg = d;
     rt.row = s;
+    rt.deg = (int32_t)d;
     rt.nslots = (int32_t)nch;
+    rt.pad = 0;
     P.rows.push_back(rt);
     for (int64_t k = 0; k < nch; ++k) {
       WorkItem it;
-      it.start = ptr[s] + k * (nch > 1 ? chunk : 0);
-      it.len = (int32_t)(nch > 1 ? std::min<int64_t>(chunk, d - k * chunk) : d);
+      it.start = ptr[s] + k * chunk;
+      it.len = (int32_t)std::min<int64_t>(chunk, d - k * chunk);
       it.row = s;
       it.slot = cur.n_slots + k;
-      P.items.push_back(it);
+      P.chunks.push_back(it);
     }
-    cur.n_items += nch;
+    cur.n_chunks += nch;
     cur.n_rows += 1;
     cur.n_slots += nch;
   }
   if (cur.n_rows > 0) P.batches.push_back(cur);
   for (const Batch &b : P.batches) P.max_slots = std::max(P.max_slots, b.n_slots);
-  HIP_OR_FAIL(ctx, dalloc(&P.d_items, (int64_t)P.items.size()));
+  P.pieces = P.chunks;
+  for (const RowTask &rt : P.rows) {
+    if (rt.nslots > 0) continue;
+    WorkItem it;
+    it.start = rt.start;
+    it.len = rt.deg;
+    it.row = rt.row;
+    it.slot = 0;
+    P.pieces.push_back(it);
+  }
+  HIP_OR_FAIL(ctx, dalloc(&P.d_chunks, (int64_t)P.chunks.size()));
   HIP_OR_FAIL(ctx, dalloc(&P.d_rows, (int64_t)P.rows.size()));
-  if (!P.items.empty())
-    HIP_OR_FAIL(ctx, hipMemcpy(P.d_items, P.items.data(), sizeof(WorkItem) * P.items.size(),
+  HIP_OR_FAIL(ctx, dalloc(&P.d_pieces, (int64_t)P.pieces.size()));
+  if (!P.chunks.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_chunks, P.chunks.data(), sizeof(WorkItem) * P.chunks.size(),
                                hipMemcpyHostToDevice));
   if (!P.rows.empty())
     HIP_OR_FAIL(ctx, hipMemcpy(P.d_rows, P.rows.data(), sizeof(RowTask) * P.rows.size(),
+                               hipMemcpyHostToDevice));
+  if (!P.pieces.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_pieces, P.pieces.data(), sizeof(WorkItem) * P.pieces.size(),
                                hipMemcpyHostToDevice));
   return ALS_OK;
 }
@@ -205,15 +232,19 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_row_idx);
   dfree(c->d_val_t);
   for (auto &P : c->plan) {
-    dfree(P.d_items);
+    dfree(P.d_chunks);
     dfree(P.d_rows);
+    dfree(P.d_pieces);
   }
   dfree(c->d_ws);
+  dfree(c->d_fpad);
   dfree(c->d_sse_items);
   dfree(c->d_partials);
+  dfree(c->d_sse_in);
   dfree(c->d_sse_total);
   dfree(c->d_flag);
   if (c->h_sse) (void)hipHostFree(c->h_sse);
+  if (c->h_sse_in) (void)hipHostFree(c->h_sse_in);
   if (c->h_flag) (void)hipHostFree(c->h_flag);
   for (auto &pe : c->prof_pending) {
     (void)hipEventDestroy(pe.a);
@@ -273,18 +304,19 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
   return pa < pb + nb && pb < pa + na;
 }
 
-// Residual pass over a side's items + fixed-order reduction into d_sse_total.
+// New-state residual pass over a side's pieces + fixed-order reduction into
+// d_sse_total; the fixed side must already be staged in d_fpad.
 als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, const uint8_t *val,
-                         const float *F, const float *X) {
-  const int64_t n_items = (int64_t)P.items.size();
+                         const float *X) {
+  const int64_t n = (int64_t)P.pieces.size();
   {
-    PhaseTimer t(c, 2);
-    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_items, n_items, idx, val, F, X, c->D,
+    PhaseTimer t(c, 3);
+    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_pieces, n, idx, val, c->d_fpad, X, c->D,
                                      c->d_sse_items, c->stream));
   }
   {
-    PhaseTimer t(c, 3);
-    HIP_OR_FAIL(c, als::launch_reduce(c->d_sse_items, n_items, c->d_partials, c->d_sse_total,
+    PhaseTimer t(c, 4);
+    HIP_OR_FAIL(c, als::launch_reduce(c->d_sse_items, n, c->d_partials, c->d_sse_total,
                                       c->stream));
   }
   return ALS_OK;
@@ -434,21 +466,25 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   if (st != ALS_OK) return bail(st);
   st = build_plan(c, c->plan[ALS_ROWS_ITEMS], c->h_col_ptr);
   if (st != ALS_OK) return bail(st);
-  int64_t max_slots = 0, max_items = 0;
+  int64_t max_slots = 0, max_sse = 0;
   for (auto &P : c->plan) {
     max_slots = std::max(max_slots, P.max_slots);
-    max_items = std::max(max_items, (int64_t)P.items.size());
+    max_sse = std::max({max_sse, P.n_sse(), (int64_t)P.pieces.size()});
   }
   c->ws_bytes = (size_t)max_slots * als::slot_floats_rt(c->DP) * sizeof(float);
   CK(dalloc(&c->d_ws, (int64_t)(c->ws_bytes / sizeof(float))));
-  CK(dalloc(&c->d_sse_items, max_items));
-  CK(dalloc(&c->d_partials, als::reduce_partials(max_items)));
+  CK(dalloc(&c->d_fpad, std::max(n_users, n_items) * (int64_t)c->DP));
+  CK(dalloc(&c->d_sse_items, max_sse));
+  CK(dalloc(&c->d_partials, als::reduce_partials(max_sse)));
+  CK(dalloc(&c->d_sse_in, 1));
   CK(dalloc(&c->d_sse_total, 1));
   CK(dalloc(&c->d_flag, 1));
   CK(hipHostMalloc((void **)&c->h_sse, sizeof(double), hipHostMallocDefault));
+  CK(hipHostMalloc((void **)&c->h_sse_in, sizeof(double), hipHostMallocDefault));
   CK(hipHostMalloc((void **)&c->h_flag, sizeof(int32_t), hipHostMallocDefault));
   *c->h_flag = 0;
   *c->h_sse = 0.0;
+  *c->h_sse_in = 0.0;
   CK(als::launch_fill_i32(c->d_flag, 1, 0, c->stream));
   CK(hipStreamSynchronize(c->stream));
 #undef CK
@@ -477,32 +513,60 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
   const SidePlan &P = ctx->plan[side];
   const int32_t *idx = users ? ctx->d_col : ctx->d_row_idx;
   const uint8_t *val = users ? ctx->d_val : ctx->d_val_t;
+  const int64_t n_chunks = (int64_t)P.chunks.size();
   HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
+  {
+    PhaseTimer t(ctx, 0);
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(fixed_factors, n_fixed, ctx->D, ctx->DP,
+                                             ctx->d_fpad, ctx->stream));
+  }
   for (const Batch &b : P.batches) {
-    {
-      PhaseTimer t(ctx, 0);
-      HIP_OR_FAIL(ctx, als::launch_gram(ctx->DP, P.d_items + b.item_off, b.n_items, idx, val,
-                                        fixed_factors, ctx->D, ctx->d_ws, ctx->stream));
+    if (b.n_chunks > 0) {
+      PhaseTimer t(ctx, 1);
+      HIP_OR_FAIL(ctx, als::launch_gram_chunks(ctx->DP, P.d_chunks + b.chunk_off, b.n_chunks, idx,
+                                               val, ctx->d_fpad, out_factors, ctx->D, ctx->d_ws,
+                                               ctx->d_sse_items + b.chunk_off, ctx->stream));
     }
     {
-      PhaseTimer t(ctx, 1);
-      HIP_OR_FAIL(ctx, als::launch_chol(ctx->DP, P.d_rows + b.row_off, b.n_rows, ctx->d_ws,
-                                        ctx->D, lambda, out_factors, ctx->d_flag, ctx->stream));
+      PhaseTimer t(ctx, 2);
+      HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val,
+                                        ctx->d_fpad, ctx->d_ws, ctx->D, lambda, out_factors,
+                                        ctx->d_sse_items + n_chunks + b.row_off, ctx->d_flag,
+                                        ctx->stream));
     }
   }
-  als_status st = residual_pass(ctx, P, idx, val, fixed_factors, out_factors);
-  if (st != ALS_OK) return st;
-  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
+  {
+    PhaseTimer t(ctx, 4);
+    HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_sse_items, P.n_sse(), ctx->d_partials,
+                                        ctx->d_sse_in, ctx->stream));
+  }
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse_in, ctx->d_sse_in, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, ctx->stream));
+  ctx->last_side = side;
   if (rmse_out) {
+    als_status st = residual_pass(ctx, P, idx, val, out_factors);
+    if (st != ALS_OK) return st;
+    HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
+                                    hipMemcpyDeviceToHost, ctx->stream));
     HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
     *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
     if (*ctx->h_flag > 0)
       return fail(ctx, ALS_ERR_NOT_SPD, "%d rows were flagged and left unchanged",
                   (int)*ctx->h_flag);
   }
+  return ALS_OK;
+}
+
+als_status als_last_rmse_in(als_ctx *ctx, double *rmse_in) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!rmse_in) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (ctx->last_side < 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no half-sweep has run yet");
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  *rmse_in = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse_in / (double)ctx->nnz) : 0.0;
   return ALS_OK;
 }
 
@@ -514,7 +578,12 @@ als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_o
     return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
   DeviceGuard g(ctx->device);
   const SidePlan &P = ctx->plan[ALS_ROWS_USERS];
-  als_status st = residual_pass(ctx, P, ctx->d_col, ctx->d_val, V, U);
+  {
+    PhaseTimer t(ctx, 0);
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(V, ctx->N, ctx->D, ctx->DP, ctx->d_fpad,
+                                             ctx->stream));
+  }
+  als_status st = residual_pass(ctx, P, ctx->d_col, ctx->d_val, U);
   if (st != ALS_OK) return st;
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
@@ -552,7 +621,7 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) 
   if ((side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS) || !out || n < 0)
     return fail(ctx, ALS_ERR_INVALID_ARG, "bad argument");
   const SidePlan &P = ctx->plan[side];
-  const int64_t v[6] = {P.rows_with, P.split_rows, (int64_t)P.items.size(),
+  const int64_t v[6] = {P.rows_with, P.split_rows, (int64_t)P.chunks.size(),
                         (int64_t)P.batches.size(), P.max_deg, (int64_t)ctx->ws_bytes};
   for (int32_t i = 0; i < n && i < 6; ++i) out[i] = v[i];
   return ALS_OK;
@@ -564,7 +633,7 @@ als_status als_set_profiling(als_ctx *ctx, int32_t enable) {
   if (st != ALS_OK) return st;
   ctx->profiling = enable != 0;
   if (enable) {
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kPhases; ++i) {
       ctx->prof_ms[i] = 0.0;
       ctx->prof_n[i] = 0;
     }
@@ -574,7 +643,7 @@ als_status als_set_profiling(als_ctx *ctx, int32_t enable) {
 
 als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches) {
   if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
-  if (phase < 0 || phase > 3 || !total_ms || !launches)
+  if (phase < 0 || phase >= kPhases || !total_ms || !launches)
     return fail(ctx, ALS_ERR_INVALID_ARG, "bad argument");
   als_status st = collect_profile(ctx);
   if (st != ALS_OK) return st;

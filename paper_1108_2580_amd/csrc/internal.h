@@ -17,14 +17,17 @@ struct WorkItem {
 };
 static_assert(sizeof(WorkItem) == 24, "WorkItem layout");
 
-// One row to factor and solve: sums nslots consecutive workspace slots.
+// One row to solve. A row with nslots == 0 builds its normal equations from its
+// ratings [start, start + deg); a split row sums nslots workspace slots.
 struct RowTask {
-  int64_t slot0;  // batch-local slot of the row's first item
-  int64_t deg;    // n_s, number of ratings of the row
+  int64_t start;  // first rating of the row
+  int64_t slot0;  // batch-local slot of the row's first chunk (split rows)
   int32_t row;
+  int32_t deg;    // n_s, number of ratings of the row
   int32_t nslots;
+  int32_t pad;
 };
-static_assert(sizeof(RowTask) == 24, "RowTask layout");
+static_assert(sizeof(RowTask) == 32, "RowTask layout");
 
 // Padded factor width: D rounded up to the 16-wide MFMA tile.
 inline int padded_width(int D) { return ((D + 15) / 16) * 16; }
@@ -43,17 +46,25 @@ hipError_t launch_csc_build(const int64_t *row_ptr, const int32_t *col, const ui
                             int32_t *scratch_cnt, int64_t *tot, int64_t *col_ptr,
                             int32_t *row_idx, uint8_t *val_t, hipStream_t s);
 
-// Partial normal equations of each work item into its workspace slot (gram.hip).
-hipError_t launch_gram(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
-                       const uint8_t *val, const float *F, int D, float *ws, hipStream_t s);
+// Copy of the fixed factors [n x D] into a zero-padded [n x DP] buffer (rowsolve.hip).
+hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *Fp, hipStream_t s);
 
-// Sum of a row's slots + lambda*n_s*I, Cholesky, two triangular solves (cholesky.hip).
-hipError_t launch_chol(int dp, const RowTask *rows, int64_t n_rows, const float *ws, int D,
-                       float lam, float *out, int32_t *flag_count, hipStream_t s);
+// Partial normal equations of the chunks of split rows, into their workspace
+// slots, with the chunks' entering-state squared residuals (rowsolve.hip).
+hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
+                              const uint8_t *val, const float *Fp, const float *Xold, int D,
+                              float *ws, double *sse, hipStream_t s);
 
-// Per-item sums of squared residuals with the rows of X against F (residual.hip).
+// Fused per-row normal equations, regularisation, Cholesky and solves; X is read
+// (entering state) and overwritten in place (rowsolve.hip).
+hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
+                       const uint8_t *val, const float *Fp, const float *ws, int D, float lam,
+                       float *X, double *sse, int32_t *flag, hipStream_t s);
+
+// Per-item sums of squared residuals with the rows of X against the staged
+// fixed side Fp (row stride DP) (residual.hip).
 hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
-                        const uint8_t *val, const float *F, const float *X, int D,
+                        const uint8_t *val, const float *Fp, const float *X, int D,
                         double *sse_items, hipStream_t s);
 
 // Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].

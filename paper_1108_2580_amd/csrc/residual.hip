@@ -1,9 +1,11 @@
-// Residuals of the predictions r_hat = x_s . f_j (Sec. 2.2) for the RMSE of
-// Sec. 4.1. One wavefront per work item (row or chunk of a split row); each
-// lane takes whole ratings: it gathers the fixed row f_j (float4 loads when D
-// is a multiple of 4), forms the dot product with x_s (held in LDS), and
-// accumulates (r - x_s . f_j)^2 in fp64. The wavefront total goes to
-// sse_items[item]; a fixed-order reduction over items follows.
+// Residuals of the predictions r_hat = x_s . f_j (Sec. 2.2) of a given state,
+// for the training RMSE of Sec. 4.1 (the standalone pass behind als_rmse and
+// the new-state RMSE of als_half_sweep). One wavefront per work item (row or
+// chunk of a split row); each lane takes whole ratings: it gathers the staged
+// fixed row f_j (row stride DP, 16-byte aligned, zero padded) with float4
+// loads, forms the dot product with x_s (held in LDS), and accumulates
+// (r - x_s . f_j)^2 in fp64. The wavefront total goes to sse_items[item]; a
+// fixed-order reduction over items follows.
 #include "internal.h"
 
 namespace als {
@@ -12,7 +14,7 @@ template <int DP>
 __global__ __launch_bounds__(64) void k_resid(const WorkItem *__restrict__ items,
                                               const int32_t *__restrict__ idx,
                                               const uint8_t *__restrict__ val,
-                                              const float *__restrict__ F,
+                                              const float *__restrict__ Fp,
                                               const float *__restrict__ X, int D,
                                               double *__restrict__ sse_items) {
   __shared__ float xs[DP];
@@ -22,36 +24,23 @@ __global__ __launch_bounds__(64) void k_resid(const WorkItem *__restrict__ items
   __syncthreads();
   const int32_t *__restrict__ ip = idx + it.start;
   const uint8_t *__restrict__ vp = val + it.start;
+  const int D4 = (D + 3) >> 2;
   double acc = 0.0;
-  if ((D & 3) == 0) {
-    const int D4 = D >> 2;
-    for (int q = lane; q < it.len; q += 64) {
-      const float4 *__restrict__ f = reinterpret_cast<const float4 *>(F + (int64_t)ip[q] * D);
-      float dot = 0.f;
+  for (int q = lane; q < it.len; q += 64) {
+    const float4 *__restrict__ f = reinterpret_cast<const float4 *>(Fp + (int64_t)ip[q] * DP);
+    float dot = 0.f;
 #pragma unroll
-      for (int d4 = 0; d4 < DP / 4; ++d4) {
-        if (d4 < D4) {
-          const float4 v = f[d4];
-          dot = fmaf(v.x, xs[4 * d4 + 0], dot);
-          dot = fmaf(v.y, xs[4 * d4 + 1], dot);
-          dot = fmaf(v.z, xs[4 * d4 + 2], dot);
-          dot = fmaf(v.w, xs[4 * d4 + 3], dot);
-        }
+    for (int d4 = 0; d4 < DP / 4; ++d4) {
+      if (d4 < D4) {
+        const float4 v = f[d4];
+        dot = fmaf(v.x, xs[4 * d4 + 0], dot);
+        dot = fmaf(v.y, xs[4 * d4 + 1], dot);
+        dot = fmaf(v.z, xs[4 * d4 + 2], dot);
+        dot = fmaf(v.w, xs[4 * d4 + 3], dot);
       }
-      const double e = (double)vp[q] - (double)dot;
-      acc += e * e;
     }
-  } else {
-    for (int q = lane; q < it.len; q += 64) {
-      const float *__restrict__ f = F + (int64_t)ip[q] * D;
-      float dot = 0.f;
-#pragma unroll
-      for (int d = 0; d < DP; ++d) {
-        if (d < D) dot = fmaf(f[d], xs[d], dot);
-      }
-      const double e = (double)vp[q] - (double)dot;
-      acc += e * e;
-    }
+    const double e = (double)vp[q] - (double)dot;
+    acc = fma(e, e, acc);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
@@ -60,26 +49,26 @@ __global__ __launch_bounds__(64) void k_resid(const WorkItem *__restrict__ items
 
 template <int DP>
 static hipError_t launch_resid_t(const WorkItem *items, int64_t n_items, const int32_t *idx,
-                                 const uint8_t *val, const float *F, const float *X, int D,
+                                 const uint8_t *val, const float *Fp, const float *X, int D,
                                  double *sse_items, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_resid<DP>, dim3((unsigned)n_items), dim3(64), 0, s, items, idx, val, F, X,
+  hipLaunchKernelGGL(k_resid<DP>, dim3((unsigned)n_items), dim3(64), 0, s, items, idx, val, Fp, X,
                      D, sse_items);
   return hipGetLastError();
 }
 
 hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
-                        const uint8_t *val, const float *F, const float *X, int D,
+                        const uint8_t *val, const float *Fp, const float *X, int D,
                         double *sse_items, hipStream_t s) {
   switch (dp) {
-    case 16: return launch_resid_t<16>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 32: return launch_resid_t<32>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 48: return launch_resid_t<48>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 64: return launch_resid_t<64>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 80: return launch_resid_t<80>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 96: return launch_resid_t<96>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 112: return launch_resid_t<112>(items, n_items, idx, val, F, X, D, sse_items, s);
-    case 128: return launch_resid_t<128>(items, n_items, idx, val, F, X, D, sse_items, s);
+    case 16: return launch_resid_t<16>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 32: return launch_resid_t<32>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 48: return launch_resid_t<48>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 64: return launch_resid_t<64>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 80: return launch_resid_t<80>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 96: return launch_resid_t<96>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 112: return launch_resid_t<112>(items, n_items, idx, val, Fp, X, D, sse_items, s);
+    case 128: return launch_resid_t<128>(items, n_items, idx, val, Fp, X, D, sse_items, s);
     default: return hipErrorInvalidValue;
   }
 }

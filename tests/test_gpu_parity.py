@@ -67,10 +67,14 @@ def check_first_half_sweeps(M, N, ptr, col, val, D, lam, U0, V0, tuning=None, la
     """Both sides from the same init: users from V0, items from U0."""
     csr = (ptr, col, val.astype(np.float64))
     csc = oracle.transpose(ptr, col, val, N)
+    rmse0 = oracle.rmse(ptr, col, val, U0, V0)
     with make_als(M, N, ptr, col, val, D, tuning) as als:
         for side, fixed, prev, (p, i, v) in (("users", V0, U0, csr), ("items", U0, V0, csc)):
             log(f"  {label} side={side} D={D}")
             xg, rm = gpu_half(als, side, fixed, prev, lam, rmse=True)
+            rin = als.rmse_in()
+            log(f"    entering-state rmse gpu {rin:.9f} oracle {rmse0:.9f}")
+            assert abs(rin - rmse0) <= RMSE_TOL
             xo, fl = oracle.half_sweep(p, i, v, fixed, lam, prev)
             assert not (fl == 1).any()
             rel = rel_rows(xg, xo)
@@ -144,7 +148,7 @@ def test_widths_with_split_rows_and_batches(D):
     # workspace so that each side runs in several batches
     slot = ((D + 15) // 16)
     slot_bytes = (slot * (slot + 1) // 2 * 256 + slot * 16) * 4
-    tun = dict(hub_threshold=40, chunk=24, workspace_bytes=slot_bytes * 64)
+    tun = dict(hub_threshold=40, chunk=24, workspace_bytes=slot_bytes * 16)
     with make_als(M, N, ptr, col, val, D, tun) as als:
         st_u, st_i = als.plan_stats("users"), als.plan_stats("items")
     log(f"  plan users {st_u} items {st_i}")
@@ -176,9 +180,14 @@ def test_rmse_free_running(k, checks):
     with make_als(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
         U, V = dev(U0), dev(V0)
         for sweep in range(1, max(checks) + 1):
+            r_before = t.rmse()
             als.half_sweep("items", U, r.lam, V)
+            assert abs(als.rmse_in() - r_before) <= RMSE_TOL
+            t.step("items")
+            r_mid = t.rmse()
             rm = als.half_sweep("users", V, r.lam, U, rmse=True)
-            t.sweep()
+            assert abs(als.rmse_in() - r_mid) <= RMSE_TOL
+            t.step("users")
             if sweep in checks:
                 ro = t.rmse()
                 log(f"  {r.name} sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
