@@ -29,8 +29,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 MFMA_F32_PEAK_TFS = 157.3  # MI355X dense fp32 matrix
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rows_traffic.txt")
-GRAM_SRC = os.path.join(ROOT, "paper_1108_2580_amd", "csrc", "rowsolve.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+CSRC = os.path.join(ROOT, "paper_1108_2580_amd", "csrc")
 
 
 def parse():
@@ -62,19 +62,24 @@ def copy_calibration():
     log(f"copy calibration: 3 copies of {4 * n} bytes")
 
 
-def gram_source_hash():
-    return hashlib.sha256(open(GRAM_SRC, "rb").read()).hexdigest()[:16]
+def kernel_source_hash():
+    """Hash of the device sources (the counters are void once any of them changes)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            h.update(open(os.path.join(CSRC, name), "rb").read())
+    return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_name):
-    """HBM bytes per row-kernel launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source for this workload; else None."""
+def measured_traffic(workload_name, kernel):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter
+    summary, if it was taken on the current device sources for this workload; else None."""
     try:
         for line in open(TRAFFIC_FILE):
             if line.startswith("TRAFFIC_JSON "):
                 rec = json.loads(line[len("TRAFFIC_JSON "):])
-                if rec.get("src_sha256_16") == gram_source_hash() and \
-                        rec.get("workload") == workload_name:
+                if rec.get("src_sha256_16") == kernel_source_hash() and \
+                        rec.get("workload") == workload_name and rec.get("kernel") == kernel:
                     return rec.get("bytes_per_launch")
     except OSError:
         pass
@@ -167,29 +172,28 @@ def main():
     halves = 2 * args.steps
     rows_with = als.plan_stats("users")["rows_with_ratings"] + \
         als.plan_stats("items")["rows_with_ratings"]
-    # the fused row kernel and the chunk kernel of split rows share the gather work
-    k_ms = prof["rows"][0] + prof["chunks"][0]
-    k_n = prof["rows"][1]
-    dominant = max(prof, key=lambda k: prof[k][0])
     D = r.D
-    if D <= 32:
-        # per rating: index, rating and the gathered fixed row; per solved row: the row
-        # pointer, the entering value and the written solution
-        alg = halves * r.nnz * (5 + 4 * D) + args.steps * rows_with * (8 + 8 * D)
+    dominant = max(prof, key=lambda k: prof[k][0])
+    if D <= 20:
+        # gather kernel: per rating the index, the rating and the gathered fixed row; per
+        # solved row the row pointer and the entering value
+        k_ms, k_n = prof["gather"]
+        alg = halves * r.nnz * (5 + 4 * D) + args.steps * rows_with * (8 + 4 * D)
         achieved = alg / (k_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS)
+                    frac=achieved / HBM_PEAK_GBS, kernel="k_gram_ne")
     else:
-        # SYRK-convention Gram flops, right-hand side and residual dot per rating, plus the
-        # Cholesky factorisation and two triangular solves per row
+        # fused row kernel + chunk kernel of split rows: SYRK-convention Gram flops, the
+        # right-hand side and residual dot per rating, Cholesky and two solves per row
+        k_ms = prof["solve"][0] + prof["gather"][0]
+        k_n = prof["solve"][1]
         alg = halves * r.nnz * (D * (D + 1) + 4 * D) + \
             args.steps * rows_with * (D ** 3 / 3.0 + 2.0 * D * D)
         achieved = alg / (k_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=achieved, peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s",
-                    frac=achieved / MFMA_F32_PEAK_TFS)
-    roof.update(kernel="k_rows+k_gram_chunks", launches=k_n, avg_launch_ms=k_ms / max(k_n, 1),
-                alg_per_launch=alg / max(k_n, 1),
-                traffic=measured_traffic(r.name), dominant_phase=dominant)
+                    frac=achieved / MFMA_F32_PEAK_TFS, kernel="k_rows+k_gram_chunks")
+    roof.update(launches=k_n, avg_launch_ms=k_ms / max(k_n, 1), alg_per_launch=alg / max(k_n, 1),
+                traffic=measured_traffic(r.name, roof["kernel"]), dominant_phase=dominant)
 
     cpu = None
     if args.cpu_seconds > 0:

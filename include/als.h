@@ -68,7 +68,7 @@ typedef struct {
 
 /*
  * Create a context for one rating matrix and one factor width D.
- *   n_users, n_items  matrix shape (M, N); each >= 1 and < 2^31.
+ *   n_users, n_items  matrix shape (M, N); each >= 1 and < 2^31 - 1.
  *   nnz               number of stored ratings; 0 <= nnz < 2^31.
  *   row_ptr           host int64[n_users + 1]: row_ptr[0] = 0, non-decreasing,
  *                     row_ptr[n_users] = nnz.
@@ -137,16 +137,18 @@ als_status als_get_csc(als_ctx *ctx, int64_t *col_ptr, int32_t *row_idx, uint8_t
 /*
  * Schedule statistics of one side, for tests and reports. out receives up to
  * n values in this order: rows with ratings, rows split into chunks, chunks,
- * batches, largest degree, workspace bytes per batch.
+ * batches, largest degree, workspace bytes per batch, bytes per workspace slot.
  */
 als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
 
 /*
  * Optional per-phase timing with HIP events recorded on the context's stream
  * around each kernel launch (no synchronisation while enabled). Phases:
- * 0 = staging of the fixed side, 1 = normal equations of split-row chunks,
- * 2 = fused row solve (normal equations, Cholesky, solves), 3 = new-state
- * residual pass, 4 = reductions. als_set_profiling(ctx, 1) resets the totals;
+ * 0 = staging of the fixed side; 1 = gather kernels (D <= 20: the normal
+ * equations of every row and chunk; D > 20: those of split-row chunks);
+ * 2 = solve kernels (D <= 20: one row per lane; D > 20: the fused row kernel,
+ * which also builds the normal equations of unsplit rows); 3 = new-state
+ * residual pass; 4 = reductions. als_set_profiling(ctx, 1) resets the totals;
  * als_get_profile synchronises the stream, folds the recorded events into the
  * totals and returns the summed milliseconds and launch count of one phase.
  */

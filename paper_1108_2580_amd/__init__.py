@@ -26,7 +26,7 @@ EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_destroy",
            "als_status_str", "als_last_error")
 
-PHASES = ("stage", "chunks", "rows", "residual", "reduce")
+PHASES = ("stage", "gather", "solve", "residual", "reduce")
 
 
 class ALSError(RuntimeError):
@@ -40,11 +40,11 @@ class Tuning(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_int64)]
 
 
-def _load_library():
-    if not os.path.exists(LIB_PATH):
+def _load_library(path=LIB_PATH):
+    if not os.path.exists(path):
         raise ImportError(
-            f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950) first")
-    lib = ctypes.CDLL(LIB_PATH)
+            f"{path} is not built; run __graft_entry__.build() (hipcc, gfx950) first")
+    lib = ctypes.CDLL(path)
     P, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
     st = ctypes.c_int
     lib.als_create.argtypes = [ctypes.POINTER(P), i64, i64, i64, P, P, P, i32, P,
@@ -166,10 +166,10 @@ class ALS:
         return col_ptr, row_idx[: self.nnz], vt[: self.nnz]
 
     def plan_stats(self, side):
-        out = np.zeros(6, dtype=np.int64)
-        self._check(lib.als_plan_stats(self._h, _SIDES[side], _np_ptr(out), 6))
+        out = np.zeros(7, dtype=np.int64)
+        self._check(lib.als_plan_stats(self._h, _SIDES[side], _np_ptr(out), 7))
         keys = ("rows_with_ratings", "split_rows", "chunks", "batches", "max_degree",
-                "workspace_bytes")
+                "workspace_bytes", "slot_bytes")
         return dict(zip(keys, (int(v) for v in out)))
 
     def set_profiling(self, on=True):

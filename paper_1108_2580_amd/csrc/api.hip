@@ -18,7 +18,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/als.h"
+#include "als.h"
 #include "internal.h"
 
 using als::RowTask;
@@ -33,25 +33,25 @@ constexpr int64_t kDefaultWorkspace = 48LL << 30;
 constexpr int64_t kCscTableEntries = 1LL << 29;
 
 struct Batch {
-  int64_t chunk_off, n_chunks;  // chunks of split rows
-  int64_t row_off, n_rows;      // row tasks
-  int64_t n_slots;              // workspace slots used by the batch's chunks
+  int64_t gitem_off;  // first gather item of the batch
+  int64_t n_gchunks;  // its chunks of split rows (they come first)
+  int64_t n_gitems;   // chunks + unsplit rows
+  int64_t row_off, n_rows;
+  int64_t n_slots;    // workspace slots used by the batch's chunks
 };
 
 struct SidePlan {
   int64_t n_rows = 0;       // rows of this side
   int64_t rows_with = 0;    // rows with at least one rating
   int64_t split_rows = 0;   // rows cut into chunks
+  int64_t n_chunks = 0;
   int64_t max_deg = 0;
   int64_t max_slots = 0;    // largest batch, in slots
   std::vector<Batch> batches;
-  std::vector<WorkItem> chunks;  // chunks of split rows, batch-major
+  std::vector<WorkItem> gitems;  // per batch: chunks of split rows, then unsplit rows
   std::vector<RowTask> rows;     // every row with ratings, batch-major, descending degree
-  std::vector<WorkItem> pieces;  // residual work: the chunks, then whole unsplit rows
-  WorkItem *d_chunks = nullptr;
+  WorkItem *d_gitems = nullptr;
   RowTask *d_rows = nullptr;
-  WorkItem *d_pieces = nullptr;
-  int64_t n_sse() const { return (int64_t)(chunks.size() + rows.size()); }
 };
 
 constexpr int kPhases = 5;  // stage, chunks, rows, residual, reduce
@@ -79,7 +79,9 @@ struct als_ctx {
   SidePlan plan[2];
   float *d_ws = nullptr;
   size_t ws_bytes = 0;
-  float *d_fpad = nullptr;       // staged fixed side [max(M, N) x DP]
+  float *d_fpad = nullptr;       // staged fixed side [(max(M, N) + 1) x DP], last row zero
+  float *d_ne = nullptr;         // packed normal equations, one record per row (narrow D)
+  bool lane_solve = false;       // narrow D: Gram records + one row per lane solve
   double *d_sse_items = nullptr; // per chunk / row / piece squared residuals
   double *d_partials = nullptr;
   double *d_sse_in = nullptr;    // entering-state SSE of the last half-sweep
@@ -142,6 +144,11 @@ struct DeviceGuard {
   }
 };
 
+size_t slot_bytes_of(const als_ctx *ctx) {
+  return ctx->lane_solve ? (size_t)als::ne_floats(als::lane_width(ctx->D)) * sizeof(float)
+                         : als::slot_floats_rt(ctx->DP) * sizeof(float);
+}
+
 // Degree-ordered schedule of one side with hub rows split into chunks.
 als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr) {
   const int64_t n_rows = (int64_t)ptr.size() - 1;
@@ -159,65 +166,89 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   });
   P.rows_with = (int64_t)order.size();
   const int64_t hub = ctx->tune.hub_threshold, chunk = ctx->tune.chunk;
-  const size_t slot_bytes = als::slot_floats_rt(ctx->DP) * sizeof(float);
-  const int64_t cap = std::max<int64_t>(1, ctx->tune.workspace_bytes / (int64_t)slot_bytes);
+  const int64_t cap = std::max<int64_t>(1, ctx->tune.workspace_bytes / (int64_t)slot_bytes_of(ctx));
   const int64_t max_chunks = P.max_deg > hub ? (P.max_deg + chunk - 1) / chunk : 0;
   if (max_chunks > cap)
     return fail(ctx, ALS_ERR_INVALID_ARG,
                 "workspace of %lld bytes holds %lld slots; a split row needs %lld",
                 (long long)ctx->tune.workspace_bytes, (long long)cap, (long long)max_chunks);
-  Batch cur{0, 0, 0, 0, 0};
-  for (int32_t s : order) {
-    const int64_t d = ptr[s + 1] - ptr[s];
-    const int64_t nch = d > hub ? (d + chunk - 1) / chunk : 0;
-    if (nch > 0) ++P.split_rows;
-    if (cur.n_slots + nch > cap) {
-      P.batches.push_back(cur);
-      cur = Batch{(int64_t)P.chunks.size(), 0, (int64_t)P.rows.size(), 0, 0};
+  // batches of consecutive rows whose chunks fit the workspace
+  std::vector<std::pair<int64_t, int64_t>> spans;  // [first, last) positions in order
+  {
+    int64_t first = 0, slots = 0;
+    for (int64_t k = 0; k < (int64_t)order.size(); ++k) {
+      const int64_t d = ptr[order[k] + 1] - ptr[order[k]];
+      const int64_t nch = d > hub ? (d + chunk - 1) / chunk : 0;
+      if (slots + nch > cap) {
+        spans.push_back({first, k});
+        first = k;
+        slots = 0;
+      }
+      slots += nch;
     }
-    RowTask rt;
-    rt.start = ptr[s];
-    rt.slot0 = cur.n_slots;
-    rt.row = s;
-    rt.deg = (int32_t)d;
-    rt.nslots = (int32_t)nch;
-    rt.pad = 0;
-    P.rows.push_back(rt);
-    for (int64_t k = 0; k < nch; ++k) {
+    if (first < (int64_t)order.size()) spans.push_back({first, (int64_t)order.size()});
+  }
+  for (const auto &sp : spans) {
+    Batch b{(int64_t)P.gitems.size(), 0, 0, (int64_t)P.rows.size(), 0, 0};
+    // chunks of the batch's split rows
+    for (int64_t k = sp.first; k < sp.second; ++k) {
+      const int32_t s = order[k];
+      const int64_t d = ptr[s + 1] - ptr[s];
+      if (d <= hub) continue;
+      const int64_t nch = (d + chunk - 1) / chunk;
+      ++P.split_rows;
+      RowTask rt;
+      rt.start = ptr[s];
+      rt.slot0 = b.n_slots;
+      rt.row = s;
+      rt.deg = (int32_t)d;
+      rt.nslots = (int32_t)nch;
+      rt.sse_idx = -1;
+      P.rows.push_back(rt);
+      for (int64_t q = 0; q < nch; ++q) {
+        WorkItem it;
+        it.start = ptr[s] + q * chunk;
+        it.len = (int32_t)std::min<int64_t>(chunk, d - q * chunk);
+        it.row = s;
+        it.slot = b.n_slots + q;
+        P.gitems.push_back(it);
+      }
+      b.n_slots += nch;
+      b.n_gchunks += nch;
+    }
+    // unsplit rows, one gather item each
+    for (int64_t k = sp.first; k < sp.second; ++k) {
+      const int32_t s = order[k];
+      const int64_t d = ptr[s + 1] - ptr[s];
+      if (d > hub) continue;
+      RowTask rt;
+      rt.start = ptr[s];
+      rt.slot0 = (int64_t)P.rows.size();  // record of the row's packed normal equations
+      rt.row = s;
+      rt.deg = (int32_t)d;
+      rt.nslots = 0;
+      rt.sse_idx = (int32_t)P.gitems.size();
+      P.rows.push_back(rt);
       WorkItem it;
-      it.start = ptr[s] + k * chunk;
-      it.len = (int32_t)std::min<int64_t>(chunk, d - k * chunk);
+      it.start = ptr[s];
+      it.len = (int32_t)d;
       it.row = s;
-      it.slot = cur.n_slots + k;
-      P.chunks.push_back(it);
+      it.slot = rt.slot0;
+      P.gitems.push_back(it);
     }
-    cur.n_chunks += nch;
-    cur.n_rows += 1;
-    cur.n_slots += nch;
+    b.n_gitems = (int64_t)P.gitems.size() - b.gitem_off;
+    b.n_rows = (int64_t)P.rows.size() - b.row_off;
+    P.n_chunks += b.n_gchunks;
+    P.batches.push_back(b);
   }
-  if (cur.n_rows > 0) P.batches.push_back(cur);
   for (const Batch &b : P.batches) P.max_slots = std::max(P.max_slots, b.n_slots);
-  P.pieces = P.chunks;
-  for (const RowTask &rt : P.rows) {
-    if (rt.nslots > 0) continue;
-    WorkItem it;
-    it.start = rt.start;
-    it.len = rt.deg;
-    it.row = rt.row;
-    it.slot = 0;
-    P.pieces.push_back(it);
-  }
-  HIP_OR_FAIL(ctx, dalloc(&P.d_chunks, (int64_t)P.chunks.size()));
+  HIP_OR_FAIL(ctx, dalloc(&P.d_gitems, (int64_t)P.gitems.size()));
   HIP_OR_FAIL(ctx, dalloc(&P.d_rows, (int64_t)P.rows.size()));
-  HIP_OR_FAIL(ctx, dalloc(&P.d_pieces, (int64_t)P.pieces.size()));
-  if (!P.chunks.empty())
-    HIP_OR_FAIL(ctx, hipMemcpy(P.d_chunks, P.chunks.data(), sizeof(WorkItem) * P.chunks.size(),
+  if (!P.gitems.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_gitems, P.gitems.data(), sizeof(WorkItem) * P.gitems.size(),
                                hipMemcpyHostToDevice));
   if (!P.rows.empty())
     HIP_OR_FAIL(ctx, hipMemcpy(P.d_rows, P.rows.data(), sizeof(RowTask) * P.rows.size(),
-                               hipMemcpyHostToDevice));
-  if (!P.pieces.empty())
-    HIP_OR_FAIL(ctx, hipMemcpy(P.d_pieces, P.pieces.data(), sizeof(WorkItem) * P.pieces.size(),
                                hipMemcpyHostToDevice));
   return ALS_OK;
 }
@@ -232,12 +263,12 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_row_idx);
   dfree(c->d_val_t);
   for (auto &P : c->plan) {
-    dfree(P.d_chunks);
+    dfree(P.d_gitems);
     dfree(P.d_rows);
-    dfree(P.d_pieces);
   }
   dfree(c->d_ws);
   dfree(c->d_fpad);
+  dfree(c->d_ne);
   dfree(c->d_sse_items);
   dfree(c->d_partials);
   dfree(c->d_sse_in);
@@ -308,10 +339,10 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 // d_sse_total; the fixed side must already be staged in d_fpad.
 als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, const uint8_t *val,
                          const float *X) {
-  const int64_t n = (int64_t)P.pieces.size();
+  const int64_t n = (int64_t)P.gitems.size();
   {
     PhaseTimer t(c, 3);
-    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_pieces, n, idx, val, c->d_fpad, X, c->D,
+    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_gitems, n, idx, val, c->d_fpad, X, c->D,
                                      c->d_sse_items, c->stream));
   }
   {
@@ -389,6 +420,7 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   c->nnz = nnz;
   c->D = D;
   c->DP = als::padded_width(D);
+  c->lane_solve = als::lane_width(D) > 0;
   c->stream = (hipStream_t)hip_stream;
   c->tune.hub_threshold = kDefaultHubThreshold;
   c->tune.chunk = kDefaultChunk;
@@ -466,14 +498,17 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   if (st != ALS_OK) return bail(st);
   st = build_plan(c, c->plan[ALS_ROWS_ITEMS], c->h_col_ptr);
   if (st != ALS_OK) return bail(st);
-  int64_t max_slots = 0, max_sse = 0;
+  int64_t max_slots = 0, max_sse = 0, max_rows = 0;
   for (auto &P : c->plan) {
     max_slots = std::max(max_slots, P.max_slots);
-    max_sse = std::max({max_sse, P.n_sse(), (int64_t)P.pieces.size()});
+    max_sse = std::max(max_sse, (int64_t)P.gitems.size());
+    max_rows = std::max(max_rows, (int64_t)P.rows.size());
   }
-  c->ws_bytes = (size_t)max_slots * als::slot_floats_rt(c->DP) * sizeof(float);
+  c->ws_bytes = (size_t)max_slots * slot_bytes_of(c);
   CK(dalloc(&c->d_ws, (int64_t)(c->ws_bytes / sizeof(float))));
-  CK(dalloc(&c->d_fpad, std::max(n_users, n_items) * (int64_t)c->DP));
+  if (c->lane_solve)
+    CK(dalloc(&c->d_ne, max_rows * (int64_t)als::ne_floats(als::lane_width(D))));
+  CK(dalloc(&c->d_fpad, (std::max(n_users, n_items) + 1) * (int64_t)c->DP));
   CK(dalloc(&c->d_sse_items, max_sse));
   CK(dalloc(&c->d_partials, als::reduce_partials(max_sse)));
   CK(dalloc(&c->d_sse_in, 1));
@@ -513,7 +548,6 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
   const SidePlan &P = ctx->plan[side];
   const int32_t *idx = users ? ctx->d_col : ctx->d_row_idx;
   const uint8_t *val = users ? ctx->d_val : ctx->d_val_t;
-  const int64_t n_chunks = (int64_t)P.chunks.size();
   HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
   {
     PhaseTimer t(ctx, 0);
@@ -521,24 +555,41 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
                                              ctx->d_fpad, ctx->stream));
   }
   for (const Batch &b : P.batches) {
-    if (b.n_chunks > 0) {
-      PhaseTimer t(ctx, 1);
-      HIP_OR_FAIL(ctx, als::launch_gram_chunks(ctx->DP, P.d_chunks + b.chunk_off, b.n_chunks, idx,
-                                               val, ctx->d_fpad, out_factors, ctx->D, ctx->d_ws,
-                                               ctx->d_sse_items + b.chunk_off, ctx->stream));
-    }
-    {
-      PhaseTimer t(ctx, 2);
-      HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val,
-                                        ctx->d_fpad, ctx->d_ws, ctx->D, lambda, out_factors,
-                                        ctx->d_sse_items + n_chunks + b.row_off, ctx->d_flag,
-                                        ctx->stream));
+    double *sse = ctx->d_sse_items + b.gitem_off;
+    if (ctx->lane_solve) {
+      {
+        PhaseTimer t(ctx, 1);
+        HIP_OR_FAIL(ctx, als::launch_gram_ne(ctx->D, P.d_gitems + b.gitem_off, b.n_gitems,
+                                             b.n_gchunks, idx, val, ctx->d_fpad, n_fixed,
+                                             out_factors, ctx->d_ws, ctx->d_ne, sse,
+                                             ctx->stream));
+      }
+      {
+        PhaseTimer t(ctx, 2);
+        HIP_OR_FAIL(ctx, als::launch_solve_lane(ctx->D, P.d_rows + b.row_off, b.n_rows,
+                                                ctx->d_ne, ctx->d_ws, lambda, out_factors,
+                                                ctx->d_flag, ctx->stream));
+      }
+    } else {
+      if (b.n_gchunks > 0) {
+        PhaseTimer t(ctx, 1);
+        HIP_OR_FAIL(ctx, als::launch_gram_chunks(ctx->DP, P.d_gitems + b.gitem_off, b.n_gchunks,
+                                                 idx, val, ctx->d_fpad, n_fixed, out_factors,
+                                                 ctx->D, ctx->d_ws, sse, ctx->stream));
+      }
+      {
+        PhaseTimer t(ctx, 2);
+        HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val,
+                                          ctx->d_fpad, n_fixed, ctx->d_ws, ctx->D, lambda,
+                                          out_factors, ctx->d_sse_items, ctx->d_flag,
+                                          ctx->stream));
+      }
     }
   }
   {
     PhaseTimer t(ctx, 4);
-    HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_sse_items, P.n_sse(), ctx->d_partials,
-                                        ctx->d_sse_in, ctx->stream));
+    HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_sse_items, (int64_t)P.gitems.size(),
+                                        ctx->d_partials, ctx->d_sse_in, ctx->stream));
   }
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse_in, ctx->d_sse_in, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
@@ -621,9 +672,9 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) 
   if ((side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS) || !out || n < 0)
     return fail(ctx, ALS_ERR_INVALID_ARG, "bad argument");
   const SidePlan &P = ctx->plan[side];
-  const int64_t v[6] = {P.rows_with, P.split_rows, (int64_t)P.chunks.size(),
-                        (int64_t)P.batches.size(), P.max_deg, (int64_t)ctx->ws_bytes};
-  for (int32_t i = 0; i < n && i < 6; ++i) out[i] = v[i];
+  const int64_t v[7] = {P.rows_with, P.split_rows, P.n_chunks, (int64_t)P.batches.size(),
+                        P.max_deg, (int64_t)ctx->ws_bytes, (int64_t)slot_bytes_of(ctx)};
+  for (int32_t i = 0; i < n && i < 7; ++i) out[i] = v[i];
   return ALS_OK;
 }
 

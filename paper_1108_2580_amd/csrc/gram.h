@@ -1,0 +1,151 @@
+// Device building blocks shared by the row kernels: lane layout helpers and
+// the gather + MFMA accumulation of one item's normal equations (Sec. 2.2)
+// together with the squared residuals of the entering state (Sec. 4.1).
+//
+// Lane (kq, c) = (lane / 16, lane % 16). Operand block X of rating k is
+// feature 16 X + c of the staged fixed row f_k in lane (k, c); one
+// v_mfma_f32_16x16x4f32 consumes four ratings. Accumulator tile (I, J),
+// I <= J, holds G[16 I + 4 kq + r][16 J + c] in element r.
+#pragma once
+
+#include "internal.h"
+
+namespace als {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float swz_xor(float v, int x) {
+  // ds_swizzle bit mode: lane' = lane ^ x within 32-lane halves
+  switch (x) {
+    case 1: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x041F));
+    case 2: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x081F));
+    case 4: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
+    default: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x201F));
+  }
+}
+
+__device__ __forceinline__ float sum16(float v) {
+  v += swz_xor(v, 8);
+  v += swz_xor(v, 4);
+  v += swz_xor(v, 2);
+  v += swz_xor(v, 1);
+  return v;
+}
+
+template <int T>
+__host__ __device__ constexpr int tidx(int I, int J) {
+  return I * T - I * (I - 1) / 2 + (J - I);
+}
+
+template <int DP>
+struct RowCfg {
+  static constexpr int T = DP / 16;
+  static constexpr int NT = T * (T + 1) / 2;
+  static constexpr int STEPS = T <= 2 ? 16 : (T <= 4 ? 8 : 4);  // steps whose loads are batched
+};
+
+// Accumulate the item's Gram tiles and right-hand side (per-lane partials over
+// the four rating groups) and the entering-state squared residuals.
+// xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
+// Ratings are taken in groups of 64; within a group the loads of all steps are
+// issued first and the MFMAs follow in blocks of four steps, so that only the
+// last block of an item carries padding.
+template <int DP>
+__device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
+                                                float (&rhs)[RowCfg<DP>::T],
+                                                const float (&xo)[RowCfg<DP>::T], double &sse,
+                                                const int32_t *__restrict__ ip,
+                                                const uint8_t *__restrict__ vp, int n,
+                                                const float *__restrict__ Fp, int zrow, int D) {
+  using C = RowCfg<DP>;
+  constexpr int T = C::T, STEPS = C::STEPS;
+  const int lane = threadIdx.x & 63;
+  const int kq = lane >> 4, c = lane & 15;
+  // Loads are never predicated per lane (a predicated load becomes a branch that
+  // waits for its own completion, which serialises the gathers): indices past the
+  // end are clamped and their values discarded, and ratings past the end of the
+  // item, as well as padded features, read the staged all-zero row zrow.
+  int jv = lane < n ? ip[lane] : zrow;
+  float rv = (float)vp[min(lane, n - 1)];
+  rv = lane < n ? rv : 0.f;
+  for (int g = 0; g < n; g += 64) {
+    const int gn = g + 64 + lane;
+    const int jl = ip[min(gn, n - 1)];
+    const float rl = (float)vp[min(gn, n - 1)];
+    const int jn = gn < n ? jl : zrow;
+    const float rn = gn < n ? rl : 0.f;
+    const int steps = min(16, (n - g + 3) >> 2);
+    float pi[16];  // per-step partial predictions of this lane's rating group
+#pragma unroll
+    for (int u = 0; u < 16; ++u) pi[u] = 0.f;
+#pragma unroll
+    for (int s0 = 0; s0 < 16; s0 += STEPS) {
+      if (s0 < steps) {
+        float a[STEPS][T];
+        float r[STEPS];
+#pragma unroll
+        for (int u = 0; u < STEPS; ++u) {
+          const int src = 4 * (s0 + u) + kq;
+          const int j = __shfl(jv, src);
+          r[u] = __shfl(rv, src);
+#pragma unroll
+          for (int X = 0; X < T; ++X) {
+            const int jr = 16 * X + c < D ? j : zrow;
+            a[u][X] = Fp[(int64_t)jr * DP + 16 * X + c];
+          }
+        }
+#pragma unroll
+        for (int u0 = 0; u0 < STEPS; u0 += 4) {
+          if (s0 + u0 < steps) {
+#pragma unroll
+            for (int u = u0; u < u0 + 4; ++u) {
+#pragma unroll
+              for (int X = 0; X < T; ++X) {
+                rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
+                pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
+              }
+#pragma unroll
+              for (int I = 0; I < T; ++I) {
+#pragma unroll
+                for (int J = I; J < T; ++J)
+                  acc[tidx<T>(I, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                      a[u][I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
+              }
+            }
+          }
+        }
+      }
+    }
+    // reduce-scatter the 16 step partials over the 16 feature lanes: afterwards
+    // lane c holds the full prediction of step c for its rating group
+    // (both halves are exchanged and the lane keeps the sum of its half; selecting
+    // between computed sums keeps the partial array statically indexed)
+#pragma unroll
+    for (int o = 8, m = 16; o >= 1; o >>= 1, m >>= 1) {
+      const bool hi = (c & o) != 0;
+#pragma unroll
+      for (int i = 0; i < m / 2; ++i) {
+        const float lo_sum = pi[i] + swz_xor(pi[i], o);
+        const float hi_sum = pi[m / 2 + i] + swz_xor(pi[m / 2 + i], o);
+        pi[i] = hi ? hi_sum : lo_sum;
+      }
+    }
+    // lane (kq, c) now holds the prediction of rating g + 4c + kq, whose value sits
+    // in lane 4c + kq of this group's rating register
+    const float rq = __shfl(rv, 4 * c + kq);
+    if (g + 4 * c + kq < n) {
+      const double e = (double)rq - (double)pi[0];
+      sse = fma(e, e, sse);
+    }
+    jv = jn;
+    rv = rn;
+  }
+}
+
+}  // namespace als

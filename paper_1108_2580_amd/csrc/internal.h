@@ -20,12 +20,12 @@ static_assert(sizeof(WorkItem) == 24, "WorkItem layout");
 // One row to solve. A row with nslots == 0 builds its normal equations from its
 // ratings [start, start + deg); a split row sums nslots workspace slots.
 struct RowTask {
-  int64_t start;  // first rating of the row
-  int64_t slot0;  // batch-local slot of the row's first chunk (split rows)
+  int64_t start;    // first rating of the row
+  int64_t slot0;    // batch-local slot of the row's first chunk (split rows)
   int32_t row;
-  int32_t deg;    // n_s, number of ratings of the row
+  int32_t deg;      // n_s, number of ratings of the row
   int32_t nslots;
-  int32_t pad;
+  int32_t sse_idx;  // where the row's entering-state squared residuals go (-1: split row)
 };
 static_assert(sizeof(RowTask) == 32, "RowTask layout");
 
@@ -46,26 +46,44 @@ hipError_t launch_csc_build(const int64_t *row_ptr, const int32_t *col, const ui
                             int32_t *scratch_cnt, int64_t *tot, int64_t *col_ptr,
                             int32_t *row_idx, uint8_t *val_t, hipStream_t s);
 
-// Copy of the fixed factors [n x D] into a zero-padded [n x DP] buffer (rowsolve.hip).
+// Copy of the fixed factors [n x D] into a zero-padded [(n + 1) x DP] buffer whose
+// row n is all zero (rowsolve.hip).
 hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *Fp, hipStream_t s);
 
 // Partial normal equations of the chunks of split rows, into their workspace
 // slots, with the chunks' entering-state squared residuals (rowsolve.hip).
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
-                              const uint8_t *val, const float *Fp, const float *Xold, int D,
-                              float *ws, double *sse, hipStream_t s);
+                              const uint8_t *val, const float *Fp, int64_t n_fixed,
+                              const float *Xold, int D, float *ws, double *sse, hipStream_t s);
 
 // Fused per-row normal equations, regularisation, Cholesky and solves; X is read
 // (entering state) and overwritten in place (rowsolve.hip).
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                       const uint8_t *val, const float *Fp, const float *ws, int D, float lam,
-                       float *X, double *sse, int32_t *flag, hipStream_t s);
+                       const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
+                       int D, float lam, float *X, double *sse, int32_t *flag, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
 // fixed side Fp (row stride DP) (residual.hip).
 hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
                         const uint8_t *val, const float *Fp, const float *X, int D,
                         double *sse_items, hipStream_t s);
+
+// Widths solved one row per lane (registers hold the packed normal equations).
+inline int lane_width(int D) { return D <= 16 ? 16 : (D <= 20 ? 20 : 0); }
+// Floats of one row's packed normal equations: upper triangle, right-hand side,
+// rounded up to a multiple of 4.
+constexpr int ne_floats(int ld) { return ((ld * (ld + 1) / 2 + ld) + 3) / 4 * 4; }
+
+// Gram of rows or chunks packed into normal-equation records (lanesolve.hip):
+// items [0, n_chunk_items) write to ws at their slot, the rest to ne at their slot.
+hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
+                          const int32_t *idx, const uint8_t *val, const float *Fp,
+                          int64_t n_fixed, const float *Xold, float *ws, float *ne, double *sse,
+                          hipStream_t s);
+
+// One row per lane: regularise, Cholesky, solve, write (lanesolve.hip).
+hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, const float *ne,
+                             const float *ws, float lam, float *X, int32_t *flag, hipStream_t s);
 
 // Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].
 int64_t reduce_partials(int64_t n);

@@ -1,0 +1,211 @@
+// Narrow factor widths (D <= 20): normal equations built by the MFMA gather
+// kernel, solved one row per lane.
+//
+// For small D a wavefront-wide factorisation leaves most lanes idle, while a
+// whole D x D system fits in one lane's registers. The half-sweep therefore
+// splits in two launches:
+//   k_gram_ne    one wavefront per row (or chunk of a split row) accumulates
+//                G = sum f f^T and b = sum r f on MFMA (gram.h), plus the
+//                entering-state squared residuals, and stores the upper
+//                triangle of G and b as a packed record;
+//   k_solve_lane one lane per row loads its record (summing the chunk records
+//                of a split row), adds lambda * n_s to the diagonal, factors
+//                A = U^T U in registers, solves U^T y = b and U x = y
+//                (Sec. 2.2; the per-update "matrix inversion" of Sec. 4.1) and
+//                writes x unless a pivot is not positive and finite.
+// Records hold LD(LD+1)/2 + LD floats (LD = 16 or 20, the width the solve is
+// compiled for; padded features solve to zero), rounded up to a multiple of 4.
+#include "gram.h"
+
+namespace als {
+
+template <int LD>
+__host__ __device__ constexpr int tri(int a, int b) {  // a <= b, row-major upper triangle
+  return a * LD - a * (a - 1) / 2 + (b - a);
+}
+
+template <int DP, int LD>
+__global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ items,
+                                                int64_t n_chunk_items,
+                                                const int32_t *__restrict__ idx,
+                                                const uint8_t *__restrict__ val,
+                                                const float *__restrict__ Fp, int zrow,
+                                                const float *__restrict__ Xold, int D,
+                                                float *__restrict__ ws, float *__restrict__ ne,
+                                                double *__restrict__ sse_out) {
+  using C = RowCfg<DP>;
+  constexpr int T = C::T, NT = C::NT;
+  constexpr int NTRI = LD * (LD + 1) / 2;
+  constexpr int NES = ne_floats(LD);
+  const WorkItem it = items[blockIdx.x];
+  const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float rhs[T], xo[T];
+#pragma unroll
+  for (int X = 0; X < T; ++X) {
+    rhs[X] = 0.f;
+    {
+      const float v = Xold[(int64_t)it.row * D + min(16 * X + c, D - 1)];
+      xo[X] = 16 * X + c < D ? v : 0.f;
+    }
+  }
+  double sse = 0.0;
+  gram_accumulate<DP>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow, D);
+#pragma unroll
+  for (int X = 0; X < T; ++X) {
+    rhs[X] += __shfl_xor(rhs[X], 16);
+    rhs[X] += __shfl_xor(rhs[X], 32);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
+  float *__restrict__ out = ((int64_t)blockIdx.x < n_chunk_items ? ws : ne) + it.slot * NES;
+#pragma unroll
+  for (int I = 0; I < T; ++I) {
+#pragma unroll
+    for (int J = I; J < T; ++J) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = 16 * I + 4 * kq + r, b = 16 * J + c;
+        if (a <= b && b < LD) out[tri<LD>(a, b)] = acc[tidx<T>(I, J)][r];
+      }
+    }
+  }
+  if (kq == 0) {
+#pragma unroll
+    for (int X = 0; X < T; ++X)
+      if (16 * X + c < LD) out[NTRI + 16 * X + c] = rhs[X];
+  }
+  if (lane == 0) sse_out[blockIdx.x] = sse;
+}
+
+template <int LD>
+__global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ rows, int64_t n_rows,
+                                                   const float *__restrict__ ne,
+                                                   const float *__restrict__ ws, int D, float lam,
+                                                   float *__restrict__ X,
+                                                   int32_t *__restrict__ flag_count) {
+  constexpr int NTRI = LD * (LD + 1) / 2;
+  constexpr int NES = ne_floats(LD);
+  const int64_t i = (int64_t)blockIdx.x * 64 + threadIdx.x;
+  if (i >= n_rows) return;
+  const RowTask rt = rows[i];
+  float A[NTRI], b[LD];
+  if (rt.nslots == 0) {
+    const float4 *__restrict__ p = reinterpret_cast<const float4 *>(ne + rt.slot0 * NES);
+#pragma unroll
+    for (int q = 0; q < NES / 4; ++q) {
+      const float4 v = p[q];
+      const float w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = 4 * q + j;
+        if (e < NTRI) A[e] = w[j];
+        else if (e < NTRI + LD) b[e - NTRI] = w[j];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < NTRI; ++e) A[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < LD; ++e) b[e] = 0.f;
+    for (int s = 0; s < rt.nslots; ++s) {
+      const float4 *__restrict__ p =
+          reinterpret_cast<const float4 *>(ws + (rt.slot0 + s) * (int64_t)NES);
+#pragma unroll
+      for (int q = 0; q < NES / 4; ++q) {
+        const float4 v = p[q];
+        const float w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = 4 * q + j;
+          if (e < NTRI) A[e] += w[j];
+          else if (e < NTRI + LD) b[e - NTRI] += w[j];
+        }
+      }
+    }
+  }
+  const float lam_n = (float)((double)lam * (double)rt.deg);
+#pragma unroll
+  for (int d = 0; d < LD; ++d) A[tri<LD>(d, d)] = d < D ? A[tri<LD>(d, d)] + lam_n : 1.f;
+
+  // A = U^T U in place (upper triangle); the diagonal keeps 1 / u_kk
+  bool bad = false;
+#pragma unroll
+  for (int k = 0; k < LD; ++k) {
+    const float p = A[tri<LD>(k, k)];
+    bad |= !(p > 0.f && p < INFINITY);
+    const float iv = 1.f / sqrtf(fmaxf(p, 1e-30f));
+    A[tri<LD>(k, k)] = iv;
+#pragma unroll
+    for (int j = k + 1; j < LD; ++j) A[tri<LD>(k, j)] *= iv;
+#pragma unroll
+    for (int r = k + 1; r < LD; ++r) {
+#pragma unroll
+      for (int j = r; j < LD; ++j)
+        A[tri<LD>(r, j)] = fmaf(-A[tri<LD>(k, r)], A[tri<LD>(k, j)], A[tri<LD>(r, j)]);
+    }
+  }
+  // U^T y = b (y overwrites b)
+#pragma unroll
+  for (int k = 0; k < LD; ++k) {
+    b[k] *= A[tri<LD>(k, k)];
+#pragma unroll
+    for (int j = k + 1; j < LD; ++j) b[j] = fmaf(-A[tri<LD>(k, j)], b[k], b[j]);
+  }
+  // U x = y (x overwrites b)
+#pragma unroll
+  for (int k = LD - 1; k >= 0; --k) {
+    float s = b[k];
+#pragma unroll
+    for (int j = k + 1; j < LD; ++j) s = fmaf(-A[tri<LD>(k, j)], b[j], s);
+    b[k] = s * A[tri<LD>(k, k)];
+  }
+#pragma unroll
+  for (int d = 0; d < LD; ++d) bad |= !(fabsf(b[d]) < INFINITY);
+  if (bad) {
+    atomicAdd(flag_count, 1);
+    return;
+  }
+  float *__restrict__ xr = X + (int64_t)rt.row * D;
+#pragma unroll
+  for (int d = 0; d < LD; ++d)
+    if (d < D) xr[d] = b[d];
+}
+
+hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
+                          const int32_t *idx, const uint8_t *val, const float *Fp,
+                          int64_t n_fixed, const float *Xold, float *ws, float *ne, double *sse,
+                          hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  const int zrow = (int)n_fixed;
+  const int ld = lane_width(D);
+  if (ld == 16)
+    hipLaunchKernelGGL((k_gram_ne<16, 16>), dim3((unsigned)n_items), dim3(64), 0, s, items,
+                       n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
+  else if (ld == 20)
+    hipLaunchKernelGGL((k_gram_ne<32, 20>), dim3((unsigned)n_items), dim3(64), 0, s, items,
+                       n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, const float *ne,
+                             const float *ws, float lam, float *X, int32_t *flag, hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n_rows + 63) / 64);
+  const int ld = lane_width(D);
+  if (ld == 16)
+    hipLaunchKernelGGL(k_solve_lane<16>, dim3(blocks), dim3(64), 0, s, rows, n_rows, ne, ws, D,
+                       lam, X, flag);
+  else if (ld == 20)
+    hipLaunchKernelGGL(k_solve_lane<20>, dim3(blocks), dim3(64), 0, s, rows, n_rows, ne, ws, D,
+                       lam, X, flag);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace als

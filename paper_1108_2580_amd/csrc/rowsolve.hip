@@ -21,147 +21,30 @@
 // (I, J), I <= J, holds A[16 I + 4 kq + r][16 J + c] in element r. The fixed
 // side is read from a staged copy with row stride DP (zero padded), so every
 // gathered row starts on a 64-byte boundary.
-#include "internal.h"
+#include "gram.h"
 
 namespace als {
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ float swz_xor(float v, int x) {
-  // ds_swizzle bit mode: lane' = lane ^ x within 32-lane halves
-  switch (x) {
-    case 1: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x041F));
-    case 2: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x081F));
-    case 4: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
-    default: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x201F));
-  }
-}
-
-__device__ __forceinline__ float sum16(float v) {
-  v += swz_xor(v, 8);
-  v += swz_xor(v, 4);
-  v += swz_xor(v, 2);
-  v += swz_xor(v, 1);
-  return v;
-}
-
-template <int T>
-__host__ __device__ constexpr int tidx(int I, int J) {
-  return I * T - I * (I - 1) / 2 + (J - I);
-}
-
-template <int DP>
-struct RowCfg {
-  static constexpr int T = DP / 16;
-  static constexpr int NT = T * (T + 1) / 2;
-  static constexpr int STEPS = T <= 2 ? 16 : (T <= 4 ? 8 : 4);  // steps whose loads are batched
-};
-
-// Copy the fixed factors [n x D] into a zero-padded [n x DP] buffer.
+// Copy the fixed factors [n x D] into a zero-padded [(n + 1) x DP] buffer whose
+// last row is all zero (the stand-in of padded features and absent ratings).
 __global__ void k_stage_fixed(const float *__restrict__ F, int64_t n, int D, int DP,
                               float *__restrict__ Fp) {
-  const int64_t total = n * DP;
+  const int64_t total = (n + 1) * DP;
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < total; i += stride) {
     const int64_t row = i / DP;
     const int d = (int)(i - row * DP);
-    Fp[i] = d < D ? F[row * D + d] : 0.f;
+    Fp[i] = (row < n && d < D) ? F[row * D + d] : 0.f;
   }
 }
 
 hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *Fp, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  int64_t blocks = (n * DP + 255) / 256;
+  if (n < 0) return hipErrorInvalidValue;
+  int64_t blocks = ((n + 1) * DP + 255) / 256;
   if (blocks > 262144) blocks = 262144;
   hipLaunchKernelGGL(k_stage_fixed, dim3((unsigned)blocks), dim3(256), 0, s, F, n, D, DP, Fp);
   return hipGetLastError();
-}
-
-// Accumulate the item's Gram tiles and right-hand side (per-lane partials over
-// the four rating groups) and the entering-state squared residuals.
-// xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
-template <int DP>
-__device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
-                                                float (&rhs)[RowCfg<DP>::T],
-                                                const float (&xo)[RowCfg<DP>::T], double &sse,
-                                                const int32_t *__restrict__ ip,
-                                                const uint8_t *__restrict__ vp, int n,
-                                                const float *__restrict__ Fp) {
-  using C = RowCfg<DP>;
-  constexpr int T = C::T, STEPS = C::STEPS;
-  const int lane = threadIdx.x & 63;
-  const int kq = lane >> 4, c = lane & 15;
-  int jv = lane < n ? ip[lane] : 0;
-  float rv = lane < n ? (float)vp[lane] : 0.f;
-  for (int g = 0; g < n; g += 64) {
-    const int gn = g + 64 + lane;
-    const int jn = gn < n ? ip[gn] : 0;
-    const float rn = gn < n ? (float)vp[gn] : 0.f;
-    const int steps = min(16, (n - g + 3) >> 2);
-    float pi[16];  // per-step partial predictions of this lane's rating group
-#pragma unroll
-    for (int u = 0; u < 16; ++u) pi[u] = 0.f;
-#pragma unroll
-    for (int s0 = 0; s0 < 16; s0 += STEPS) {
-      if (s0 < steps) {
-        float a[STEPS][T];
-        float r[STEPS];
-#pragma unroll
-        for (int u = 0; u < STEPS; ++u) {
-          const int src = 4 * (s0 + u) + kq;
-          const int j = __shfl(jv, src);
-          r[u] = __shfl(rv, src);
-          const bool ok = g + src < n;
-          const float *__restrict__ fr = Fp + (int64_t)j * DP + c;
-#pragma unroll
-          for (int X = 0; X < T; ++X) a[u][X] = ok ? fr[16 * X] : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < STEPS; ++u) {
-          if (s0 + u < steps) {
-#pragma unroll
-            for (int X = 0; X < T; ++X) {
-              rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
-              pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
-            }
-#pragma unroll
-            for (int I = 0; I < T; ++I) {
-#pragma unroll
-              for (int J = I; J < T; ++J)
-                acc[tidx<T>(I, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                    a[u][I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
-            }
-          }
-        }
-      }
-    }
-    // reduce-scatter the 16 step partials over the 16 feature lanes: afterwards
-    // lane c holds the full prediction of step c for its rating group
-#pragma unroll
-    for (int o = 8, m = 16; o >= 1; o >>= 1, m >>= 1) {
-      const bool hi = (c & o) != 0;
-#pragma unroll
-      for (int i = 0; i < m / 2; ++i) {
-        const float keep = hi ? pi[m / 2 + i] : pi[i];
-        const float give = hi ? pi[i] : pi[m / 2 + i];
-        pi[i] = keep + swz_xor(give, o);
-      }
-    }
-    const int q = g + 4 * c + kq;  // rating whose prediction this lane now holds
-    if (q < n) {
-      const double e = (double)vp[q] - (double)pi[0];
-      sse = fma(e, e, sse);
-    }
-    jv = jn;
-    rv = rn;
-  }
 }
 
 // Partial normal equations of the chunks of split rows, with the chunks'
@@ -170,7 +53,7 @@ template <int DP>
 __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__ items,
                                                     const int32_t *__restrict__ idx,
                                                     const uint8_t *__restrict__ val,
-                                                    const float *__restrict__ Fp,
+                                                    const float *__restrict__ Fp, int zrow,
                                                     const float *__restrict__ Xold, int D,
                                                     float *__restrict__ ws,
                                                     double *__restrict__ sse_out) {
@@ -185,10 +68,13 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
 #pragma unroll
   for (int X = 0; X < T; ++X) {
     rhs[X] = 0.f;
-    xo[X] = 16 * X + c < D ? Xold[(int64_t)it.row * D + 16 * X + c] : 0.f;
+    {
+      const float v = Xold[(int64_t)it.row * D + min(16 * X + c, D - 1)];
+      xo[X] = 16 * X + c < D ? v : 0.f;
+    }
   }
   double sse = 0.0;
-  gram_accumulate<DP>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp);
+  gram_accumulate<DP>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow, D);
 #pragma unroll
   for (int X = 0; X < T; ++X) {
     rhs[X] += __shfl_xor(rhs[X], 16);
@@ -211,8 +97,9 @@ constexpr int kRowWaves = 4;  // independent rows per workgroup (one per wavefro
 template <int DP>
 __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
-    const uint8_t *__restrict__ val, const float *__restrict__ Fp, const float *__restrict__ ws,
-    int D, float lam, float *__restrict__ X_io, double *__restrict__ sse_out,
+    const uint8_t *__restrict__ val, const float *__restrict__ Fp, int zrow,
+    const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
+    double *__restrict__ sse_out,
     int32_t *__restrict__ flag_count) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
@@ -239,9 +126,12 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
   if (rt.nslots == 0) {
     float xo[T];
 #pragma unroll
-    for (int X = 0; X < T; ++X) xo[X] = 16 * X + c < D ? xrow[16 * X + c] : 0.f;
+    for (int X = 0; X < T; ++X) {
+      const float v = xrow[min(16 * X + c, D - 1)];
+      xo[X] = 16 * X + c < D ? v : 0.f;
+    }
     double sse = 0.0;
-    gram_accumulate<DP>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp);
+    gram_accumulate<DP>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow, D);
 #pragma unroll
     for (int X = 0; X < T; ++X) {
       rhs[X] += __shfl_xor(rhs[X], 16);
@@ -249,7 +139,7 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
-    if (lane == 0) sse_out[task] = sse;
+    if (lane == 0 && rt.sse_idx >= 0) sse_out[rt.sse_idx] = sse;
   } else {
     const float *__restrict__ base = ws + rt.slot0 * (int64_t)slot_floats(DP);
     for (int s = 0; s < rt.nslots; ++s) {
@@ -259,7 +149,6 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
 #pragma unroll
       for (int X = 0; X < T; ++X) rhs[X] += sl[NT * 256 + 16 * X + c];
     }
-    if (lane == 0) sse_out[task] = 0.0;
   }
 
   // ---- A = G + lambda n I on the first D diagonal entries, identity on the padding ----
@@ -415,22 +304,24 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
 
 template <int DP>
 static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                                const uint8_t *val, const float *Fp, const float *ws, int D,
-                                float lam, float *X, double *sse, int32_t *flag, hipStream_t s) {
+                                const uint8_t *val, const float *Fp, int zrow, const float *ws,
+                                int D, float lam, float *X, double *sse, int32_t *flag,
+                                hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
   hipLaunchKernelGGL(k_rows<DP>, dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s, rows, n_rows,
-                     idx, val, Fp, ws, D, lam, X, sse, flag);
+                     idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
   return hipGetLastError();
 }
 
 template <int DP>
 static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_t *idx,
-                                  const uint8_t *val, const float *Fp, const float *Xold, int D,
-                                  float *ws, double *sse, hipStream_t s) {
+                                  const uint8_t *val, const float *Fp, int zrow,
+                                  const float *Xold, int D, float *ws, double *sse,
+                                  hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_gram_chunks<DP>, dim3((unsigned)n), dim3(64), 0, s, items, idx, val, Fp,
-                     Xold, D, ws, sse);
+                     zrow, Xold, D, ws, sse);
   return hipGetLastError();
 }
 
@@ -448,16 +339,19 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
   }
 
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                       const uint8_t *val, const float *Fp, const float *ws, int D, float lam,
-                       float *X, double *sse, int32_t *flag, hipStream_t s) {
-  ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, Fp, ws, D, lam, X, sse,
-                                              flag, s));
+                       const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
+                       int D, float lam, float *X, double *sse, int32_t *flag, hipStream_t s) {
+  const int zrow = (int)n_fixed;
+  ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X,
+                                              sse, flag, s));
 }
 
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
-                              const uint8_t *val, const float *Fp, const float *Xold, int D,
-                              float *ws, double *sse, hipStream_t s) {
-  ALS_DP_SWITCH(dp, return launch_chunks_t<DPV>(items, n, idx, val, Fp, Xold, D, ws, sse, s));
+                              const uint8_t *val, const float *Fp, int64_t n_fixed,
+                              const float *Xold, int D, float *ws, double *sse, hipStream_t s) {
+  const int zrow = (int)n_fixed;
+  ALS_DP_SWITCH(dp, return launch_chunks_t<DPV>(items, n, idx, val, Fp, zrow, Xold, D, ws, sse,
+                                                s));
 }
 
 }  // namespace als

@@ -145,9 +145,9 @@ def test_widths_with_split_rows_and_batches(D):
     ptr, col, val = small_matrix(D)
     U0, V0 = workload.init_factors(M, N, D, seed=77 + D)
     # tiny thresholds: rows above 40 ratings split into chunks of 24, and a small
-    # workspace so that each side runs in several batches
-    slot = ((D + 15) // 16)
-    slot_bytes = (slot * (slot + 1) // 2 * 256 + slot * 16) * 4
+    # workspace (16 slots) so that each side runs in several batches
+    with make_als(M, N, ptr, col, val, D, dict(hub_threshold=40, chunk=24)) as als:
+        slot_bytes = als.plan_stats("users")["slot_bytes"]
     tun = dict(hub_threshold=40, chunk=24, workspace_bytes=slot_bytes * 16)
     with make_als(M, N, ptr, col, val, D, tun) as als:
         st_u, st_i = als.plan_stats("users"), als.plan_stats("items")
