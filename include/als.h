@@ -68,7 +68,10 @@ typedef struct {
 
 /*
  * Create a context for one rating matrix and one factor width D.
- *   n_users, n_items  matrix shape (M, N); each >= 1 and < 2^31 - 1.
+ *   n_users, n_items  matrix shape (M, N); each >= 1, and (max(M, N) + 1) * DP * 4
+ *                     < 2^32 bytes with DP = 16 * ceil(D / 16) (the staged fixed side
+ *                     is addressed with 32-bit offsets): up to 8.4M rows per side at
+ *                     D = 128, 33.5M at D = 20.
  *   nnz               number of stored ratings; 0 <= nnz < 2^31.
  *   row_ptr           host int64[n_users + 1]: row_ptr[0] = 0, non-decreasing,
  *                     row_ptr[n_users] = nnz.

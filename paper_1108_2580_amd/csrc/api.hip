@@ -37,6 +37,7 @@ struct Batch {
   int64_t n_gchunks;  // its chunks of split rows (they come first)
   int64_t n_gitems;   // chunks + unsplit rows
   int64_t row_off, n_rows;
+  int64_t n_split;    // the batch's first n_split rows are split rows
   int64_t n_slots;    // workspace slots used by the batch's chunks
 };
 
@@ -189,7 +190,7 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
     if (first < (int64_t)order.size()) spans.push_back({first, (int64_t)order.size()});
   }
   for (const auto &sp : spans) {
-    Batch b{(int64_t)P.gitems.size(), 0, 0, (int64_t)P.rows.size(), 0, 0};
+    Batch b{(int64_t)P.gitems.size(), 0, 0, (int64_t)P.rows.size(), 0, 0, 0};
     // chunks of the batch's split rows
     for (int64_t k = sp.first; k < sp.second; ++k) {
       const int32_t s = order[k];
@@ -215,6 +216,7 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
       }
       b.n_slots += nch;
       b.n_gchunks += nch;
+      b.n_split += 1;
     }
     // unsplit rows, one gather item each
     for (int64_t k = sp.first; k < sp.second; ++k) {
@@ -385,6 +387,10 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   if (nnz < 0 || nnz >= (1LL << 31))
     return fail(nullptr, ALS_ERR_INVALID_ARG, "nnz %lld out of range", (long long)nnz);
   if (D < 1 || D > 128) return fail(nullptr, ALS_ERR_INVALID_ARG, "D = %d outside [1, 128]", D);
+  if ((std::max(n_users, n_items) + 1) * (int64_t)als::padded_width(D) * 4 > als::kMaxStagedBytes)
+    return fail(nullptr, ALS_ERR_INVALID_ARG,
+                "(max(n_users, n_items) + 1) * %d * 4 bytes exceeds the 4 GiB staged-factor limit",
+                als::padded_width(D));
   if (!row_ptr || (nnz > 0 && (!col_idx || !ratings)))
     return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL host array");
   // ---- A1: validation of the CSR ----
@@ -566,9 +572,9 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
       }
       {
         PhaseTimer t(ctx, 2);
-        HIP_OR_FAIL(ctx, als::launch_solve_lane(ctx->D, P.d_rows + b.row_off, b.n_rows,
-                                                ctx->d_ne, ctx->d_ws, lambda, out_factors,
-                                                ctx->d_flag, ctx->stream));
+        HIP_OR_FAIL(ctx, als::launch_solve_lane(ctx->D, P.d_rows + b.row_off, b.n_rows, b.n_split,
+                                                b.row_off, ctx->d_ws, ctx->d_ne, lambda,
+                                                out_factors, ctx->d_flag, ctx->stream));
       }
     } else {
       if (b.n_gchunks > 0) {

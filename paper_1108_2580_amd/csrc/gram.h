@@ -94,10 +94,13 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
           const int src = 4 * (s0 + u) + kq;
           const int j = __shfl(jv, src);
           r[u] = __shfl(rv, src);
+          // 32-bit byte offsets from the (uniform) table base; every block but the
+          // last holds real features only
 #pragma unroll
           for (int X = 0; X < T; ++X) {
-            const int jr = 16 * X + c < D ? j : zrow;
-            a[u][X] = Fp[(int64_t)jr * DP + 16 * X + c];
+            const int jr = (X < T - 1 || 16 * X + c < D) ? j : zrow;
+            const uint32_t off = (uint32_t)jr * (uint32_t)(DP * 4) + (uint32_t)((16 * X + c) * 4);
+            a[u][X] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(Fp) + off);
           }
         }
 #pragma unroll

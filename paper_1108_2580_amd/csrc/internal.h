@@ -29,6 +29,10 @@ struct RowTask {
 };
 static_assert(sizeof(RowTask) == 32, "RowTask layout");
 
+// The staged fixed side is addressed with 32-bit byte offsets:
+// (rows + 1) * DP * 4 must stay below 2^32.
+constexpr int64_t kMaxStagedBytes = (1LL << 32) - 1;
+
 // Padded factor width: D rounded up to the 16-wide MFMA tile.
 inline int padded_width(int D) { return ((D + 15) / 16) * 16; }
 // Upper-triangle 16x16 tiles of a DP x DP Gram matrix.
@@ -81,9 +85,12 @@ hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t
                           int64_t n_fixed, const float *Xold, float *ws, float *ne, double *sse,
                           hipStream_t s);
 
-// One row per lane: regularise, Cholesky, solve, write (lanesolve.hip).
-hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, const float *ne,
-                             const float *ws, float lam, float *X, int32_t *flag, hipStream_t s);
+// One row per lane: regularise, Cholesky, solve, write (lanesolve.hip). Row i of
+// the launch uses record base + i; its first n_split rows are split rows whose
+// chunk records (in ws) are summed into their records first.
+hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t n_split,
+                             int64_t base, const float *ws, float *ne, float lam, float *X,
+                             int32_t *flag, hipStream_t s);
 
 // Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].
 int64_t reduce_partials(int64_t n);

@@ -8,8 +8,9 @@
 //                G = sum f f^T and b = sum r f on MFMA (gram.h), plus the
 //                entering-state squared residuals, and stores the upper
 //                triangle of G and b as a packed record;
-//   k_solve_lane one lane per row loads its record (summing the chunk records
-//                of a split row), adds lambda * n_s to the diagonal, factors
+//   k_sum_records sums the chunk records of each split row into its record;
+//   k_solve_lane one lane per row loads its record, adds lambda * n_s to the
+//                diagonal, factors
 //                A = U^T U in registers, solves U^T y = b and U x = y
 //                (Sec. 2.2; the per-update "matrix inversion" of Sec. 4.1) and
 //                writes x unless a pivot is not positive and finite.
@@ -80,11 +81,24 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   if (lane == 0) sse_out[blockIdx.x] = sse;
 }
 
+// Sum the chunk records of each split row, in slot order, into the row's record.
+template <int LD>
+__global__ __launch_bounds__(256) void k_sum_records(const RowTask *__restrict__ rows, int64_t base,
+                                                     const float *__restrict__ ws,
+                                                     float *__restrict__ ne) {
+  constexpr int NES = ne_floats(LD);
+  const RowTask rt = rows[blockIdx.x];
+  for (int e = threadIdx.x; e < NES; e += 256) {
+    float v = 0.f;
+    for (int s = 0; s < rt.nslots; ++s) v += ws[(rt.slot0 + s) * (int64_t)NES + e];
+    ne[(base + blockIdx.x) * (int64_t)NES + e] = v;
+  }
+}
+
 template <int LD>
 __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ rows, int64_t n_rows,
-                                                   const float *__restrict__ ne,
-                                                   const float *__restrict__ ws, int D, float lam,
-                                                   float *__restrict__ X,
+                                                   int64_t base, const float *__restrict__ ne,
+                                                   int D, float lam, float *__restrict__ X,
                                                    int32_t *__restrict__ flag_count) {
   constexpr int NTRI = LD * (LD + 1) / 2;
   constexpr int NES = ne_floats(LD);
@@ -92,38 +106,16 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
   if (i >= n_rows) return;
   const RowTask rt = rows[i];
   float A[NTRI], b[LD];
-  if (rt.nslots == 0) {
-    const float4 *__restrict__ p = reinterpret_cast<const float4 *>(ne + rt.slot0 * NES);
+  const float4 *__restrict__ p = reinterpret_cast<const float4 *>(ne + (base + i) * NES);
 #pragma unroll
-    for (int q = 0; q < NES / 4; ++q) {
-      const float4 v = p[q];
-      const float w[4] = {v.x, v.y, v.z, v.w};
+  for (int q = 0; q < NES / 4; ++q) {
+    const float4 v = p[q];
+    const float w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = 4 * q + j;
-        if (e < NTRI) A[e] = w[j];
-        else if (e < NTRI + LD) b[e - NTRI] = w[j];
-      }
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < NTRI; ++e) A[e] = 0.f;
-#pragma unroll
-    for (int e = 0; e < LD; ++e) b[e] = 0.f;
-    for (int s = 0; s < rt.nslots; ++s) {
-      const float4 *__restrict__ p =
-          reinterpret_cast<const float4 *>(ws + (rt.slot0 + s) * (int64_t)NES);
-#pragma unroll
-      for (int q = 0; q < NES / 4; ++q) {
-        const float4 v = p[q];
-        const float w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int e = 4 * q + j;
-          if (e < NTRI) A[e] += w[j];
-          else if (e < NTRI + LD) b[e - NTRI] += w[j];
-        }
-      }
+    for (int j = 0; j < 4; ++j) {
+      const int e = 4 * q + j;
+      if (e < NTRI) A[e] = w[j];
+      else if (e < NTRI + LD) b[e - NTRI] = w[j];
     }
   }
   const float lam_n = (float)((double)lam * (double)rt.deg);
@@ -192,19 +184,29 @@ hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, const float *ne,
-                             const float *ws, float lam, float *X, int32_t *flag, hipStream_t s) {
+hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t n_split,
+                             int64_t base, const float *ws, float *ne, float lam, float *X,
+                             int32_t *flag, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((n_rows + 63) / 64);
   const int ld = lane_width(D);
+  if (ld != 16 && ld != 20) return hipErrorInvalidValue;
+  if (n_split > 0) {
+    if (ld == 16)
+      hipLaunchKernelGGL(k_sum_records<16>, dim3((unsigned)n_split), dim3(256), 0, s, rows, base,
+                         ws, ne);
+    else
+      hipLaunchKernelGGL(k_sum_records<20>, dim3((unsigned)n_split), dim3(256), 0, s, rows, base,
+                         ws, ne);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const unsigned blocks = (unsigned)((n_rows + 63) / 64);
   if (ld == 16)
-    hipLaunchKernelGGL(k_solve_lane<16>, dim3(blocks), dim3(64), 0, s, rows, n_rows, ne, ws, D,
-                       lam, X, flag);
-  else if (ld == 20)
-    hipLaunchKernelGGL(k_solve_lane<20>, dim3(blocks), dim3(64), 0, s, rows, n_rows, ne, ws, D,
+    hipLaunchKernelGGL(k_solve_lane<16>, dim3(blocks), dim3(64), 0, s, rows, n_rows, base, ne, D,
                        lam, X, flag);
   else
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_solve_lane<20>, dim3(blocks), dim3(64), 0, s, rows, n_rows, base, ne, D,
+                       lam, X, flag);
   return hipGetLastError();
 }
 
