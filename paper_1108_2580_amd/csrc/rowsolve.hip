@@ -6,12 +6,15 @@
 //      the squared residuals (r_k - x_s . f_k)^2 of the state entering the
 //      half-sweep (x_s = the row's previous value) for the training RMSE
 //      (Sec. 4.1);
-//   2. adds lambda * n_s to the diagonal and factors A = U^T U in place, in
+//   2. factors A = U^T U (lambda n_s I is the accumulators' initial value) in
 //      panels of four rows: the 4x4 diagonal block is factored in every lane,
-//      the panel rows are formed by a 4x4 triangular solve per column, and the
-//      trailing tiles are updated on MFMA (K = 4);
+//      the panel rows of U are formed by a 4x4 triangular solve per column, and
+//      the trailing tiles are updated on MFMA (K = 4). The accumulators are only
+//      written by MFMA and read by VALU, so they stay in accumulator registers;
 //   3. forward substitution of b rides along the panels; back substitution
-//      follows; x_s is written unless a pivot was not positive and finite.
+//      follows, forming U's panel rows from the untouched A_p rows and the
+//      stored 4x4 blocks; x_s is written unless a pivot was not positive and
+//      finite.
 // Rows with more ratings than the hub threshold have their normal equations
 // built by several wavefronts (k_gram_chunks, partials in a workspace) and are
 // only summed and solved here.
@@ -94,8 +97,12 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
 
 constexpr int kRowWaves = 4;  // independent rows per workgroup (one per wavefront)
 
+// Two wavefronts per SIMD (the second launch bound) outweigh the few registers the
+// wide widths then spill: the accumulator tiles move to arch VGPRs and the gather
+// latency of one row hides behind the other row's MFMAs.
+
 template <int DP>
-__global__ __launch_bounds__(64 * kRowWaves) void k_rows(
+__global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
     const uint8_t *__restrict__ val, const float *__restrict__ Fp, int zrow,
     const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
@@ -115,9 +122,20 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
   floatx4(&panel)[T][16] = s_panel[wv];
   float(&ud)[NPAN][12] = s_ud[wv];
 
+  // A starts as lambda n_s I on the first D diagonal entries and I on the padding;
+  // the Gram (or the sum of a split row's chunk partials) is accumulated on top
+  const float lam_n = (float)((double)lam * (double)rt.deg);
   floatx4 acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int I = 0; I < T; ++I) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int d = 16 * I + 4 * kq + r;
+      acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? (d < D ? lam_n : 1.f) : 0.f;
+    }
+  }
   float rhs[T];
 #pragma unroll
   for (int X = 0; X < T; ++X) rhs[X] = 0.f;
@@ -151,21 +169,13 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
     }
   }
 
-  // ---- A = G + lambda n I on the first D diagonal entries, identity on the padding ----
-  const float lam_n = (float)((double)lam * (double)rt.deg);
-#pragma unroll
-  for (int I = 0; I < T; ++I) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int d = 16 * I + 4 * kq + r;
-      if (c == 4 * kq + r) acc[tidx<T>(I, I)][r] = d < D ? acc[tidx<T>(I, I)][r] + lam_n : 1.f;
-    }
-  }
-
   // ---- factorisation A = U^T U with forward substitution U^T y = b ------------------------
   bool bad = false;
 #pragma unroll
   for (int I0 = 0; I0 < T; ++I0) {
+    // panels of one tile row run as a loop (unrolling them all would blow up the
+    // register allocation around the accumulator tiles)
+#pragma clang loop unroll(disable)
     for (int g = 0; g < 4; ++g) {
       const int p0 = 16 * I0 + 4 * g;
       if (p0 >= D) break;
@@ -223,7 +233,6 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
           const float Y2 = (col[2] - u02 * Y0 - u12 * Y1) * i22;
           const float Y3 = (col[3] - u03 * Y0 - u13 * Y1 - u23 * Y2) * i33;
           const int j = 16 * X + c;
-          if (kq == g && j >= p0) acc[tidx<T>(I0, X)] = floatx4{Y0, Y1, Y2, Y3};
           if (j > p0 + 3) {
             u[X] = kq == 0 ? Y0 : (kq == 1 ? Y1 : (kq == 2 ? Y2 : Y3));
             rhs[X] -= Y0 * y0 + Y1 * y1 + Y2 * y2 + Y3 * y3;
@@ -250,10 +259,11 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
   for (int X = 0; X < T; ++X) xv[X] = 0.f;
 #pragma unroll
   for (int I0 = T - 1; I0 >= 0; --I0) {
+#pragma clang loop unroll(disable)
     for (int g = 3; g >= 0; --g) {
       const int p0 = 16 * I0 + 4 * g;
       if (p0 >= D) continue;
-      // s_r = sum_{j > p0 + 3} U[p0 + r][j] x_j, partials in row group g
+      // s_r = sum_{j > p0 + 3} A_p[r][j] x_j, partials in row group g
       float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
       for (int X = I0; X < T; ++X) {
@@ -269,14 +279,21 @@ __global__ __launch_bounds__(64 * kRowWaves) void k_rows(
       s1 = sum16(s1);
       s2 = sum16(s2);
       s3 = sum16(s3);
-      const float t0 = __shfl(s0, 16 * g), t1 = __shfl(s1, 16 * g);
-      const float t2 = __shfl(s2, 16 * g), t3 = __shfl(s3, 16 * g);
+      const float a0 = __shfl(s0, 16 * g), a1 = __shfl(s1, 16 * g);
+      const float a2 = __shfl(s2, 16 * g), a3 = __shfl(s3, 16 * g);
       const float y0 = __shfl(rhs[I0], 4 * g + 0), y1 = __shfl(rhs[I0], 4 * g + 1);
       const float y2 = __shfl(rhs[I0], 4 * g + 2), y3 = __shfl(rhs[I0], 4 * g + 3);
       const int pan = p0 >> 2;
       const float i00 = ud[pan][0], u01 = ud[pan][1], u02 = ud[pan][2], u03 = ud[pan][3];
       const float i11 = ud[pan][4], u12 = ud[pan][5], u13 = ud[pan][6];
       const float i22 = ud[pan][7], u23 = ud[pan][8], i33 = ud[pan][9];
+      // the accumulators still hold the panel rows A_p as they were when the panel
+      // was factored, and U's panel rows are U_gg^{-T} A_p, so
+      // sum_j U[p0 + r][j] x_j = (U_gg^{-T} (A_p x))_r
+      const float t0 = a0 * i00;
+      const float t1 = (a1 - u01 * t0) * i11;
+      const float t2 = (a2 - u02 * t0 - u12 * t1) * i22;
+      const float t3 = (a3 - u03 * t0 - u13 * t1 - u23 * t2) * i33;
       const float x3 = (y3 - t3) * i33;
       const float x2 = (y2 - t2 - u23 * x3) * i22;
       const float x1 = (y1 - t1 - u12 * x2 - u13 * x3) * i11;
