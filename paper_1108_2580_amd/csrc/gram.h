@@ -30,12 +30,32 @@ __device__ __forceinline__ float swz_xor(float v, int x) {
   }
 }
 
+// Rotate a value right by K lanes within each 16-lane row (DPP row_ror).
+template <int K>
+__device__ __forceinline__ float row_ror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + K, 0xF, 0xF, false));
+}
+
+// Sum over the 16 lanes of a row; every lane of the row receives the same value.
 __device__ __forceinline__ float sum16(float v) {
-  v += swz_xor(v, 8);
-  v += swz_xor(v, 4);
-  v += swz_xor(v, 2);
-  v += swz_xor(v, 1);
+  v += row_ror<8>(v);
+  v += row_ror<4>(v);
+  v += row_ror<2>(v);
+  v += row_ror<1>(v);
   return v;
+}
+
+// Value of lane l (wave-uniform) broadcast to the wave through a scalar register.
+__device__ __forceinline__ float lane_value(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// 1 / sqrt(p) of a pivot, clamped to a small positive value (callers flag pivots that
+// are not positive and finite). The hardware reciprocal square root is accurate to
+// about one ulp; the exactly rounded sqrtf and division cost about 25 dependent
+// instructions per pivot on the factorisation's critical path.
+__device__ __forceinline__ float inv_sqrt_pivot(float p) {
+  return __builtin_amdgcn_rsqf(fmaxf(p, 1e-30f));
 }
 
 template <int T>

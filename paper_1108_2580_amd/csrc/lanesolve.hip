@@ -128,7 +128,7 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
   for (int k = 0; k < LD; ++k) {
     const float p = A[tri<LD>(k, k)];
     bad |= !(p > 0.f && p < INFINITY);
-    const float iv = 1.f / sqrtf(fmaxf(p, 1e-30f));
+    const float iv = inv_sqrt_pivot(p);
     A[tri<LD>(k, k)] = iv;
 #pragma unroll
     for (int j = k + 1; j < LD; ++j) A[tri<LD>(k, j)] *= iv;

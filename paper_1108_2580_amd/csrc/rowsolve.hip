@@ -195,19 +195,19 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       float p;
       p = a00;
       bad |= !(p > 0.f && p < INFINITY);
-      const float u00 = sqrtf(fmaxf(p, 1e-30f)), i00 = 1.f / u00;
+      const float i00 = inv_sqrt_pivot(p);
       const float u01 = a01 * i00, u02 = a02 * i00, u03 = a03 * i00;
       p = a11 - u01 * u01;
       bad |= !(p > 0.f && p < INFINITY);
-      const float u11 = sqrtf(fmaxf(p, 1e-30f)), i11 = 1.f / u11;
+      const float i11 = inv_sqrt_pivot(p);
       const float u12 = (a12 - u01 * u02) * i11, u13 = (a13 - u01 * u03) * i11;
       p = a22 - u02 * u02 - u12 * u12;
       bad |= !(p > 0.f && p < INFINITY);
-      const float u22 = sqrtf(fmaxf(p, 1e-30f)), i22 = 1.f / u22;
+      const float i22 = inv_sqrt_pivot(p);
       const float u23 = (a23 - u02 * u03 - u12 * u13) * i22;
       p = a33 - u03 * u03 - u13 * u13 - u23 * u23;
       bad |= !(p > 0.f && p < INFINITY);
-      const float u33 = sqrtf(fmaxf(p, 1e-30f)), i33 = 1.f / u33;
+      const float i33 = inv_sqrt_pivot(p);
       const int pan = p0 >> 2;
       if (lane == 0) {
         ud[pan][0] = i00; ud[pan][1] = u01; ud[pan][2] = u02; ud[pan][3] = u03;
@@ -215,8 +215,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
         ud[pan][7] = i22; ud[pan][8] = u23; ud[pan][9] = i33;
       }
       // right-hand side of the panel rows, from lanes c = 4g + r
-      const float b0 = __shfl(rhs[I0], 4 * g + 0), b1 = __shfl(rhs[I0], 4 * g + 1);
-      const float b2 = __shfl(rhs[I0], 4 * g + 2), b3 = __shfl(rhs[I0], 4 * g + 3);
+      const float b0 = lane_value(rhs[I0], 4 * g + 0), b1 = lane_value(rhs[I0], 4 * g + 1);
+      const float b2 = lane_value(rhs[I0], 4 * g + 2), b3 = lane_value(rhs[I0], 4 * g + 3);
       const float y0 = b0 * i00;
       const float y1 = (b1 - u01 * y0) * i11;
       const float y2 = (b2 - u02 * y0 - u12 * y1) * i22;
@@ -279,10 +279,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       s1 = sum16(s1);
       s2 = sum16(s2);
       s3 = sum16(s3);
-      const float a0 = __shfl(s0, 16 * g), a1 = __shfl(s1, 16 * g);
-      const float a2 = __shfl(s2, 16 * g), a3 = __shfl(s3, 16 * g);
-      const float y0 = __shfl(rhs[I0], 4 * g + 0), y1 = __shfl(rhs[I0], 4 * g + 1);
-      const float y2 = __shfl(rhs[I0], 4 * g + 2), y3 = __shfl(rhs[I0], 4 * g + 3);
+      const float a0 = lane_value(s0, 16 * g), a1 = lane_value(s1, 16 * g);
+      const float a2 = lane_value(s2, 16 * g), a3 = lane_value(s3, 16 * g);
+      const float y0 = lane_value(rhs[I0], 4 * g + 0), y1 = lane_value(rhs[I0], 4 * g + 1);
+      const float y2 = lane_value(rhs[I0], 4 * g + 2), y3 = lane_value(rhs[I0], 4 * g + 3);
       const int pan = p0 >> 2;
       const float i00 = ud[pan][0], u01 = ud[pan][1], u02 = ud[pan][2], u03 = ud[pan][3];
       const float i11 = ud[pan][4], u12 = ud[pan][5], u13 = ud[pan][6];
