@@ -67,15 +67,120 @@ template <int DP>
 struct RowCfg {
   static constexpr int T = DP / 16;
   static constexpr int NT = T * (T + 1) / 2;
-  static constexpr int STEPS = T <= 2 ? 16 : (T <= 4 ? 8 : 4);  // steps whose loads are batched
+  // steps per gathered block (wide rows keep two blocks in flight)
+  static constexpr int STEPS = T <= 2 ? 16 : (T <= 4 ? 8 : (T <= 6 ? 4 : 2));
 };
 
-// Accumulate the item's Gram tiles and right-hand side (per-lane partials over
-// the four rating groups) and the entering-state squared residuals.
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
+template <int B, int NB, class F>
+__device__ __forceinline__ void unroll_blocks(F &f) {
+  if constexpr (B < NB) {
+    f(IntC<B>{});
+    unroll_blocks<B + 1, NB>(f);
+  }
+}
+
+// Gather the staged fixed rows of steps s0 .. s0 + STEPS - 1 of a 64-rating group:
+// lane (kq, c) receives feature 16 X + c of rating 4 s + kq. jsrc / rsrc hold the
+// group's column indices and ratings, one per lane.
+// Loads are never predicated per lane (a predicated load becomes a branch that waits
+// for its own completion, which serialises the gathers): ratings past the end of the
+// item and padded features read the staged all-zero row zrow. Byte offsets are 32-bit
+// from the (uniform) table base.
+template <int DP, int STEPS>
+__device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
+                                             int jsrc, float rsrc, int s0,
+                                             const float *__restrict__ Fp, int zrow, int D) {
+  constexpr int T = DP / 16;
+  const int lane = threadIdx.x & 63;
+  const int kq = lane >> 4, c = lane & 15;
+#pragma unroll
+  for (int u = 0; u < STEPS; ++u) {
+    const int src = 4 * (s0 + u) + kq;
+    const int j = __shfl(jsrc, src);
+    r[u] = __shfl(rsrc, src);
+#pragma unroll
+    for (int X = 0; X < T; ++X) {
+      const int jr = (X < T - 1 || 16 * X + c < D) ? j : zrow;
+      const uint32_t off = (uint32_t)jr * (uint32_t)(DP * 4) + (uint32_t)((16 * X + c) * 4);
+      a[u][X] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(Fp) + off);
+    }
+  }
+}
+
+// MFMA Gram update, right-hand side and per-step partial predictions of the gathered
+// steps s0 .. s0 + STEPS - 1, in sub-blocks of up to four steps; sub-blocks past the
+// item's last step (steps of this group) are skipped.
+template <int DP, int STEPS>
+__device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
+                                          float (&rhs)[DP / 16], const float (&xo)[DP / 16],
+                                          float (&pi)[16], const float (&a)[STEPS][DP / 16],
+                                          const float (&r)[STEPS], int s0, int steps) {
+  constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
+#pragma unroll
+  for (int u0 = 0; u0 < STEPS; u0 += SUB) {
+    if (s0 + u0 < steps) {
+#pragma unroll
+      for (int u = u0; u < u0 + SUB; ++u) {
+#pragma unroll
+        for (int X = 0; X < T; ++X) {
+          rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
+          pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
+        }
+#pragma unroll
+        for (int I = 0; I < T; ++I) {
+#pragma unroll
+          for (int J = I; J < T; ++J)
+            acc[tidx<T>(I, J)] =
+                __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// End of a 64-rating group: reduce-scatter the 16 step partials over the 16 feature
+// lanes, after which lane c holds the full prediction of step c for its rating group
+// (both halves are exchanged and the lane keeps the sum of its half; selecting between
+// computed sums keeps the partial array statically indexed), and add the squared
+// residuals of the group's ratings.
+__device__ __forceinline__ void group_residuals(float (&pi)[16], float rv, int g, int n,
+                                                double &sse) {
+  const int lane = threadIdx.x & 63;
+  const int kq = lane >> 4, c = lane & 15;
+#pragma unroll
+  for (int o = 8, m = 16; o >= 1; o >>= 1, m >>= 1) {
+    const bool hi = (c & o) != 0;
+#pragma unroll
+    for (int i = 0; i < m / 2; ++i) {
+      const float lo_sum = pi[i] + swz_xor(pi[i], o);
+      const float hi_sum = pi[m / 2 + i] + swz_xor(pi[m / 2 + i], o);
+      pi[i] = hi ? hi_sum : lo_sum;
+    }
+  }
+  // lane (kq, c) now holds the prediction of rating g + 4c + kq, whose value sits in
+  // lane 4c + kq of this group's rating register
+  const float rq = __shfl(rv, 4 * c + kq);
+  if (g + 4 * c + kq < n) {
+    const double e = (double)rq - (double)pi[0];
+    sse = fma(e, e, sse);
+  }
+}
+
+// Accumulate the item's Gram tiles and right-hand side (per-lane partials over the
+// four rating groups) and the entering-state squared residuals.
 // xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
-// Ratings are taken in groups of 64; within a group the loads of all steps are
-// issued first and the MFMAs follow in blocks of four steps, so that only the
-// last block of an item carries padding.
+// Ratings are taken in groups of 64, each gathered in blocks of STEPS steps (four
+// ratings per step).
+//  - Narrow rows (T <= 2): one block per group, gathered and then multiplied.
+//  - Wider rows: two block buffers; the gather of the next block (of this group, or
+//    the first block of the next group) is issued before the MFMAs of the current
+//    one, so that its latency hides behind them. The blocks of the last group that
+//    lie past the item's end are still gathered (from the zero row) but not multiplied.
 template <int DP>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
@@ -84,90 +189,66 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 const uint8_t *__restrict__ vp, int n,
                                                 const float *__restrict__ Fp, int zrow, int D) {
   using C = RowCfg<DP>;
-  constexpr int T = C::T, STEPS = C::STEPS;
+  constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
-  const int kq = lane >> 4, c = lane & 15;
-  // Loads are never predicated per lane (a predicated load becomes a branch that
-  // waits for its own completion, which serialises the gathers): indices past the
-  // end are clamped and their values discarded, and ratings past the end of the
-  // item, as well as padded features, read the staged all-zero row zrow.
   int jv = lane < n ? ip[lane] : zrow;
   float rv = (float)vp[min(lane, n - 1)];
   rv = lane < n ? rv : 0.f;
-  for (int g = 0; g < n; g += 64) {
-    const int gn = g + 64 + lane;
-    const int jl = ip[min(gn, n - 1)];
-    const float rl = (float)vp[min(gn, n - 1)];
-    const int jn = gn < n ? jl : zrow;
-    const float rn = gn < n ? rl : 0.f;
-    const int steps = min(16, (n - g + 3) >> 2);
-    float pi[16];  // per-step partial predictions of this lane's rating group
+  if constexpr (T <= 2) {
+    for (int g = 0; g < n; g += 64) {
+      const int gn = g + 64 + lane;
+      const int jl = ip[min(gn, n - 1)];
+      const float rl = (float)vp[min(gn, n - 1)];
+      const int jn = gn < n ? jl : zrow;
+      const float rn = gn < n ? rl : 0.f;
+      const int steps = min(16, (n - g + 3) >> 2);
+      float pi[16];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) pi[u] = 0.f;
+      for (int u = 0; u < 16; ++u) pi[u] = 0.f;
 #pragma unroll
-    for (int s0 = 0; s0 < 16; s0 += STEPS) {
-      if (s0 < steps) {
-        float a[STEPS][T];
-        float r[STEPS];
-#pragma unroll
-        for (int u = 0; u < STEPS; ++u) {
-          const int src = 4 * (s0 + u) + kq;
-          const int j = __shfl(jv, src);
-          r[u] = __shfl(rv, src);
-          // 32-bit byte offsets from the (uniform) table base; every block but the
-          // last holds real features only
-#pragma unroll
-          for (int X = 0; X < T; ++X) {
-            const int jr = (X < T - 1 || 16 * X + c < D) ? j : zrow;
-            const uint32_t off = (uint32_t)jr * (uint32_t)(DP * 4) + (uint32_t)((16 * X + c) * 4);
-            a[u][X] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(Fp) + off);
-          }
-        }
-#pragma unroll
-        for (int u0 = 0; u0 < STEPS; u0 += 4) {
-          if (s0 + u0 < steps) {
-#pragma unroll
-            for (int u = u0; u < u0 + 4; ++u) {
-#pragma unroll
-              for (int X = 0; X < T; ++X) {
-                rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
-                pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
-              }
-#pragma unroll
-              for (int I = 0; I < T; ++I) {
-#pragma unroll
-                for (int J = I; J < T; ++J)
-                  acc[tidx<T>(I, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                      a[u][I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
-              }
-            }
-          }
+      for (int s0 = 0; s0 < 16; s0 += STEPS) {
+        if (s0 < steps) {
+          float a[STEPS][T];
+          float r[STEPS];
+          gather_block<DP, STEPS>(a, r, jv, rv, s0, Fp, zrow, D);
+          mma_block<DP, STEPS>(acc, rhs, xo, pi, a, r, s0, steps);
         }
       }
+      group_residuals(pi, rv, g, n, sse);
+      jv = jn;
+      rv = rn;
     }
-    // reduce-scatter the 16 step partials over the 16 feature lanes: afterwards
-    // lane c holds the full prediction of step c for its rating group
-    // (both halves are exchanged and the lane keeps the sum of its half; selecting
-    // between computed sums keeps the partial array statically indexed)
+  } else {
+    static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
+    float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS];
+    gather_block<DP, STEPS>(a0, r0, jv, rv, 0, Fp, zrow, D);
+    for (int g = 0; g < n; g += 64) {
+      const int gn = g + 64 + lane;
+      const int jl = ip[min(gn, n - 1)];
+      const float rl = (float)vp[min(gn, n - 1)];
+      const int jn = gn < n ? jl : zrow;
+      const float rn = gn < n ? rl : 0.f;
+      const int steps = min(16, (n - g + 3) >> 2);
+      float pi[16];
 #pragma unroll
-    for (int o = 8, m = 16; o >= 1; o >>= 1, m >>= 1) {
-      const bool hi = (c & o) != 0;
-#pragma unroll
-      for (int i = 0; i < m / 2; ++i) {
-        const float lo_sum = pi[i] + swz_xor(pi[i], o);
-        const float hi_sum = pi[m / 2 + i] + swz_xor(pi[m / 2 + i], o);
-        pi[i] = hi ? hi_sum : lo_sum;
-      }
+      for (int u = 0; u < 16; ++u) pi[u] = 0.f;
+      auto block = [&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        constexpr int s0 = b * STEPS;
+        if constexpr (b % 2 == 0) {
+          if constexpr (b + 1 < NB) gather_block<DP, STEPS>(a1, r1, jv, rv, s0 + STEPS, Fp, zrow, D);
+          mma_block<DP, STEPS>(acc, rhs, xo, pi, a0, r0, s0, steps);
+        } else {
+          if constexpr (b + 1 < NB) gather_block<DP, STEPS>(a0, r0, jv, rv, s0 + STEPS, Fp, zrow, D);
+          else gather_block<DP, STEPS>(a0, r0, jn, rn, 0, Fp, zrow, D);
+          mma_block<DP, STEPS>(acc, rhs, xo, pi, a1, r1, s0, steps);
+        }
+      };
+      unroll_blocks<0, NB>(block);
+      group_residuals(pi, rv, g, n, sse);
+      jv = jn;
+      rv = rn;
     }
-    // lane (kq, c) now holds the prediction of rating g + 4c + kq, whose value sits
-    // in lane 4c + kq of this group's rating register
-    const float rq = __shfl(rv, 4 * c + kq);
-    if (g + 4 * c + kq < n) {
-      const double e = (double)rq - (double)pi[0];
-      sse = fma(e, e, sse);
-    }
-    jv = jn;
-    rv = rn;
   }
 }
 

@@ -241,9 +241,19 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
           }
         }
       }
-      // (4) trailing update on MFMA: A_IJ -= U_p(:, I)^T U_p(:, J)
+      // (4) trailing update on MFMA: A_IJ -= U_p(:, I)^T U_p(:, J). The tile row that the
+      // next panel publishes is issued first, so that the next panel's factorisation runs
+      // while the matrix unit works through the rest. After the last panel of a tile row
+      // (g == 3) that row has no unfactored rows left and its update is skipped.
+      if (g < 3) {
 #pragma unroll
-      for (int I = I0; I < T; ++I) {
+        for (int J = I0; J < T; ++J)
+          acc[tidx<T>(I0, J)] =
+              __builtin_amdgcn_mfma_f32_16x16x4f32(-u[I0], u[J], acc[tidx<T>(I0, J)], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int I = I0 + 1; I < T; ++I) {
 #pragma unroll
         for (int J = I; J < T; ++J)
           acc[tidx<T>(I, J)] =
