@@ -89,12 +89,16 @@ __device__ __forceinline__ void unroll_blocks(F &f) {
 // group's column indices and ratings, one per lane.
 // Loads are never predicated per lane (a predicated load becomes a branch that waits
 // for its own completion, which serialises the gathers): ratings past the end of the
-// item and padded features read the staged all-zero row zrow. Byte offsets are 32-bit
-// from the (uniform) table base.
-template <int DP, int STEPS>
+// item read the staged all-zero row, and padded features read the staged row's zero
+// padding. One 32-bit byte offset per step from the (uniform) table base; the tiles
+// follow at immediate offsets.
+// With AUG, lane column aug_c of the last tile carries the rating instead of the
+// (zero) padded feature, so that the MFMA Gram also accumulates b = sum r f in that
+// column (and sum r^2 on its diagonal).
+template <int DP, int STEPS, bool AUG>
 __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
                                              int jsrc, float rsrc, int s0,
-                                             const float *__restrict__ Fp, int zrow, int D) {
+                                             const float *__restrict__ Fp, bool aug_lane) {
   constexpr int T = DP / 16;
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
@@ -103,19 +107,19 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
     const int src = 4 * (s0 + u) + kq;
     const int j = __shfl(jsrc, src);
     r[u] = __shfl(rsrc, src);
+    const uint32_t off = (uint32_t)j * (uint32_t)(DP * 4) + (uint32_t)(c * 4);
+    const char *row = reinterpret_cast<const char *>(Fp) + (uint64_t)off;
 #pragma unroll
-    for (int X = 0; X < T; ++X) {
-      const int jr = (X < T - 1 || 16 * X + c < D) ? j : zrow;
-      const uint32_t off = (uint32_t)jr * (uint32_t)(DP * 4) + (uint32_t)((16 * X + c) * 4);
-      a[u][X] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(Fp) + off);
-    }
+    for (int X = 0; X < T; ++X) a[u][X] = *reinterpret_cast<const float *>(row + 64 * X);
+    if constexpr (AUG) a[u][T - 1] = aug_lane ? r[u] : a[u][T - 1];
   }
 }
 
 // MFMA Gram update, right-hand side and per-step partial predictions of the gathered
 // steps s0 .. s0 + STEPS - 1, in sub-blocks of up to four steps; sub-blocks past the
-// item's last step (steps of this group) are skipped.
-template <int DP, int STEPS>
+// item's last step (steps of this group) are skipped. With AUG the right-hand side is
+// a column of the Gram and rhs is left alone.
+template <int DP, int STEPS, bool AUG>
 __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float (&rhs)[DP / 16], const float (&xo)[DP / 16],
                                           float (&pi)[16], const float (&a)[STEPS][DP / 16],
@@ -128,7 +132,7 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
       for (int u = u0; u < u0 + SUB; ++u) {
 #pragma unroll
         for (int X = 0; X < T; ++X) {
-          rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
+          if constexpr (!AUG) rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
           pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
         }
 #pragma unroll
@@ -171,8 +175,10 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], float rv, int g
   }
 }
 
-// Accumulate the item's Gram tiles and right-hand side (per-lane partials over the
-// four rating groups) and the entering-state squared residuals.
+// Accumulate the item's Gram tiles and right-hand side and the entering-state squared
+// residuals. Without AUG the right-hand side is kept in rhs as per-lane partials over
+// the four rating groups; with AUG it is the Gram's column 16 (T - 1) + aug_c (a padding
+// column whose lane carries the ratings) and rhs is untouched.
 // xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
 // Ratings are taken in groups of 64, each gathered in blocks of STEPS steps (four
 // ratings per step).
@@ -181,16 +187,18 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], float rv, int g
 //    the first block of the next group) is issued before the MFMAs of the current
 //    one, so that its latency hides behind them. The blocks of the last group that
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
-template <int DP>
+template <int DP, bool AUG>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
                                                 const float (&xo)[RowCfg<DP>::T], double &sse,
                                                 const int32_t *__restrict__ ip,
                                                 const uint8_t *__restrict__ vp, int n,
-                                                const float *__restrict__ Fp, int zrow, int D) {
+                                                const float *__restrict__ Fp, int zrow,
+                                                int aug_c) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
+  const bool aug_lane = (lane & 15) == aug_c;
   int jv = lane < n ? ip[lane] : zrow;
   float rv = (float)vp[min(lane, n - 1)];
   rv = lane < n ? rv : 0.f;
@@ -202,6 +210,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
       const int jn = gn < n ? jl : zrow;
       const float rn = gn < n ? rl : 0.f;
       const int steps = min(16, (n - g + 3) >> 2);
+      __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
       float pi[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) pi[u] = 0.f;
@@ -210,8 +219,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         if (s0 < steps) {
           float a[STEPS][T];
           float r[STEPS];
-          gather_block<DP, STEPS>(a, r, jv, rv, s0, Fp, zrow, D);
-          mma_block<DP, STEPS>(acc, rhs, xo, pi, a, r, s0, steps);
+          gather_block<DP, STEPS, AUG>(a, r, jv, rv, s0, Fp, aug_lane);
+          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a, r, s0, steps);
         }
       }
       group_residuals(pi, rv, g, n, sse);
@@ -221,7 +230,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
   } else {
     static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
     float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS];
-    gather_block<DP, STEPS>(a0, r0, jv, rv, 0, Fp, zrow, D);
+    gather_block<DP, STEPS, AUG>(a0, r0, jv, rv, 0, Fp, aug_lane);
     for (int g = 0; g < n; g += 64) {
       const int gn = g + 64 + lane;
       const int jl = ip[min(gn, n - 1)];
@@ -229,6 +238,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
       const int jn = gn < n ? jl : zrow;
       const float rn = gn < n ? rl : 0.f;
       const int steps = min(16, (n - g + 3) >> 2);
+      __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
       float pi[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) pi[u] = 0.f;
@@ -236,12 +246,12 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         constexpr int b = decltype(bc)::value;
         constexpr int s0 = b * STEPS;
         if constexpr (b % 2 == 0) {
-          if constexpr (b + 1 < NB) gather_block<DP, STEPS>(a1, r1, jv, rv, s0 + STEPS, Fp, zrow, D);
-          mma_block<DP, STEPS>(acc, rhs, xo, pi, a0, r0, s0, steps);
+          if constexpr (b + 1 < NB) gather_block<DP, STEPS, AUG>(a1, r1, jv, rv, s0 + STEPS, Fp, aug_lane);
+          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a0, r0, s0, steps);
         } else {
-          if constexpr (b + 1 < NB) gather_block<DP, STEPS>(a0, r0, jv, rv, s0 + STEPS, Fp, zrow, D);
-          else gather_block<DP, STEPS>(a0, r0, jn, rn, 0, Fp, zrow, D);
-          mma_block<DP, STEPS>(acc, rhs, xo, pi, a1, r1, s0, steps);
+          if constexpr (b + 1 < NB) gather_block<DP, STEPS, AUG>(a0, r0, jv, rv, s0 + STEPS, Fp, aug_lane);
+          else gather_block<DP, STEPS, AUG>(a0, r0, jn, rn, 0, Fp, aug_lane);
+          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a1, r1, s0, steps);
         }
       };
       unroll_blocks<0, NB>(block);

@@ -25,7 +25,10 @@ __host__ __device__ constexpr int tri(int a, int b) {  // a <= b, row-major uppe
   return a * LD - a * (a - 1) / 2 + (b - a);
 }
 
-template <int DP, int LD>
+// AUG (used for D = 17..20, LD = 20): the ratings ride in padding feature 20 of the
+// gathered rows, so the MFMA Gram delivers b in column 20 (tile column 4 of the last
+// tile) and the per-rating right-hand-side FMAs disappear.
+template <int DP, int LD, bool AUG>
 __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ items,
                                                 int64_t n_chunk_items,
                                                 const int32_t *__restrict__ idx,
@@ -38,6 +41,8 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   constexpr int T = C::T, NT = C::NT;
   constexpr int NTRI = LD * (LD + 1) / 2;
   constexpr int NES = ne_floats(LD);
+  static_assert(!AUG || (LD < DP && LD > 16 * (T - 1) && LD % 4 == 0),
+                "the augmented column is feature LD of the last tile");
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
   floatx4 acc[NT];
@@ -53,11 +58,14 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
     }
   }
   double sse = 0.0;
-  gram_accumulate<DP>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow, D);
+  gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
+                           AUG ? LD - 16 * (T - 1) : -1);
+  if constexpr (!AUG) {
 #pragma unroll
-  for (int X = 0; X < T; ++X) {
-    rhs[X] += __shfl_xor(rhs[X], 16);
-    rhs[X] += __shfl_xor(rhs[X], 32);
+    for (int X = 0; X < T; ++X) {
+      rhs[X] += __shfl_xor(rhs[X], 16);
+      rhs[X] += __shfl_xor(rhs[X], 32);
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
@@ -70,13 +78,19 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
       for (int r = 0; r < 4; ++r) {
         const int a = 16 * I + 4 * kq + r, b = 16 * J + c;
         if (a <= b && b < LD) out[tri<LD>(a, b)] = acc[tidx<T>(I, J)][r];
+        if constexpr (AUG) {
+          // b_a = G[a][LD] sits in tile (I, T - 1), lane column LD - 16 (T - 1)
+          if (J == T - 1 && b == LD && a < LD) out[NTRI + a] = acc[tidx<T>(I, J)][r];
+        }
       }
     }
   }
-  if (kq == 0) {
+  if constexpr (!AUG) {
+    if (kq == 0) {
 #pragma unroll
-    for (int X = 0; X < T; ++X)
-      if (16 * X + c < LD) out[NTRI + 16 * X + c] = rhs[X];
+      for (int X = 0; X < T; ++X)
+        if (16 * X + c < LD) out[NTRI + 16 * X + c] = rhs[X];
+    }
   }
   if (lane == 0) sse_out[blockIdx.x] = sse;
 }
@@ -174,10 +188,10 @@ hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t
   const int zrow = (int)n_fixed;
   const int ld = lane_width(D);
   if (ld == 16)
-    hipLaunchKernelGGL((k_gram_ne<16, 16>), dim3((unsigned)n_items), dim3(64), 0, s, items,
+    hipLaunchKernelGGL((k_gram_ne<16, 16, false>), dim3((unsigned)n_items), dim3(64), 0, s, items,
                        n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
   else if (ld == 20)
-    hipLaunchKernelGGL((k_gram_ne<32, 20>), dim3((unsigned)n_items), dim3(64), 0, s, items,
+    hipLaunchKernelGGL((k_gram_ne<32, 20, true>), dim3((unsigned)n_items), dim3(64), 0, s, items,
                        n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
   else
     return hipErrorInvalidValue;

@@ -7,14 +7,14 @@
 //      half-sweep (x_s = the row's previous value) for the training RMSE
 //      (Sec. 4.1);
 //   2. factors A = U^T U (lambda n_s I is the accumulators' initial value) in
-//      panels of four rows: the 4x4 diagonal block is factored in every lane,
-//      the panel rows of U are formed by a 4x4 triangular solve per column, and
-//      the trailing tiles are updated on MFMA (K = 4). The accumulators are only
-//      written by MFMA and read by VALU, so they stay in accumulator registers;
-//   3. forward substitution of b rides along the panels; back substitution
-//      follows, forming U's panel rows from the untouched A_p rows and the
-//      stored 4x4 blocks; x_s is written unless a pivot was not positive and
-//      finite.
+//      panels of four rows: the 4x4 diagonal block is factored in every lane and
+//      inverted (M = U_gg^{-T}), each lane forms its panel row of U with one
+//      4-term dot product per tile, and the trailing tiles are updated on MFMA
+//      (K = 4). The accumulators are only written by MFMA and read by VALU;
+//   3. forward substitution of b rides along the panels (as a column of the
+//      matrix when a padding feature can carry it); back substitution follows,
+//      from the untouched panel rows A_p and the stored M blocks; x_s is written
+//      unless a pivot was not positive and finite.
 // Rows with more ratings than the hub threshold have their normal equations
 // built by several wavefronts (k_gram_chunks, partials in a workspace) and are
 // only summed and solved here.
@@ -50,9 +50,18 @@ hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *F
   return hipGetLastError();
 }
 
+// The augmented column: when DA = 4 ceil(D / 4) is a padding feature (DA < DP), the
+// gathered rows carry the rating in feature DA, so the Gram's column DA is b = sum r f
+// and the elimination of A = U^T U carries b along as y = U^{-T} b. DA always falls in
+// the last tile; aug_c is its lane column there.
+template <int DP>
+__host__ __device__ constexpr int aug_column(int D) {
+  return ((D + 3) & ~3) - 16 * (DP / 16 - 1);
+}
+
 // Partial normal equations of the chunks of split rows, with the chunks'
 // entering-state squared residuals.
-template <int DP>
+template <int DP, bool AUG>
 __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__ items,
                                                     const int32_t *__restrict__ idx,
                                                     const uint8_t *__restrict__ val,
@@ -77,20 +86,23 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
     }
   }
   double sse = 0.0;
-  gram_accumulate<DP>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow, D);
-#pragma unroll
-  for (int X = 0; X < T; ++X) {
-    rhs[X] += __shfl_xor(rhs[X], 16);
-    rhs[X] += __shfl_xor(rhs[X], 32);
-  }
+  gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
+                           AUG ? aug_column<DP>(D) : -1);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
 #pragma unroll
   for (int t = 0; t < NT; ++t) *reinterpret_cast<floatx4 *>(out + t * 256 + lane * 4) = acc[t];
-  if (kq == 0) {
+  if constexpr (!AUG) {
 #pragma unroll
-    for (int X = 0; X < T; ++X) out[NT * 256 + 16 * X + c] = rhs[X];
+    for (int X = 0; X < T; ++X) {
+      rhs[X] += __shfl_xor(rhs[X], 16);
+      rhs[X] += __shfl_xor(rhs[X], 32);
+    }
+    if (kq == 0) {
+#pragma unroll
+      for (int X = 0; X < T; ++X) out[NT * 256 + 16 * X + c] = rhs[X];
+    }
   }
   if (lane == 0) sse_out[blockIdx.x] = sse;
 }
@@ -100,8 +112,15 @@ constexpr int kRowWaves = 4;  // independent rows per workgroup (one per wavefro
 // Two wavefronts per SIMD (the second launch bound) outweigh the few registers the
 // wide widths then spill: the accumulator tiles move to arch VGPRs and the gather
 // latency of one row hides behind the other row's MFMAs.
-
-template <int DP>
+//
+// Panel step (rows p0 .. p0 + 3, held by row group g of tile row I0):
+//   the 4x4 diagonal block A_gg = U_gg^T U_gg is factored in every lane and
+//   M = U_gg^{-T} formed explicitly (10 entries); lane (kq, c) then forms the panel
+//   row U[p0 + kq][j] = sum_r M[kq][r] A[p0 + r][j] for its columns j = 16 X + c
+//   with one 4-term dot product per tile, and the trailing tiles are updated on MFMA
+//   (K = 4). Without the augmented column the right-hand side is eliminated along:
+//   y_p = M b_p, and b_j -= sum_r A[p0 + r][j] (M^T y_p)_r for the later columns.
+template <int DP, bool AUG>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
     const uint8_t *__restrict__ val, const float *__restrict__ Fp, int zrow,
@@ -112,7 +131,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   constexpr int T = C::T, NT = C::NT;
   constexpr int NPAN = DP / 4;
   __shared__ floatx4 s_panel[kRowWaves][T][16];  // one panel's rows, per tile column and lane column
-  __shared__ float s_ud[kRowWaves][NPAN][12];    // per panel: 4x4 U block (10) + spare
+  __shared__ float s_ud[kRowWaves][NPAN][16];    // per panel: M (10 entries) and y_p (4)
 
   const int wv = threadIdx.x >> 6;
   const int64_t task = (int64_t)blockIdx.x * kRowWaves + wv;
@@ -120,7 +139,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   const RowTask rt = rows[task];
   const int lane = threadIdx.x & 63, kq = lane >> 4, c = lane & 15;
   floatx4(&panel)[T][16] = s_panel[wv];
-  float(&ud)[NPAN][12] = s_ud[wv];
+  float(&ud)[NPAN][16] = s_ud[wv];
+  const int aug_c = AUG ? aug_column<DP>(D) : -1;
 
   // A starts as lambda n_s I on the first D diagonal entries and I on the padding;
   // the Gram (or the sum of a split row's chunk partials) is accumulated on top
@@ -149,11 +169,14 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       xo[X] = 16 * X + c < D ? v : 0.f;
     }
     double sse = 0.0;
-    gram_accumulate<DP>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow, D);
+    gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow,
+                             aug_c);
+    if constexpr (!AUG) {
 #pragma unroll
-    for (int X = 0; X < T; ++X) {
-      rhs[X] += __shfl_xor(rhs[X], 16);
-      rhs[X] += __shfl_xor(rhs[X], 32);
+      for (int X = 0; X < T; ++X) {
+        rhs[X] += __shfl_xor(rhs[X], 16);
+        rhs[X] += __shfl_xor(rhs[X], 32);
+      }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
@@ -164,8 +187,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       const float *__restrict__ sl = base + s * (int64_t)slot_floats(DP);
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] += *reinterpret_cast<const floatx4 *>(sl + t * 256 + lane * 4);
+      if constexpr (!AUG) {
 #pragma unroll
-      for (int X = 0; X < T; ++X) rhs[X] += sl[NT * 256 + 16 * X + c];
+        for (int X = 0; X < T; ++X) rhs[X] += sl[NT * 256 + 16 * X + c];
+      }
     }
   }
 
@@ -208,38 +233,63 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       p = a33 - u03 * u03 - u13 * u13 - u23 * u23;
       bad |= !(p > 0.f && p < INFINITY);
       const float i33 = inv_sqrt_pivot(p);
+      // M = U_gg^{-T} (lower triangular; diagonal 1 / u_qq)
+      const float m00 = i00;
+      const float m10 = -(u01 * m00) * i11, m11 = i11;
+      const float m20 = -(u02 * m00 + u12 * m10) * i22, m21 = -(u12 * m11) * i22, m22 = i22;
+      const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
+      const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
+      // this lane's row of M
+      const float w0 = kq == 0 ? m00 : (kq == 1 ? m10 : (kq == 2 ? m20 : m30));
+      const float w1 = kq == 0 ? 0.f : (kq == 1 ? m11 : (kq == 2 ? m21 : m31));
+      const float w2 = kq <= 1 ? 0.f : (kq == 2 ? m22 : m32);
+      const float w3 = kq == 3 ? m33 : 0.f;
       const int pan = p0 >> 2;
-      if (lane == 0) {
-        ud[pan][0] = i00; ud[pan][1] = u01; ud[pan][2] = u02; ud[pan][3] = u03;
-        ud[pan][4] = i11; ud[pan][5] = u12; ud[pan][6] = u13;
-        ud[pan][7] = i22; ud[pan][8] = u23; ud[pan][9] = i33;
+      float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+      if constexpr (!AUG) {
+        // y_p = M b_p, and the weights v = M^T y_p of the right-hand-side update
+        const float b0 = lane_value(rhs[I0], 4 * g + 0), b1 = lane_value(rhs[I0], 4 * g + 1);
+        const float b2 = lane_value(rhs[I0], 4 * g + 2), b3 = lane_value(rhs[I0], 4 * g + 3);
+        const float y0 = m00 * b0;
+        const float y1 = m10 * b0 + m11 * b1;
+        const float y2 = m20 * b0 + m21 * b1 + m22 * b2;
+        const float y3 = m30 * b0 + m31 * b1 + m32 * b2 + m33 * b3;
+        v0 = m00 * y0 + m10 * y1 + m20 * y2 + m30 * y3;
+        v1 = m11 * y1 + m21 * y2 + m31 * y3;
+        v2 = m22 * y2 + m32 * y3;
+        v3 = m33 * y3;
+        if (lane == 0) {
+          ud[pan][10] = y0; ud[pan][11] = y1; ud[pan][12] = y2; ud[pan][13] = y3;
+        }
       }
-      // right-hand side of the panel rows, from lanes c = 4g + r
-      const float b0 = lane_value(rhs[I0], 4 * g + 0), b1 = lane_value(rhs[I0], 4 * g + 1);
-      const float b2 = lane_value(rhs[I0], 4 * g + 2), b3 = lane_value(rhs[I0], 4 * g + 3);
-      const float y0 = b0 * i00;
-      const float y1 = (b1 - u01 * y0) * i11;
-      const float y2 = (b2 - u02 * y0 - u12 * y1) * i22;
-      const float y3 = (b3 - u03 * y0 - u13 * y1 - u23 * y2) * i33;
-      // (3) panel rows U[p0 + q][j] = (U^{-T} A[p0.., j])_q and trailing operands
+      if (lane == 0) {
+        ud[pan][0] = m00; ud[pan][1] = m10; ud[pan][2] = m11; ud[pan][3] = m20;
+        ud[pan][4] = m21; ud[pan][5] = m22; ud[pan][6] = m30; ud[pan][7] = m31;
+        ud[pan][8] = m32; ud[pan][9] = m33;
+      }
+      // (3) panel rows U[p0 + kq][j] = (M A_p)[kq][j] for the later columns j (zero for
+      // j <= p0 + 3, which keeps the finished rows and columns out of the update)
       float u[T];
 #pragma unroll
       for (int X = 0; X < T; ++X) {
         u[X] = 0.f;
         if (X >= I0) {
           const floatx4 col = panel[X][c];
-          const float Y0 = col[0] * i00;
-          const float Y1 = (col[1] - u01 * Y0) * i11;
-          const float Y2 = (col[2] - u02 * Y0 - u12 * Y1) * i22;
-          const float Y3 = (col[3] - u03 * Y0 - u13 * Y1 - u23 * Y2) * i33;
+          float Y = w0 * col[0];
+          Y = fmaf(w1, col[1], Y);
+          Y = fmaf(w2, col[2], Y);
+          Y = fmaf(w3, col[3], Y);
           const int j = 16 * X + c;
-          if (j > p0 + 3) {
-            u[X] = kq == 0 ? Y0 : (kq == 1 ? Y1 : (kq == 2 ? Y2 : Y3));
-            rhs[X] -= Y0 * y0 + Y1 * y1 + Y2 * y2 + Y3 * y3;
-          } else if (j >= p0) {
-            rhs[X] = j == p0 ? y0 : (j == p0 + 1 ? y1 : (j == p0 + 2 ? y2 : y3));
+          if (X == I0) Y = j > p0 + 3 ? Y : 0.f;
+          if constexpr (!AUG) {
+            if (j > p0 + 3) rhs[X] -= v0 * col[0] + v1 * col[1] + v2 * col[2] + v3 * col[3];
           }
+          u[X] = Y;
         }
+      }
+      if constexpr (AUG) {
+        // the augmented column's panel entries are y_p = U_gg^{-T} b_p
+        if (c == aug_c) ud[pan][10 + kq] = u[T - 1];
       }
       // (4) trailing update on MFMA: A_IJ -= U_p(:, I)^T U_p(:, J). The tile row that the
       // next panel publishes is issued first, so that the next panel's factorisation runs
@@ -263,7 +313,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     }
   }
 
-  // ---- back substitution U x = y (rhs holds y) ----------------------------------------------
+  // ---- back substitution U x = y --------------------------------------------------------
+  // Panel p: U_gg x_p = y_p - U_p,rest x_rest with U_p,rest = M A_p,rest, where the
+  // accumulators still hold the panel rows A_p as they were when the panel was factored
+  // (later updates leave finished rows alone); so x_p = M^T (y_p - M (A_p,rest x_rest)).
   float xv[T];
 #pragma unroll
   for (int X = 0; X < T; ++X) xv[X] = 0.f;
@@ -291,23 +344,18 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       s3 = sum16(s3);
       const float a0 = lane_value(s0, 16 * g), a1 = lane_value(s1, 16 * g);
       const float a2 = lane_value(s2, 16 * g), a3 = lane_value(s3, 16 * g);
-      const float y0 = lane_value(rhs[I0], 4 * g + 0), y1 = lane_value(rhs[I0], 4 * g + 1);
-      const float y2 = lane_value(rhs[I0], 4 * g + 2), y3 = lane_value(rhs[I0], 4 * g + 3);
       const int pan = p0 >> 2;
-      const float i00 = ud[pan][0], u01 = ud[pan][1], u02 = ud[pan][2], u03 = ud[pan][3];
-      const float i11 = ud[pan][4], u12 = ud[pan][5], u13 = ud[pan][6];
-      const float i22 = ud[pan][7], u23 = ud[pan][8], i33 = ud[pan][9];
-      // the accumulators still hold the panel rows A_p as they were when the panel
-      // was factored, and U's panel rows are U_gg^{-T} A_p, so
-      // sum_j U[p0 + r][j] x_j = (U_gg^{-T} (A_p x))_r
-      const float t0 = a0 * i00;
-      const float t1 = (a1 - u01 * t0) * i11;
-      const float t2 = (a2 - u02 * t0 - u12 * t1) * i22;
-      const float t3 = (a3 - u03 * t0 - u13 * t1 - u23 * t2) * i33;
-      const float x3 = (y3 - t3) * i33;
-      const float x2 = (y2 - t2 - u23 * x3) * i22;
-      const float x1 = (y1 - t1 - u12 * x2 - u13 * x3) * i11;
-      const float x0 = (y0 - t0 - u01 * x1 - u02 * x2 - u03 * x3) * i00;
+      const float m00 = ud[pan][0], m10 = ud[pan][1], m11 = ud[pan][2], m20 = ud[pan][3];
+      const float m21 = ud[pan][4], m22 = ud[pan][5], m30 = ud[pan][6], m31 = ud[pan][7];
+      const float m32 = ud[pan][8], m33 = ud[pan][9];
+      const float z0 = ud[pan][10] - m00 * a0;
+      const float z1 = ud[pan][11] - (m10 * a0 + m11 * a1);
+      const float z2 = ud[pan][12] - (m20 * a0 + m21 * a1 + m22 * a2);
+      const float z3 = ud[pan][13] - (m30 * a0 + m31 * a1 + m32 * a2 + m33 * a3);
+      const float x0 = m00 * z0 + m10 * z1 + m20 * z2 + m30 * z3;
+      const float x1 = m11 * z1 + m21 * z2 + m31 * z3;
+      const float x2 = m22 * z2 + m32 * z3;
+      const float x3 = m33 * z3;
       const int jj = c - 4 * g;
       if (jj >= 0 && jj < 4) xv[I0] = jj == 0 ? x0 : (jj == 1 ? x1 : (jj == 2 ? x2 : x3));
     }
@@ -330,14 +378,23 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
 }
 
 template <int DP>
+static constexpr bool has_aug(int D) {
+  return ((D + 3) & ~3) < DP;
+}
+
+template <int DP>
 static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32_t *idx,
                                 const uint8_t *val, const float *Fp, int zrow, const float *ws,
                                 int D, float lam, float *X, double *sse, int32_t *flag,
                                 hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
-  hipLaunchKernelGGL(k_rows<DP>, dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s, rows, n_rows,
-                     idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
+  if (has_aug<DP>(D))
+    hipLaunchKernelGGL((k_rows<DP, true>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
+                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
+  else
+    hipLaunchKernelGGL((k_rows<DP, false>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
+                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
   return hipGetLastError();
 }
 
@@ -347,14 +404,18 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
                                   const float *Xold, int D, float *ws, double *sse,
                                   hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gram_chunks<DP>, dim3((unsigned)n), dim3(64), 0, s, items, idx, val, Fp,
-                     zrow, Xold, D, ws, sse);
+  if (has_aug<DP>(D))
+    hipLaunchKernelGGL((k_gram_chunks<DP, true>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
+                       val, Fp, zrow, Xold, D, ws, sse);
+  else
+    hipLaunchKernelGGL((k_gram_chunks<DP, false>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
+                       val, Fp, zrow, Xold, D, ws, sse);
   return hipGetLastError();
 }
 
+// Row kernels serve D > 20 (narrower widths take the one-lane solve).
 #define ALS_DP_SWITCH(dp, CALL)                 \
   switch (dp) {                                 \
-    case 16: { constexpr int DPV = 16; CALL; }  \
     case 32: { constexpr int DPV = 32; CALL; }  \
     case 48: { constexpr int DPV = 48; CALL; }  \
     case 64: { constexpr int DPV = 64; CALL; }  \
