@@ -20,16 +20,6 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ __forceinline__ float swz_xor(float v, int x) {
-  // ds_swizzle bit mode: lane' = lane ^ x within 32-lane halves
-  switch (x) {
-    case 1: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x041F));
-    case 2: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x081F));
-    case 4: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
-    default: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x201F));
-  }
-}
-
 // Rotate a value right by K lanes within each 16-lane row (DPP row_ror).
 template <int K>
 __device__ __forceinline__ float row_ror(float v) {
@@ -43,6 +33,29 @@ __device__ __forceinline__ float sum16(float v) {
   v += row_ror<2>(v);
   v += row_ror<1>(v);
   return v;
+}
+
+// Lane permutations within 16-lane rows (DPP): mirror within each half-row
+// (lane i <-> 7 - i) and swaps within quads (lane i <-> i ^ 2, i <-> i ^ 1).
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppHalfMirror = 0x141, kDppQuadXor2 = 0x4E, kDppQuadXor1 = 0xB1;
+
+// Four 16-lane row sums at once (reduce-scatter): afterwards lane c of a row holds
+// the row's sum of s[c >> 2]. Partners at each level share every lane bit above the
+// one that decides which half a lane keeps, so each lane ends with the full sum.
+__device__ __forceinline__ float sum16x4(float s0, float s1, float s2, float s3) {
+  const int c = threadIdx.x & 15;
+  const bool h8 = (c & 8) != 0, h4 = (c & 4) != 0;
+  const float k0 = h8 ? s2 : s0, k1 = h8 ? s3 : s1;  // kept half
+  const float g0 = h8 ? s0 : s2, g1 = h8 ? s1 : s3;  // half given to lane c ^ 8
+  const float t0 = k0 + row_ror<8>(g0), t1 = k1 + row_ror<8>(g1);
+  float u = (h4 ? t1 : t0) + dpp_move<kDppHalfMirror>(h4 ? t0 : t1);
+  u += dpp_move<kDppQuadXor2>(u);
+  u += dpp_move<kDppQuadXor1>(u);
+  return u;
 }
 
 // Value of lane l (wave-uniform) broadcast to the wave through a scalar register.
@@ -84,9 +97,26 @@ __device__ __forceinline__ void unroll_blocks(F &f) {
   }
 }
 
+// Per-wave LDS staging of a 64-rating group's column indices and ratings, transposed
+// so that lane (kq, c) finds the values of its steps s (ratings 4 s + kq) contiguously
+// at [kq * 16 + s]; two buffers let the next group be staged while the current one is
+// still read.
+struct GroupStage {
+  int32_t j[2][64];
+  float r[2][64];
+};
+
+// Stage the group held one rating per lane (lane L holds rating L of the group).
+__device__ __forceinline__ void stage_group(GroupStage &st, int buf, int jv, float rv) {
+  const int lane = threadIdx.x & 63;
+  const int at = (lane & 3) * 16 + (lane >> 2);
+  st.j[buf][at] = jv;
+  st.r[buf][at] = rv;
+}
+
 // Gather the staged fixed rows of steps s0 .. s0 + STEPS - 1 of a 64-rating group:
-// lane (kq, c) receives feature 16 X + c of rating 4 s + kq. jsrc / rsrc hold the
-// group's column indices and ratings, one per lane.
+// lane (kq, c) receives feature 16 X + c of rating 4 s + kq. The group's column
+// indices and ratings come from its staging buffer.
 // Loads are never predicated per lane (a predicated load becomes a branch that waits
 // for its own completion, which serialises the gathers): ratings past the end of the
 // item read the staged all-zero row, and padded features read the staged row's zero
@@ -97,16 +127,17 @@ __device__ __forceinline__ void unroll_blocks(F &f) {
 // column (and sum r^2 on its diagonal).
 template <int DP, int STEPS, bool AUG>
 __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
-                                             int jsrc, float rsrc, int s0,
+                                             const GroupStage &st, int buf, int s0,
                                              const float *__restrict__ Fp, bool aug_lane) {
   constexpr int T = DP / 16;
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
+  const int32_t *__restrict__ sj = &st.j[buf][kq * 16 + s0];
+  const float *__restrict__ sr = &st.r[buf][kq * 16 + s0];
 #pragma unroll
   for (int u = 0; u < STEPS; ++u) {
-    const int src = 4 * (s0 + u) + kq;
-    const int j = __shfl(jsrc, src);
-    r[u] = __shfl(rsrc, src);
+    const int j = sj[u];
+    r[u] = sr[u];
     const uint32_t off = (uint32_t)j * (uint32_t)(DP * 4) + (uint32_t)(c * 4);
     const char *row = reinterpret_cast<const char *>(Fp) + (uint64_t)off;
 #pragma unroll
@@ -147,28 +178,42 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
   }
 }
 
+// The partner of lane c at reduce-scatter level O (within 16-lane rows): c ^ 8, the
+// half-row mirror c ^ 7, then c ^ 2 and c ^ 1. Each pair differs in bit O of the lane
+// and agrees on the bits of the earlier levels, and {8, 7, 2, 1} span all 16 lanes.
+template <int O>
+__device__ __forceinline__ float rs_partner(float v) {
+  if constexpr (O == 8) return row_ror<8>(v);
+  else if constexpr (O == 4) return dpp_move<kDppHalfMirror>(v);
+  else if constexpr (O == 2) return dpp_move<kDppQuadXor2>(v);
+  else return dpp_move<kDppQuadXor1>(v);
+}
+
+template <int O>
+__device__ __forceinline__ void rs_level(float (&pi)[16], int c) {
+  const bool hi = (c & O) != 0;
+#pragma unroll
+  for (int i = 0; i < O; ++i) {
+    const float keep = hi ? pi[O + i] : pi[i];
+    const float give = hi ? pi[i] : pi[O + i];
+    pi[i] = keep + rs_partner<O>(give);
+  }
+}
+
 // End of a 64-rating group: reduce-scatter the 16 step partials over the 16 feature
 // lanes, after which lane c holds the full prediction of step c for its rating group
-// (both halves are exchanged and the lane keeps the sum of its half; selecting between
-// computed sums keeps the partial array statically indexed), and add the squared
-// residuals of the group's ratings.
-__device__ __forceinline__ void group_residuals(float (&pi)[16], float rv, int g, int n,
-                                                double &sse) {
+// (at each level a lane keeps the half selected by one bit of c and adds the partner's
+// copy of it), and add the squared residuals of the group's ratings.
+__device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStage &st, int buf,
+                                                int g, int n, double &sse) {
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
-#pragma unroll
-  for (int o = 8, m = 16; o >= 1; o >>= 1, m >>= 1) {
-    const bool hi = (c & o) != 0;
-#pragma unroll
-    for (int i = 0; i < m / 2; ++i) {
-      const float lo_sum = pi[i] + swz_xor(pi[i], o);
-      const float hi_sum = pi[m / 2 + i] + swz_xor(pi[m / 2 + i], o);
-      pi[i] = hi ? hi_sum : lo_sum;
-    }
-  }
-  // lane (kq, c) now holds the prediction of rating g + 4c + kq, whose value sits in
-  // lane 4c + kq of this group's rating register
-  const float rq = __shfl(rv, 4 * c + kq);
+  rs_level<8>(pi, c);
+  rs_level<4>(pi, c);
+  rs_level<2>(pi, c);
+  rs_level<1>(pi, c);
+  // lane (kq, c) now holds the prediction of rating g + 4c + kq (step c of row group kq)
+  const float rq = st.r[buf][kq * 16 + c];
   if (g + 4 * c + kq < n) {
     const double e = (double)rq - (double)pi[0];
     sse = fma(e, e, sse);
@@ -194,7 +239,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 const int32_t *__restrict__ ip,
                                                 const uint8_t *__restrict__ vp, int n,
                                                 const float *__restrict__ Fp, int zrow,
-                                                int aug_c) {
+                                                int aug_c, GroupStage &st) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
@@ -211,6 +256,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
       const float rn = gn < n ? rl : 0.f;
       const int steps = min(16, (n - g + 3) >> 2);
       __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
+      stage_group(st, 0, jv, rv);
+      wave_sync();
       float pi[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) pi[u] = 0.f;
@@ -219,18 +266,22 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         if (s0 < steps) {
           float a[STEPS][T];
           float r[STEPS];
-          gather_block<DP, STEPS, AUG>(a, r, jv, rv, s0, Fp, aug_lane);
+          gather_block<DP, STEPS, AUG>(a, r, st, 0, s0, Fp, aug_lane);
           mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a, r, s0, steps);
         }
       }
-      group_residuals(pi, rv, g, n, sse);
+      group_residuals(pi, st, 0, g, n, sse);
+      wave_sync();  // the buffer is restaged by the next group
       jv = jn;
       rv = rn;
     }
   } else {
     static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
     float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS];
-    gather_block<DP, STEPS, AUG>(a0, r0, jv, rv, 0, Fp, aug_lane);
+    stage_group(st, 0, jv, rv);
+    wave_sync();
+    gather_block<DP, STEPS, AUG>(a0, r0, st, 0, 0, Fp, aug_lane);
+    int buf = 0;
     for (int g = 0; g < n; g += 64) {
       const int gn = g + 64 + lane;
       const int jl = ip[min(gn, n - 1)];
@@ -246,18 +297,24 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         constexpr int b = decltype(bc)::value;
         constexpr int s0 = b * STEPS;
         if constexpr (b % 2 == 0) {
-          if constexpr (b + 1 < NB) gather_block<DP, STEPS, AUG>(a1, r1, jv, rv, s0 + STEPS, Fp, aug_lane);
+          if constexpr (b + 1 < NB)
+            gather_block<DP, STEPS, AUG>(a1, r1, st, buf, s0 + STEPS, Fp, aug_lane);
           mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a0, r0, s0, steps);
         } else {
-          if constexpr (b + 1 < NB) gather_block<DP, STEPS, AUG>(a0, r0, jv, rv, s0 + STEPS, Fp, aug_lane);
-          else gather_block<DP, STEPS, AUG>(a0, r0, jn, rn, 0, Fp, aug_lane);
+          if constexpr (b + 1 < NB) {
+            gather_block<DP, STEPS, AUG>(a0, r0, st, buf, s0 + STEPS, Fp, aug_lane);
+          } else {
+            // the next group goes to the other buffer, then its first block is gathered
+            stage_group(st, buf ^ 1, jn, rn);
+            wave_sync();
+            gather_block<DP, STEPS, AUG>(a0, r0, st, buf ^ 1, 0, Fp, aug_lane);
+          }
           mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a1, r1, s0, steps);
         }
       };
       unroll_blocks<0, NB>(block);
-      group_residuals(pi, rv, g, n, sse);
-      jv = jn;
-      rv = rn;
+      group_residuals(pi, st, buf, g, n, sse);
+      buf ^= 1;
     }
   }
 }

@@ -43,6 +43,7 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   constexpr int NES = ne_floats(LD);
   static_assert(!AUG || (LD < DP && LD > 16 * (T - 1) && LD % 4 == 0),
                 "the augmented column is feature LD of the last tile");
+  __shared__ GroupStage s_stage;
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
   floatx4 acc[NT];
@@ -59,7 +60,7 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   }
   double sse = 0.0;
   gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? LD - 16 * (T - 1) : -1);
+                           AUG ? LD - 16 * (T - 1) : -1, s_stage);
   if constexpr (!AUG) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {

@@ -71,6 +71,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
                                                     double *__restrict__ sse_out) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
+  __shared__ GroupStage s_stage;
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
   floatx4 acc[NT];
@@ -87,7 +88,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   }
   double sse = 0.0;
   gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? aug_column<DP>(D) : -1);
+                           AUG ? aug_column<DP>(D) : -1, s_stage);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -132,6 +133,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   constexpr int NPAN = DP / 4;
   __shared__ floatx4 s_panel[kRowWaves][T][16];  // one panel's rows, per tile column and lane column
   __shared__ float s_ud[kRowWaves][NPAN][16];    // per panel: M (10 entries) and y_p (4)
+  __shared__ GroupStage s_stage[kRowWaves];        // gather staging of the row's rating groups
 
   const int wv = threadIdx.x >> 6;
   const int64_t task = (int64_t)blockIdx.x * kRowWaves + wv;
@@ -170,7 +172,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     }
     double sse = 0.0;
     gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow,
-                             aug_c);
+                             aug_c, s_stage[wv]);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -204,19 +206,21 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     for (int g = 0; g < 4; ++g) {
       const int p0 = 16 * I0 + 4 * g;
       if (p0 >= D) break;
-      // (1) publish the panel rows p0..p0+3 (held by row group g)
+      // (1) the 4x4 diagonal block A[p0 + r][p0 + r'] sits in element r of lane
+      // (g, 4 g + r') of tile (I0, I0); it goes to scalar registers directly, while the
+      // panel rows p0..p0+3 (held by row group g) are published to LDS for the columns
+      const floatx4 dg = acc[tidx<T>(I0, I0)];
+      const int l0 = 20 * g;
+      const float a00 = lane_value(dg[0], l0), a01 = lane_value(dg[0], l0 + 1);
+      const float a02 = lane_value(dg[0], l0 + 2), a03 = lane_value(dg[0], l0 + 3);
+      const float a11 = lane_value(dg[1], l0 + 1), a12 = lane_value(dg[1], l0 + 2);
+      const float a13 = lane_value(dg[1], l0 + 3), a22 = lane_value(dg[2], l0 + 2);
+      const float a23 = lane_value(dg[2], l0 + 3), a33 = lane_value(dg[3], l0 + 3);
       if (kq == g) {
 #pragma unroll
         for (int X = I0; X < T; ++X) panel[X][c] = acc[tidx<T>(I0, X)];
       }
-      wave_sync();
       // (2) 4x4 diagonal block, factored redundantly in every lane
-      const floatx4 d0 = panel[I0][4 * g + 0], d1 = panel[I0][4 * g + 1];
-      const floatx4 d2 = panel[I0][4 * g + 2], d3 = panel[I0][4 * g + 3];
-      // d{r'}[r] = A[p0 + r][p0 + r']
-      const float a00 = d0[0], a01 = d1[0], a02 = d2[0], a03 = d3[0];
-      const float a11 = d1[1], a12 = d2[1], a13 = d3[1];
-      const float a22 = d2[2], a23 = d3[2], a33 = d3[3];
       float p;
       p = a00;
       bad |= !(p > 0.f && p < INFINITY);
@@ -269,6 +273,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       }
       // (3) panel rows U[p0 + kq][j] = (M A_p)[kq][j] for the later columns j (zero for
       // j <= p0 + 3, which keeps the finished rows and columns out of the update)
+      wave_sync();
       float u[T];
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -322,28 +327,29 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   for (int X = 0; X < T; ++X) xv[X] = 0.f;
 #pragma unroll
   for (int I0 = T - 1; I0 >= 0; --I0) {
+    // this tile row's partial products with the solved tiles X > I0 (row group g
+    // holds panel g's rows; the 16-lane sums follow per panel)
+    float P0 = 0.f, P1 = 0.f, P2 = 0.f, P3 = 0.f;
+#pragma unroll
+    for (int X = I0 + 1; X < T; ++X) {
+      const floatx4 aa = acc[tidx<T>(I0, X)];
+      P0 = fmaf(aa[0], xv[X], P0);
+      P1 = fmaf(aa[1], xv[X], P1);
+      P2 = fmaf(aa[2], xv[X], P2);
+      P3 = fmaf(aa[3], xv[X], P3);
+    }
 #pragma clang loop unroll(disable)
     for (int g = 3; g >= 0; --g) {
       const int p0 = 16 * I0 + 4 * g;
       if (p0 >= D) continue;
-      // s_r = sum_{j > p0 + 3} A_p[r][j] x_j, partials in row group g
-      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-#pragma unroll
-      for (int X = I0; X < T; ++X) {
-        const int j = 16 * X + c;
-        const float xj = j > p0 + 3 ? xv[X] : 0.f;
-        const floatx4 uu = acc[tidx<T>(I0, X)];
-        s0 = fmaf(uu[0], xj, s0);
-        s1 = fmaf(uu[1], xj, s1);
-        s2 = fmaf(uu[2], xj, s2);
-        s3 = fmaf(uu[3], xj, s3);
-      }
-      s0 = sum16(s0);
-      s1 = sum16(s1);
-      s2 = sum16(s2);
-      s3 = sum16(s3);
-      const float a0 = lane_value(s0, 16 * g), a1 = lane_value(s1, 16 * g);
-      const float a2 = lane_value(s2, 16 * g), a3 = lane_value(s3, 16 * g);
+      // s_r = sum_{j > p0 + 3} A_p[r][j] x_j: the solved tiles plus the later panels
+      // of this tile
+      const float xj = c > 4 * g + 3 ? xv[I0] : 0.f;
+      const floatx4 aa = acc[tidx<T>(I0, I0)];
+      const float sr = sum16x4(fmaf(aa[0], xj, P0), fmaf(aa[1], xj, P1), fmaf(aa[2], xj, P2),
+                               fmaf(aa[3], xj, P3));
+      const float a0 = lane_value(sr, 16 * g + 0), a1 = lane_value(sr, 16 * g + 4);
+      const float a2 = lane_value(sr, 16 * g + 8), a3 = lane_value(sr, 16 * g + 12);
       const int pan = p0 >> 2;
       const float m00 = ud[pan][0], m10 = ud[pan][1], m11 = ud[pan][2], m20 = ud[pan][3];
       const float m21 = ud[pan][4], m22 = ud[pan][5], m30 = ud[pan][6], m31 = ud[pan][7];
