@@ -2,10 +2,12 @@
 """ALS half-sweep throughput on one MI355X.
 
 One step = one ALS sweep of the paper's order (Sec. 2.2): the item half-sweep
-(solve V with U fixed) then the user half-sweep (solve U with V fixed), each
-with its residual pass for the training RMSE. The metric is ratings per
+(solve V with U fixed) then the user half-sweep (solve U with V fixed); each
+half-sweep's gather also yields the squared residuals of the state it enters,
+so every state's training RMSE is produced once. The metric is ratings per
 second per half-sweep, 2 * nnz * steps / elapsed, with the rating matrix and
-factors resident in HBM before the timed region.
+factors resident in HBM before the timed region; per_side gives each side's
+median half-sweep time (HIP events) and its ratings per second.
 
 Default workload: the full-scale synthetic stand-in for the paper's data set
 (1,000,990 users x 624,961 items x 262,810,175 ratings, Sec. 1), D = 20,
@@ -110,11 +112,20 @@ def cpu_baseline(r, side_fixed, target_s):
         dt = time.perf_counter() - t0
         return int(deg[sel].sum()), k, dt
 
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     n0, k0, t0 = run(max(1, r.nnz // 500))
     rate0 = n0 / max(t0, 1e-9)
     target = min(r.nnz, int(rate0 * target_s))
     n1, k1, t1 = run(target)
     return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
+                cpu_model=cpu_model,
                 sample=(f"user half-sweep of {r.name}: {k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
@@ -154,12 +165,24 @@ def main():
         log(f"warmup {w + 1}/{args.warmup} done")
     torch.cuda.synchronize()
     als.set_profiling(True)
+    # HIP events around each half-sweep on the stream the library enqueues on
+    ev = {side: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(args.steps)] for side in ("items", "users")}
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for k in range(args.steps):
+        ev["items"][k][0].record()
         als.half_sweep("items", U, r.lam, V)
+        ev["items"][k][1].record()
+        ev["users"][k][0].record()
         als.half_sweep("users", V, r.lam, U)
+        ev["users"][k][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    per_side = {}
+    for side in ("items", "users"):
+        ms = sorted(a.elapsed_time(b) for a, b in ev[side])
+        med = ms[len(ms) // 2] if len(ms) % 2 else 0.5 * (ms[len(ms) // 2 - 1] + ms[len(ms) // 2])
+        per_side[side] = {"ms_median": med, "ms_min": ms[0], "ratings_per_s": r.nnz / (med * 1e-3)}
     prof = als.profile()
     als.set_profiling(False)
     elapsed = t1 - t0
@@ -219,6 +242,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "per_side": per_side,
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
         "rmse": rmse,
         "rmse_entering_last_half_sweep": rmse_in,

@@ -29,24 +29,29 @@
 namespace als {
 
 // Copy the fixed factors [n x D] into a zero-padded [(n + 1) x DP] buffer whose
-// last row is all zero (the stand-in of padded features and absent ratings).
+// last row is all zero (the stand-in of absent ratings). Thread (q, y) of a block
+// writes float4 q of staged row blockIdx.x * blockDim.y + y (grid-stride over rows).
 __global__ void k_stage_fixed(const float *__restrict__ F, int64_t n, int D, int DP,
                               float *__restrict__ Fp) {
-  const int64_t total = (n + 1) * DP;
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (; i < total; i += stride) {
-    const int64_t row = i / DP;
-    const int d = (int)(i - row * DP);
-    Fp[i] = (row < n && d < D) ? F[row * D + d] : 0.f;
+  const int q = threadIdx.x;
+  const int d0 = 4 * q;
+  for (int64_t row = (int64_t)blockIdx.x * blockDim.y + threadIdx.y; row <= n;
+       row += (int64_t)gridDim.x * blockDim.y) {
+    float v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = (row < n && d0 + k < D) ? F[row * D + d0 + k] : 0.f;
+    *reinterpret_cast<float4 *>(Fp + row * DP + d0) = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
 hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *Fp, hipStream_t s) {
-  if (n < 0) return hipErrorInvalidValue;
-  int64_t blocks = ((n + 1) * DP + 255) / 256;
-  if (blocks > 262144) blocks = 262144;
-  hipLaunchKernelGGL(k_stage_fixed, dim3((unsigned)blocks), dim3(256), 0, s, F, n, D, DP, Fp);
+  if (n < 0 || DP % 4 != 0 || DP / 4 > 256) return hipErrorInvalidValue;
+  const int dp4 = DP / 4;
+  const int rows_per_block = 256 / dp4;
+  int64_t blocks = (n + 1 + rows_per_block - 1) / rows_per_block;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_stage_fixed, dim3((unsigned)blocks), dim3(dp4, rows_per_block), 0, s, F, n,
+                     D, DP, Fp);
   return hipGetLastError();
 }
 
