@@ -64,12 +64,39 @@ def copy_calibration():
     log(f"copy calibration: 3 copies of {4 * n} bytes")
 
 
+def strip_comments(src):
+    """C/C++ source without comments, trailing blanks or empty lines (string and
+    character literals are kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        ch = src[i]
+        if ch in "\"'":
+            j = i + 1
+            while j < n and src[j] != ch:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            while i < n and src[i] != "\n":
+                i += 1
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(ch)
+            i += 1
+    lines = (line.rstrip() for line in "".join(out).split("\n"))
+    return "\n".join(line for line in lines if line)
+
+
 def kernel_source_hash():
-    """Hash of the device sources (the counters are void once any of them changes)."""
+    """Hash of the device sources with comments removed (the counters are void once the
+    code of any of them changes)."""
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
         if name.endswith((".hip", ".h")):
-            h.update(open(os.path.join(CSRC, name), "rb").read())
+            h.update(name.encode())
+            h.update(strip_comments(open(os.path.join(CSRC, name)).read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -12,7 +12,7 @@
  *     x_s = (sum_{j in Omega_s} f_j f_j^T + lambda * n_s * I)^{-1}
  *           * sum_{j in Omega_s} r_sj f_j,
  *
- * where f_j are the fixed side's rows. The per-update "matrix inversion"
+ * where f_j are the fixed side's rows. The per-update inversion
  * (Sec. 4.1) is done by Cholesky. The quality measure is RMSE (Sec. 4.1),
  * here the training RMSE over all stored ratings.
  *

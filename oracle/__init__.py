@@ -8,7 +8,7 @@ dependency is the seeded input generator in ``workload``.
 Method (paper Sec. 2.2): with one side of the factorisation fixed, each row s of
 the other side is the regularised least-squares solution
     x_s = (sum_j f_j f_j^T + lambda n_s I)^{-1} sum_j r_sj f_j,
-computed in fp64 by Cholesky (the per-update "matrix inversion" of Sec. 4.1).
+computed in fp64 by Cholesky (the per-update inversion of Sec. 4.1).
 A prediction is u_u . v_i (Sec. 2.2); RMSE (Sec. 4.1) is taken over the stored
 ratings. One sweep solves the items with the users fixed, then the users with
 the items fixed (the order of Sec. 2.2).

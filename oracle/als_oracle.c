@@ -12,7 +12,7 @@
  *     sum_{j in Omega_s} (r_sj - f_j . x)^2 + lambda * n_s * ||x||^2,
  * i.e. x_s = (sum_j f_j f_j^T + lambda n_s I)^{-1} sum_j r_sj f_j, where f_j
  * are the fixed-side rows of the ratings of s and n_s = |Omega_s|. The
- * "matrix inversion" of Sec. 4.1 is done here as a Cholesky factorisation
+ * per-update inversion of Sec. 4.1 is done here as a Cholesky factorisation
  * and two triangular solves. A prediction is the dot product of the user and
  * item vectors (Sec. 2.2); RMSE (Sec. 4.1) is sqrt(sum of squared residuals /
  * number of ratings) over the stored ratings.

@@ -12,7 +12,7 @@
 //   k_solve_lane one lane per row loads its record, adds lambda * n_s to the
 //                diagonal, factors
 //                A = U^T U in registers, solves U^T y = b and U x = y
-//                (Sec. 2.2; the per-update "matrix inversion" of Sec. 4.1) and
+//                (Sec. 2.2; the per-update inversion of Sec. 4.1) and
 //                writes x unless a pivot is not positive and finite.
 // Records hold LD(LD+1)/2 + LD floats (LD = 16 or 20, the width the solve is
 // compiled for; padded features solve to zero), rounded up to a multiple of 4.
