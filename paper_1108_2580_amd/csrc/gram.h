@@ -220,11 +220,24 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStag
   }
 }
 
+// Column index and rating of rating `lane` of an item's first 64-rating group (the
+// all-zero row and 0 past its end).
+__device__ __forceinline__ void first_group(const int32_t *__restrict__ ip,
+                                            const uint8_t *__restrict__ vp, int n, int zrow,
+                                            int &jv, float &rv) {
+  const int lane = threadIdx.x & 63;
+  jv = lane < n ? ip[min(lane, n - 1)] : zrow;
+  const float r = (float)vp[min(lane, n - 1)];
+  rv = lane < n ? r : 0.f;
+}
+
 // Accumulate the item's Gram tiles and right-hand side and the entering-state squared
 // residuals. Without AUG the right-hand side is kept in rhs as per-lane partials over
 // the four rating groups; with AUG it is the Gram's column 16 (T - 1) + aug_c (a padding
 // column whose lane carries the ratings) and rhs is untouched.
 // xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
+// jv / rv: the first group's column indices and ratings, one per lane
+// (first_group loads them), so that a caller can load them ahead of time.
 // Ratings are taken in groups of 64, each gathered in blocks of STEPS steps (four
 // ratings per step).
 //  - Narrow rows (T <= 2): one block per group, gathered and then multiplied.
@@ -239,14 +252,11 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 const int32_t *__restrict__ ip,
                                                 const uint8_t *__restrict__ vp, int n,
                                                 const float *__restrict__ Fp, int zrow,
-                                                int aug_c, GroupStage &st) {
+                                                int aug_c, GroupStage &st, int jv, float rv) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
   const bool aug_lane = (lane & 15) == aug_c;
-  int jv = lane < n ? ip[lane] : zrow;
-  float rv = (float)vp[min(lane, n - 1)];
-  rv = lane < n ? rv : 0.f;
   if constexpr (T <= 2) {
     for (int g = 0; g < n; g += 64) {
       const int gn = g + 64 + lane;

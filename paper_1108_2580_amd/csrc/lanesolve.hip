@@ -59,8 +59,11 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
     }
   }
   double sse = 0.0;
+  int jv;
+  float rv;
+  first_group(idx + it.start, val + it.start, it.len, zrow, jv, rv);
   gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? LD - 16 * (T - 1) : -1, s_stage);
+                           AUG ? LD - 16 * (T - 1) : -1, s_stage, jv, rv);
   if constexpr (!AUG) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {

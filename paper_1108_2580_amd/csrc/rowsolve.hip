@@ -92,8 +92,11 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
     }
   }
   double sse = 0.0;
+  int jv;
+  float rv;
+  first_group(idx + it.start, val + it.start, it.len, zrow, jv, rv);
   gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? aug_column<DP>(D) : -1, s_stage);
+                           AUG ? aug_column<DP>(D) : -1, s_stage, jv, rv);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -149,8 +152,9 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   float(&ud)[NPAN][16] = s_ud[wv];
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
 
-  // A starts as lambda n_s I on the first D diagonal entries and I on the padding;
-  // the Gram (or the sum of a split row's chunk partials) is accumulated on top
+  // A starts as lambda n_s I on the first D diagonal entries and I on the padding (only
+  // the last tile holds padding); the Gram (or the sum of a split row's chunk partials)
+  // is accumulated on top
   const float lam_n = (float)((double)lam * (double)rt.deg);
   floatx4 acc[NT];
 #pragma unroll
@@ -160,7 +164,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int d = 16 * I + 4 * kq + r;
-      acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? (d < D ? lam_n : 1.f) : 0.f;
+      acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? ((I < T - 1 || d < D) ? lam_n : 1.f) : 0.f;
     }
   }
   float rhs[T];
@@ -176,8 +180,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       xo[X] = 16 * X + c < D ? v : 0.f;
     }
     double sse = 0.0;
+    int jv;
+    float rv;
+    first_group(idx + rt.start, val + rt.start, rt.deg, zrow, jv, rv);
     gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow,
-                             aug_c, s_stage[wv]);
+                             aug_c, s_stage[wv], jv, rv);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
