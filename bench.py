@@ -215,6 +215,16 @@ def main():
     elapsed = t1 - t0
     rmse_in = als.rmse_in()
     rmse = als.rmse(U, V)
+    gram_share = None
+    if r.D > 20:
+        # one extra, untimed half-sweep per side with the row kernel's phase clocks on
+        als.set_phase_timing(True)
+        als.half_sweep("items", U, r.lam, V)
+        als.half_sweep("users", V, r.lam, U)
+        gi, si = als.phase_cycles("items")
+        gu, su = als.phase_cycles("users")
+        als.set_phase_timing(False)
+        gram_share = (gi + gu) / max(gi + si + gu + su, 1.0)
     log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
         f"rmse entering last half-sweep {rmse_in:.6f}, final {rmse:.6f}")
 
@@ -244,6 +254,19 @@ def main():
                     frac=achieved / MFMA_F32_PEAK_TFS, kernel="k_rows+k_gram_chunks")
     roof.update(launches=k_n, avg_launch_ms=k_ms / max(k_n, 1), alg_per_launch=alg / max(k_n, 1),
                 traffic=measured_traffic(r.name, roof["kernel"]), dominant_phase=dominant)
+    gram_phase = None
+    if gram_share is not None:
+        # Gram phase: the chunk kernel plus the share of the fused row kernel's wavefront
+        # time spent before the factorisation (gather, Gram, RHS, residuals); flops in
+        # the SYRK convention plus the right-hand side
+        g_ms = (prof["gather"][0] + gram_share * prof["solve"][0]) / args.steps
+        g_flops = 2 * r.nnz * (D * (D + 1) + 2 * D)
+        g_tf = g_flops / (g_ms * 1e-3) / 1e12
+        gram_phase = dict(ms_per_step=g_ms, flops_per_step=g_flops, achieved=g_tf,
+                          peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s", frac=g_tf / MFMA_F32_PEAK_TFS,
+                          row_kernel_gram_share=gram_share,
+                          method="chunk-kernel time plus the row kernel's time scaled by the "
+                                 "share of wavefront clock cycles before the factorisation")
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -270,6 +293,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "per_side": per_side,
+        "gram_phase": gram_phase,
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
         "rmse": rmse,
         "rmse_entering_last_half_sweep": rmse_in,

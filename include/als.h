@@ -158,6 +158,21 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
 als_status als_set_profiling(als_ctx *ctx, int32_t enable);
 als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches);
 
+/*
+ * Optional phase clocks of the fused row kernel (widths D > 20, which build the
+ * normal equations and factor them in one kernel, Sec. 2.2). While enabled, every
+ * row records the wavefront clock cycles spent before its factorisation begins
+ * (gather, Gram, right-hand side and residuals, or the sum of a split row's chunk
+ * partials) and from there to its end (factorisation, solves, write), and each
+ * half-sweep adds them up per side; this costs one stream synchronisation per
+ * half-sweep and leaves the results unchanged. Enabling allocates 16 bytes per row
+ * of the larger side on first use and resets the totals. als_get_phase_cycles
+ * returns a side's totals (zero for D <= 20, whose Gram kernel is separate).
+ */
+als_status als_set_phase_timing(als_ctx *ctx, int32_t enable);
+als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles,
+                                double *solve_cycles);
+
 void als_destroy(als_ctx *ctx);
 
 const char *als_status_str(als_status s);

@@ -23,8 +23,8 @@ _SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
 
 EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_flagged_rows",
            "als_get_csc",
-           "als_plan_stats", "als_set_profiling", "als_get_profile", "als_destroy",
-           "als_status_str", "als_last_error")
+           "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_phase_timing",
+           "als_get_phase_cycles", "als_destroy", "als_status_str", "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
 
@@ -67,6 +67,11 @@ def _load_library(path=LIB_PATH):
     lib.als_get_profile.argtypes = [P, i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_int64)]
     lib.als_get_profile.restype = st
+    lib.als_set_phase_timing.argtypes = [P, i32]
+    lib.als_set_phase_timing.restype = st
+    lib.als_get_phase_cycles.argtypes = [P, st, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double)]
+    lib.als_get_phase_cycles.restype = st
     lib.als_destroy.argtypes = [P]
     lib.als_destroy.restype = None
     lib.als_status_str.argtypes = [st]
@@ -183,6 +188,17 @@ class ALS:
             self._check(lib.als_get_profile(self._h, i, ctypes.byref(ms), ctypes.byref(n)))
             res[name] = (ms.value, n.value)
         return res
+
+    def set_phase_timing(self, on=True):
+        """Per-row clocks of the fused row kernel (D > 20); resets the totals."""
+        self._check(lib.als_set_phase_timing(self._h, 1 if on else 0))
+
+    def phase_cycles(self, side):
+        """(cycles before the factorisation, cycles from it on), summed over rows."""
+        g = ctypes.c_double(0.0)
+        v = ctypes.c_double(0.0)
+        self._check(lib.als_get_phase_cycles(self._h, _SIDES[side], ctypes.byref(g), ctypes.byref(v)))
+        return g.value, v.value
 
     def close(self):
         if getattr(self, "_h", None):

@@ -98,6 +98,12 @@ struct als_ctx {
   std::vector<hipEvent_t> ev_pool;
   double prof_ms[kPhases] = {0, 0, 0, 0, 0};
   int64_t prof_n[kPhases] = {0, 0, 0, 0, 0};
+  bool phase_timing = false;
+  int64_t cyc_cap = 0;            // rows per array of d_cyc
+  double *d_cyc = nullptr;        // [2 x cyc_cap]: per-row Gram and solve cycles
+  double *d_cyc_sum = nullptr;    // [2]
+  double *h_cyc_sum = nullptr;    // pinned [2]
+  double cyc[2][2] = {{0, 0}, {0, 0}};  // per side: Gram, solve
 };
 
 namespace {
@@ -279,6 +285,9 @@ void free_ctx(als_ctx *c) {
   if (c->h_sse) (void)hipHostFree(c->h_sse);
   if (c->h_sse_in) (void)hipHostFree(c->h_sse_in);
   if (c->h_flag) (void)hipHostFree(c->h_flag);
+  dfree(c->d_cyc);
+  dfree(c->d_cyc_sum);
+  if (c->h_cyc_sum) (void)hipHostFree(c->h_cyc_sum);
   for (auto &pe : c->prof_pending) {
     (void)hipEventDestroy(pe.a);
     (void)hipEventDestroy(pe.b);
@@ -585,9 +594,11 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
       }
       {
         PhaseTimer t(ctx, 2);
+        double *cg = ctx->phase_timing ? ctx->d_cyc + b.row_off : nullptr;
+        double *cs = ctx->phase_timing ? ctx->d_cyc + ctx->cyc_cap + b.row_off : nullptr;
         HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val,
                                           ctx->d_fpad, n_fixed, ctx->d_ws, ctx->D, lambda,
-                                          out_factors, ctx->d_sse_items, ctx->d_flag,
+                                          out_factors, ctx->d_sse_items, ctx->d_flag, cg, cs,
                                           ctx->stream));
       }
     }
@@ -602,6 +613,18 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, ctx->stream));
   ctx->last_side = side;
+  if (ctx->phase_timing && !ctx->lane_solve && !P.rows.empty()) {
+    const int64_t nr = (int64_t)P.rows.size();
+    HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_cyc, nr, ctx->d_partials, ctx->d_cyc_sum,
+                                        ctx->stream));
+    HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_cyc + ctx->cyc_cap, nr, ctx->d_partials,
+                                        ctx->d_cyc_sum + 1, ctx->stream));
+    HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_cyc_sum, ctx->d_cyc_sum, 2 * sizeof(double),
+                                    hipMemcpyDeviceToHost, ctx->stream));
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    ctx->cyc[side][0] += ctx->h_cyc_sum[0];
+    ctx->cyc[side][1] += ctx->h_cyc_sum[1];
+  }
   if (rmse_out) {
     als_status st = residual_pass(ctx, P, idx, val, out_factors);
     if (st != ALS_OK) return st;
@@ -681,6 +704,45 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) 
   const int64_t v[7] = {P.rows_with, P.split_rows, P.n_chunks, (int64_t)P.batches.size(),
                         P.max_deg, (int64_t)ctx->ws_bytes, (int64_t)slot_bytes_of(ctx)};
   for (int32_t i = 0; i < n && i < 7; ++i) out[i] = v[i];
+  return ALS_OK;
+}
+
+als_status als_set_phase_timing(als_ctx *ctx, int32_t enable) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  DeviceGuard g(ctx->device);
+  if (enable && !ctx->d_cyc) {
+    const int64_t cap = std::max<int64_t>(
+        1, std::max((int64_t)ctx->plan[0].rows.size(), (int64_t)ctx->plan[1].rows.size()));
+    double *cyc = nullptr, *sum = nullptr, *host = nullptr;
+    hipError_t e = dalloc(&cyc, 2 * cap);
+    if (e == hipSuccess) e = dalloc(&sum, 2);
+    if (e == hipSuccess) e = hipHostMalloc((void **)&host, 2 * sizeof(double), hipHostMallocDefault);
+    if (e != hipSuccess) {
+      dfree(cyc);
+      dfree(sum);
+      return fail(ctx, e == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP,
+                  "phase timing buffers: %s", hipGetErrorString(e));
+    }
+    ctx->d_cyc = cyc;
+    ctx->d_cyc_sum = sum;
+    ctx->h_cyc_sum = host;
+    ctx->cyc_cap = cap;
+  }
+  ctx->phase_timing = enable != 0;
+  for (auto &side : ctx->cyc) side[0] = side[1] = 0.0;
+  return ALS_OK;
+}
+
+als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles,
+                                double *solve_cycles) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "side must be ALS_ROWS_USERS or ALS_ROWS_ITEMS");
+  if (!gram_cycles || !solve_cycles) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  *gram_cycles = ctx->cyc[side][0];
+  *solve_cycles = ctx->cyc[side][1];
   return ALS_OK;
 }
 

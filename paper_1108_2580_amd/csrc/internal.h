@@ -62,9 +62,14 @@ hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const in
 
 // Fused per-row normal equations, regularisation, Cholesky and solves; X is read
 // (entering state) and overwritten in place (rowsolve.hip).
+// cyc_gram / cyc_solve: both null, or arrays of n_rows doubles that receive each
+// row's wavefront clock cycles spent before the factorisation (gather, Gram and
+// residuals, or the sum of chunk partials) and from there on (factorisation, solves,
+// write); a measurement aid that leaves the results unchanged.
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
-                       int D, float lam, float *X, double *sse, int32_t *flag, hipStream_t s);
+                       int D, float lam, float *X, double *sse, int32_t *flag, double *cyc_gram,
+                       double *cyc_solve, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
 // fixed side Fp (row stride DP) (residual.hip).

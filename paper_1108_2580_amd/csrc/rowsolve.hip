@@ -116,7 +116,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   if (lane == 0) sse_out[blockIdx.x] = sse;
 }
 
-constexpr int kRowWaves = 4;  // independent rows per workgroup (one per wavefront)
+constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 
 // Two wavefronts per SIMD (the second launch bound) outweigh the few registers the
 // wide widths then spill: the accumulator tiles move to arch VGPRs and the gather
@@ -135,7 +135,9 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const uint8_t *__restrict__ val, const float *__restrict__ Fp, int zrow,
     const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
     double *__restrict__ sse_out,
-    int32_t *__restrict__ flag_count) {
+    int32_t *__restrict__ flag_count, double *__restrict__ cyc_gram,
+    double *__restrict__ cyc_solve) {
+  const uint64_t t_start = __builtin_readcyclecounter();
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
   constexpr int NPAN = DP / 4;
@@ -207,6 +209,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       }
     }
   }
+
+  const uint64_t t_gram = __builtin_readcyclecounter();
 
   // ---- factorisation A = U^T U with forward substitution U^T y = b ------------------------
   bool bad = false;
@@ -393,6 +397,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   } else if (lane == 0) {
     atomicAdd(flag_count, 1);
   }
+  if (cyc_gram != nullptr && lane == 0) {
+    const uint64_t t_end = __builtin_readcyclecounter();
+    cyc_gram[task] = (double)(t_gram - t_start);
+    cyc_solve[task] = (double)(t_end - t_gram);
+  }
 }
 
 template <int DP>
@@ -404,15 +413,17 @@ template <int DP>
 static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32_t *idx,
                                 const uint8_t *val, const float *Fp, int zrow, const float *ws,
                                 int D, float lam, float *X, double *sse, int32_t *flag,
-                                hipStream_t s) {
+                                double *cyc_gram, double *cyc_solve, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
   if (has_aug<DP>(D))
     hipLaunchKernelGGL((k_rows<DP, true>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
-                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
+                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
+                       cyc_solve);
   else
     hipLaunchKernelGGL((k_rows<DP, false>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
-                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag);
+                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
+                       cyc_solve);
   return hipGetLastError();
 }
 
@@ -446,10 +457,12 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
 
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
-                       int D, float lam, float *X, double *sse, int32_t *flag, hipStream_t s) {
+                       int D, float lam, float *X, double *sse, int32_t *flag, double *cyc_gram,
+                       double *cyc_solve, hipStream_t s) {
+  if ((cyc_gram == nullptr) != (cyc_solve == nullptr)) return hipErrorInvalidValue;
   const int zrow = (int)n_fixed;
   ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X,
-                                              sse, flag, s));
+                                              sse, flag, cyc_gram, cyc_solve, s));
 }
 
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,

@@ -280,6 +280,35 @@ def test_bitwise_deterministic():
     assert a[1] == b[1] and a[3] == b[3]
 
 
+@pytest.mark.parametrize("D", [20, 33, 100])
+def test_phase_timing_leaves_results_unchanged(D):
+    # the row kernel's phase clocks are a measurement aid: factors and RMSE must be
+    # bitwise the same with them on, and they count cycles only for the fused kernel
+    M, N = 400, 300
+    ptr, col, val = small_matrix(D)
+    U0, V0 = workload.init_factors(M, N, D, seed=5 + D)
+    outs = []
+    for timing in (False, True):
+        with make_als(M, N, ptr, col, val, D, dict(hub_threshold=40, chunk=24)) as als:
+            als.set_phase_timing(timing)
+            V = dev(V0)
+            U = dev(U0)
+            rv = als.half_sweep("items", U, 0.065, V, rmse=True)
+            ru = als.half_sweep("users", V, 0.065, U, rmse=True)
+            cyc = {side: als.phase_cycles(side) for side in ("items", "users")}
+            outs.append((U.cpu().numpy(), V.cpu().numpy(), rv, ru, cyc))
+    (U_a, V_a, rv_a, ru_a, cyc_a), (U_b, V_b, rv_b, ru_b, cyc_b) = outs
+    assert np.array_equal(U_a, U_b) and np.array_equal(V_a, V_b)
+    assert rv_a == rv_b and ru_a == ru_b
+    assert all(g == 0 and s == 0 for g, s in cyc_a.values())
+    for g, s in cyc_b.values():
+        if D > 20:
+            assert g > 0 and s > 0
+        else:
+            assert g == 0 and s == 0
+    log(f"  D={D} phase cycles {cyc_b}")
+
+
 def test_api_errors():
     from paper_1108_2580_amd import ALS_ERR_INVALID_ARG, ALSError, lib
 
