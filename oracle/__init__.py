@@ -9,6 +9,10 @@ Method (paper Sec. 2.2): with one side of the factorisation fixed, each row s of
 the other side is the regularised least-squares solution
     x_s = (sum_j f_j f_j^T + lambda n_s I)^{-1} sum_j r_sj f_j,
 computed in fp64 by Cholesky (the per-update inversion of Sec. 4.1).
+Weighted ALS (wALS, named beside ALS in Sec. 2 and Sec. 4 but not defined there):
+the functions taking ``w`` (one non-negative weight per stored rating, in the
+same order as ``val``) solve x_s = (sum_j c_sj f_j f_j^T + lambda n_s I)^{-1}
+sum_j c_sj r_sj f_j; ``w=None`` is plain ALS, and unit weights reproduce it bitwise.
 A prediction is u_u . v_i (Sec. 2.2); RMSE (Sec. 4.1) is taken over the stored
 ratings. One sweep solves the items with the users fixed, then the users with
 the items fixed (the order of Sec. 2.2).
@@ -51,15 +55,15 @@ def _configure(lib):
                                ctypes.c_int)
     lib.orc_transpose.argtypes = [i64, i64, P, P, P, P, P, P]
     lib.orc_transpose.restype = c_int
-    lib.orc_normal_equations.argtypes = [i32, i64, P, P, P, f64, P, P]
+    lib.orc_normal_equations.argtypes = [i32, i64, P, P, P, P, f64, P, P]
     lib.orc_normal_equations.restype = None
     lib.orc_cholesky_solve.argtypes = [i32, P, P, P, P]
     lib.orc_cholesky_solve.restype = c_int
-    lib.orc_half_sweep.argtypes = [i64, P, P, P, i32, P, f64, P, P, c_int]
+    lib.orc_half_sweep.argtypes = [i64, P, P, P, P, i32, P, f64, P, P, c_int]
     lib.orc_half_sweep.restype = i64
-    lib.orc_solve_rows.argtypes = [i64, P, P, P, P, i32, P, f64, P, P, c_int]
+    lib.orc_solve_rows.argtypes = [i64, P, P, P, P, P, i32, P, f64, P, P, c_int]
     lib.orc_solve_rows.restype = i64
-    lib.orc_sse.argtypes = [i64, P, P, P, i32, P, P, P, c_int]
+    lib.orc_sse.argtypes = [i64, P, P, P, P, i32, P, P, P, c_int]
     lib.orc_sse.restype = f64
     lib.orc_weighted_norm.argtypes = [i64, P, i32, P]
     lib.orc_weighted_norm.restype = f64
@@ -105,14 +109,26 @@ def transpose(ptr, idx, val, n_cols):
     return out_ptr, out_idx, out_val
 
 
-def normal_equations(row, ptr, idx, val, F, lam):
-    """(A, b) of one row: A = sum f f^T + lam n I, b = sum r f (fp64, rating order)."""
+def _opt_f64(w, n):
+    if w is None:
+        return None
+    w = _f64(w)
+    if w.shape != (n,):
+        raise ValueError(f"weights have shape {w.shape}, expected ({n},)")
+    return w
+
+
+def normal_equations(row, ptr, idx, val, F, lam, w=None):
+    """(A, b) of one row: A = sum c f f^T + lam n I, b = sum c r f (fp64, rating order;
+    c = 1 without weights)."""
     ptr, idx, val, F = _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    w = _opt_f64(w, val.size)
     D = F.shape[1]
     s, e = int(ptr[row]), int(ptr[row + 1])
     A = np.empty((D, D))
     b = np.empty(D)
-    _load().orc_normal_equations(D, e - s, _p(idx[s:e]), _p(val[s:e]), _p(F), float(lam), _p(A),
+    _load().orc_normal_equations(D, e - s, _p(idx[s:e]), _p(val[s:e]),
+                                 None if w is None else _p(w[s:e]), _p(F), float(lam), _p(A),
                                  _p(b))
     return A, b
 
@@ -128,39 +144,44 @@ def cholesky_solve(A, b):
     return x
 
 
-def half_sweep(ptr, idx, val, F, lam, X_prev, threads=0):
+def half_sweep(ptr, idx, val, F, lam, X_prev, threads=0, w=None):
     """One half-sweep. Returns (X_new, flags) with flags 0 solved / 1 not SPD / 2 empty.
 
-    Rows that are empty or flagged keep their value from X_prev."""
+    Rows that are empty or flagged keep their value from X_prev. ``w``: optional
+    per-rating weights (weighted ALS)."""
     ptr, idx, val, F = _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    w = _opt_f64(w, val.size)
     X = np.array(X_prev, dtype=np.float64, order="C", copy=True)
     n_rows = ptr.size - 1
     D = F.shape[1]
     assert X.shape == (n_rows, D)
     flags = np.empty(n_rows, dtype=np.int8)
-    _load().orc_half_sweep(n_rows, _p(ptr), _p(idx), _p(val), D, _p(F), float(lam), _p(X),
+    _load().orc_half_sweep(n_rows, _p(ptr), _p(idx), _p(val), _p(w), D, _p(F), float(lam), _p(X),
                            _p(flags), int(threads))
     return X, flags
 
 
-def solve_rows(rows, ptr, idx, val, F, lam, threads=0):
+def solve_rows(rows, ptr, idx, val, F, lam, threads=0, w=None):
     """The half-sweep update of the listed rows only: (X_sel, flags)."""
     rows, ptr, idx, val, F = _i64(rows), _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    w = _opt_f64(w, val.size)
     D = F.shape[1]
     X = np.empty((rows.size, D))
     flags = np.empty(rows.size, dtype=np.int8)
-    _load().orc_solve_rows(rows.size, _p(rows), _p(ptr), _p(idx), _p(val), D, _p(F), float(lam),
-                           _p(X), _p(flags), int(threads))
+    _load().orc_solve_rows(rows.size, _p(rows), _p(ptr), _p(idx), _p(val), _p(w), D, _p(F),
+                           float(lam), _p(X), _p(flags), int(threads))
     return X, flags
 
 
-def sse(ptr, idx, val, X, F, threads=0, per_row=False):
-    """Sum of squared residuals over the stored ratings of the rows of X."""
+def sse(ptr, idx, val, X, F, threads=0, per_row=False, w=None):
+    """Sum of squared residuals over the stored ratings of the rows of X (each
+    multiplied by its weight when ``w`` is given)."""
     ptr, idx, val, X, F = _i64(ptr), _i32(idx), _f64(val), _f64(X), _f64(F)
+    w = _opt_f64(w, val.size)
     n_rows = ptr.size - 1
     rs = np.empty(n_rows) if per_row else None
-    tot = _load().orc_sse(n_rows, _p(ptr), _p(idx), _p(val), F.shape[1], _p(X), _p(F), _p(rs),
-                          int(threads))
+    tot = _load().orc_sse(n_rows, _p(ptr), _p(idx), _p(val), _p(w), F.shape[1], _p(X), _p(F),
+                          _p(rs), int(threads))
     return (tot, rs) if per_row else tot
 
 
@@ -174,11 +195,12 @@ def weighted_norm(ptr, X):
     return _load().orc_weighted_norm(ptr.size - 1, _p(ptr), X.shape[1], _p(X))
 
 
-def objective(csr, csc, U, V, lam, threads=0):
-    """L(U,V) = sum (r - u.v)^2 + lam (sum_u n_u ||u||^2 + sum_i n_i ||v_i||^2)."""
+def objective(csr, csc, U, V, lam, threads=0, w=None):
+    """L(U,V) = sum c (r - u.v)^2 + lam (sum_u n_u ||u||^2 + sum_i n_i ||v_i||^2), with
+    c the per-rating weights in CSR order (1 without them)."""
     ptr, col, val = csr
     cptr = csc[0]
-    return (sse(ptr, col, val, U, V, threads)
+    return (sse(ptr, col, val, U, V, threads, w=w)
             + lam * (weighted_norm(ptr, U) + weighted_norm(cptr, V)))
 
 
@@ -188,9 +210,12 @@ class Trajectory:
     ``step(side)`` performs one half-sweep: side "items" solves V with U fixed,
     side "users" solves U with V fixed."""
 
-    def __init__(self, M, N, row_ptr, col, val, U0, V0, lam, threads=0):
+    def __init__(self, M, N, row_ptr, col, val, U0, V0, lam, threads=0, w=None):
         self.csr = (_i64(row_ptr), _i32(col), _f64(val))
         self.csc = transpose(self.csr[0], self.csr[1], self.csr[2], N)
+        self.w = _opt_f64(w, self.csr[2].size)
+        # the weights travel with the ratings: transposing them as the carried values
+        self.w_t = None if self.w is None else transpose(self.csr[0], self.csr[1], self.w, N)[2]
         self.U = _f64(U0).copy()
         self.V = _f64(V0).copy()
         self.lam = float(lam)
@@ -199,9 +224,9 @@ class Trajectory:
 
     def step(self, side):
         if side == "items":
-            self.V, fl = half_sweep(*self.csc, self.U, self.lam, self.V, self.threads)
+            self.V, fl = half_sweep(*self.csc, self.U, self.lam, self.V, self.threads, w=self.w_t)
         else:
-            self.U, fl = half_sweep(*self.csr, self.V, self.lam, self.U, self.threads)
+            self.U, fl = half_sweep(*self.csr, self.V, self.lam, self.U, self.threads, w=self.w)
         self.nflag = int((fl == 1).sum())
         return self
 
@@ -212,4 +237,4 @@ class Trajectory:
         return rmse(*self.csr, self.U, self.V, self.threads)
 
     def objective(self):
-        return objective(self.csr, self.csc, self.U, self.V, self.lam, self.threads)
+        return objective(self.csr, self.csc, self.U, self.V, self.lam, self.threads, w=self.w)

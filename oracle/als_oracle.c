@@ -17,6 +17,13 @@
  * item vectors (Sec. 2.2); RMSE (Sec. 4.1) is sqrt(sum of squared residuals /
  * number of ratings) over the stored ratings.
  *
+ * Weighted ALS (the paper's wALS, listed with ALS in Sec. 2 and Sec. 4, whose
+ * weighting the paper does not define): with a non-negative weight c_sj on every
+ * stored rating, the row minimises sum_j c_sj (r_sj - f_j . x)^2 + lambda n_s ||x||^2,
+ * so x_s = (sum_j c_sj f_j f_j^T + lambda n_s I)^{-1} sum_j c_sj r_sj f_j; the
+ * regulariser keeps the count n_s, so unit weights give plain ALS. Every function
+ * that takes a weight array wt treats NULL as the unweighted method.
+ *
  * Everything is double precision, sequential within a row, rows in parallel
  * (OpenMP). Reductions over rows are done in row order from per-row values,
  * so every result is independent of the thread count.
@@ -56,19 +63,21 @@ int orc_transpose(int64_t n_rows, int64_t n_cols, const int64_t *ptr, const int3
   return 0;
 }
 
-/* Normal equations of one row: A = sum_k f_k f_k^T + lambda * n * I (full
- * D x D, row-major) and b = sum_k r_k f_k, accumulated in the order of the
- * row's ratings. */
+/* Normal equations of one row: A = sum_k c_k f_k f_k^T + lambda * n * I (full
+ * D x D, row-major) and b = sum_k c_k r_k f_k, accumulated in the order of the
+ * row's ratings; c_k = wt[k], or 1 when wt is NULL. */
 void orc_normal_equations(int32_t D, int64_t n, const int32_t *idx, const double *val,
-                          const double *F, double lambda, double *A, double *b) {
+                          const double *wt, const double *F, double lambda, double *A,
+                          double *b) {
   for (int32_t a = 0; a < D * D; ++a) A[a] = 0.0;
   for (int32_t a = 0; a < D; ++a) b[a] = 0.0;
   for (int64_t k = 0; k < n; ++k) {
     const double *f = F + (int64_t)idx[k] * D;
     double r = val[k];
     for (int32_t a = 0; a < D; ++a) {
-      for (int32_t c = 0; c < D; ++c) A[a * D + c] += f[a] * f[c];
-      b[a] += r * f[a];
+      const double cf = wt ? wt[k] * f[a] : f[a];
+      for (int32_t e = 0; e < D; ++e) A[a * D + e] += cf * f[e];
+      b[a] += r * cf;
     }
   }
   for (int32_t a = 0; a < D; ++a) A[a * D + a] += lambda * (double)n;
@@ -113,10 +122,10 @@ int orc_cholesky_solve(int32_t D, const double *A, const double *b, double *W, d
 /* One row's update into x (length D). Returns 0 (solved), 1 (not SPD /
  * non-finite: x untouched) or 2 (no ratings: x untouched). */
 static int solve_one(int32_t D, int64_t n, const int32_t *idx, const double *val,
-                     const double *F, double lambda, double *A, double *b, double *W,
-                     double *xs, double *x) {
+                     const double *wt, const double *F, double lambda, double *A, double *b,
+                     double *W, double *xs, double *x) {
   if (n == 0) return 2;
-  orc_normal_equations(D, n, idx, val, F, lambda, A, b);
+  orc_normal_equations(D, n, idx, val, wt, F, lambda, A, b);
   if (orc_cholesky_solve(D, A, b, W, xs) != 0) return 1;
   for (int32_t a = 0; a < D; ++a) x[a] = xs[a];
   return 0;
@@ -127,8 +136,8 @@ static int solve_one(int32_t D, int64_t n, const int32_t *idx, const double *val
  * no ratings and flagged rows keep their previous X. flags[s] (nullable)
  * receives 0 solved, 1 flagged, 2 empty. Returns the number of flagged rows. */
 int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, const double *val,
-                       int32_t D, const double *F, double lambda, double *X, int8_t *flags,
-                       int nthreads) {
+                       const double *wt, int32_t D, const double *F, double lambda, double *X,
+                       int8_t *flags, int nthreads) {
   set_threads(nthreads);
   int64_t nflag = 0;
 #pragma omp parallel reduction(+ : nflag)
@@ -139,8 +148,8 @@ int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, c
     double *xs = (double *)malloc(sizeof(double) * D);
 #pragma omp for schedule(dynamic, 16)
     for (int64_t s = 0; s < n_rows; ++s) {
-      int st = solve_one(D, ptr[s + 1] - ptr[s], idx + ptr[s], val + ptr[s], F, lambda, A, b, W,
-                         xs, X + s * D);
+      int st = solve_one(D, ptr[s + 1] - ptr[s], idx + ptr[s], val + ptr[s],
+                         wt ? wt + ptr[s] : NULL, F, lambda, A, b, W, xs, X + s * D);
       if (flags) flags[s] = (int8_t)st;
       nflag += (st == 1);
     }
@@ -152,8 +161,8 @@ int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, c
 /* The same update for a list of rows only (sampled checks at full size).
  * X_sel is n_sel x D; rows that are empty or flagged get NaN. */
 int64_t orc_solve_rows(int64_t n_sel, const int64_t *rows, const int64_t *ptr, const int32_t *idx,
-                       const double *val, int32_t D, const double *F, double lambda,
-                       double *X_sel, int8_t *flags, int nthreads) {
+                       const double *val, const double *wt, int32_t D, const double *F,
+                       double lambda, double *X_sel, int8_t *flags, int nthreads) {
   set_threads(nthreads);
   int64_t nflag = 0;
 #pragma omp parallel reduction(+ : nflag)
@@ -167,8 +176,8 @@ int64_t orc_solve_rows(int64_t n_sel, const int64_t *rows, const int64_t *ptr, c
       int64_t s = rows[t];
       double *x = X_sel + t * D;
       for (int32_t a = 0; a < D; ++a) x[a] = NAN;
-      int st = solve_one(D, ptr[s + 1] - ptr[s], idx + ptr[s], val + ptr[s], F, lambda, A, b, W,
-                         xs, x);
+      int st = solve_one(D, ptr[s + 1] - ptr[s], idx + ptr[s], val + ptr[s],
+                         wt ? wt + ptr[s] : NULL, F, lambda, A, b, W, xs, x);
       if (flags) flags[t] = (int8_t)st;
       nflag += (st == 1);
     }
@@ -177,10 +186,11 @@ int64_t orc_solve_rows(int64_t n_sel, const int64_t *rows, const int64_t *ptr, c
   return nflag;
 }
 
-/* Per-row sums of squared residuals (r_sj - x_s . f_j)^2 into row_sse
- * (nullable), and their total summed in row order. */
+/* Per-row sums of squared residuals c_sj (r_sj - x_s . f_j)^2 (c = 1 when wt is
+ * NULL) into row_sse (nullable), and their total summed in row order. */
 double orc_sse(int64_t n_rows, const int64_t *ptr, const int32_t *idx, const double *val,
-               int32_t D, const double *X, const double *F, double *row_sse, int nthreads) {
+               const double *wt, int32_t D, const double *X, const double *F, double *row_sse,
+               int nthreads) {
   set_threads(nthreads);
   double *per = row_sse ? row_sse : (double *)malloc(sizeof(double) * (n_rows > 0 ? n_rows : 1));
 #pragma omp parallel for schedule(dynamic, 64)
@@ -192,7 +202,7 @@ double orc_sse(int64_t n_rows, const int64_t *ptr, const int32_t *idx, const dou
       double pred = 0.0;
       for (int32_t a = 0; a < D; ++a) pred += x[a] * f[a];
       double e = val[p] - pred;
-      acc += e * e;
+      acc += wt ? wt[p] * (e * e) : e * e;
     }
     per[s] = acc;
   }

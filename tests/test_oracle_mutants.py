@@ -9,13 +9,14 @@ import pytest
 
 import oracle
 from tests import test_oracle_pins as pins
+from tests import test_oracle_weighted_pins as wpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
 
 # (name, original text, mutated text)
 MUTANTS = [
     ("unweighted_lambda", "A[a * D + a] += lambda * (double)n;", "A[a * D + a] += lambda;"),
-    ("rhs_without_rating", "b[a] += r * f[a];", "b[a] += f[a];"),
+    ("rhs_without_rating", "b[a] += r * cf;", "b[a] += cf;"),
     ("first_rating_dropped", "for (int64_t k = 0; k < n; ++k) {", "for (int64_t k = 1; k < n; ++k) {"),
     ("backsolve_transposed", "s -= W[m * D + i] * x[m];", "s -= W[i * D + m] * x[m];"),
     ("cholesky_sign", "s -= W[i * D + m] * W[j * D + m];", "s += W[i * D + m] * W[j * D + m];"),
@@ -25,9 +26,23 @@ MUTANTS = [
      "for (int64_t r = n_rows - 1; r >= 0; --r) {\n    for (int64_t p = ptr[r];"),
     ("norm_unweighted", "total += (double)(ptr[s + 1] - ptr[s]) * q;", "total += q;"),
     ("zero_degree_overwritten", "if (n == 0) return 2;", "if (n < 0) return 2;"),
+    ("weight_squared", "const double cf = wt ? wt[k] * f[a] : f[a];",
+     "const double cf = wt ? wt[k] * wt[k] * f[a] : f[a];"),
+    ("weight_ignored_in_gram", "for (int32_t e = 0; e < D; ++e) A[a * D + e] += cf * f[e];",
+     "for (int32_t e = 0; e < D; ++e) A[a * D + e] += f[a] * f[e];"),
+    ("weight_ignored_in_rhs", "b[a] += r * cf;", "b[a] += r * f[a];"),
+    ("weight_offset_wrong_row", "wt ? wt + ptr[s] : NULL, F, lambda, A, b, W, xs, X + s * D);",
+     "wt ? wt + ptr[s] + 1 : NULL, F, lambda, A, b, W, xs, X + s * D);"),
+    ("weighted_sse_unweighted", "acc += wt ? wt[p] * (e * e) : e * e;", "acc += e * e;"),
 ]
 
 PIN_TESTS = [
+    wpins.test_w1_unit_weights_are_plain_als,
+    lambda: wpins.test_w2_matches_weighted_lstsq(3),
+    wpins.test_w3_weighted_gradient_zero,
+    wpins.test_w5_integer_weight_is_repeated_rating,
+    wpins.test_w7_single_rating_closed_form,
+    wpins.test_w9_weighted_sse,
     pins.test_golden_worked_solves,
     pins.test_golden_worked_rmse,
     lambda: pins.test_brute_force_rational(3, 5),

@@ -333,6 +333,19 @@ def init_factors(M: int, N: int, D: int, seed: int) -> tuple:
     return U, V
 
 
+def rating_weights(nnz: int, seed: int, lo: float = 0.25, hi: float = 4.0) -> np.ndarray:
+    """Seeded per-rating weights for weighted ALS, log-uniform on [lo, hi), fp32, in the
+    order of the ratings (CSR). The paper does not define its weighting; throughput does
+    not depend on the values, and this spread exercises weights both below and above 1."""
+    rng = np.random.default_rng(seed)
+    return np.exp(rng.uniform(np.log(lo), np.log(hi), size=nnz)).astype(np.float32)
+
+
+def weight_seed(k: int) -> int:
+    """Seed of the weight stream of config k (separate from data and init seeds)."""
+    return data_seed(k) + 2000
+
+
 def degree_stats(ptr: np.ndarray) -> dict:
     d = np.diff(ptr)
     return dict(n=int(d.size), total=int(d.sum()), max=int(d.max()), p99=float(np.percentile(d, 99)),
