@@ -159,6 +159,19 @@ als_status als_set_profiling(als_ctx *ctx, int32_t enable);
 als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches);
 
 /*
+ * Weighted ALS (wALS: named beside ALS in the paper's Sec. 2 and Sec. 4, which do not
+ * define its weighting). weights: host array of nnz floats, one non-negative finite
+ * weight c per stored rating in CSR order (the order of col_idx / ratings at create);
+ * the library copies it to the device in both orders (8 bytes per rating). Later
+ * half-sweeps solve x_s = (sum_j c_sj f_j f_j^T + lambda n_s I)^{-1} sum_j c_sj r_sj f_j
+ * (the regulariser keeps the count n_s, so unit weights give plain ALS exactly); the
+ * RMSE stays the unweighted training RMSE. NULL detaches the weights. Errors:
+ * ALS_ERR_INVALID_ARG for a negative or non-finite weight (nothing changes),
+ * ALS_ERR_OUT_OF_MEMORY, ALS_ERR_HIP. Synchronises the context's stream.
+ */
+als_status als_set_weights(als_ctx *ctx, const float *weights);
+
+/*
  * Optional phase clocks of the fused row kernel (widths D > 20, which build the
  * normal equations and factor them in one kernel, Sec. 2.2). While enabled, every
  * row records the wavefront clock cycles spent before its factorisation begins

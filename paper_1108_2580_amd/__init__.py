@@ -23,8 +23,9 @@ _SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
 
 EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_flagged_rows",
            "als_get_csc",
-           "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_phase_timing",
-           "als_get_phase_cycles", "als_destroy", "als_status_str", "als_last_error")
+           "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_weights",
+           "als_set_phase_timing", "als_get_phase_cycles", "als_destroy", "als_status_str",
+           "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
 
@@ -67,6 +68,8 @@ def _load_library(path=LIB_PATH):
     lib.als_get_profile.argtypes = [P, i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_int64)]
     lib.als_get_profile.restype = st
+    lib.als_set_weights.argtypes = [P, P]
+    lib.als_set_weights.restype = st
     lib.als_set_phase_timing.argtypes = [P, i32]
     lib.als_set_phase_timing.restype = st
     lib.als_get_phase_cycles.argtypes = [P, st, ctypes.POINTER(ctypes.c_double),
@@ -188,6 +191,17 @@ class ALS:
             self._check(lib.als_get_profile(self._h, i, ctypes.byref(ms), ctypes.byref(n)))
             res[name] = (ms.value, n.value)
         return res
+
+    def set_weights(self, weights):
+        """Per-rating weights (CSR order, nnz non-negative floats) for weighted ALS; None
+        restores plain ALS."""
+        if weights is None:
+            self._check(lib.als_set_weights(self._h, None))
+            return
+        w = np.ascontiguousarray(weights, dtype=np.float32)
+        if w.shape != (self.nnz,):
+            raise ValueError(f"weights have shape {w.shape}, expected ({self.nnz},)")
+        self._check(lib.als_set_weights(self._h, _np_ptr(w)))
 
     def set_phase_timing(self, on=True):
         """Per-row clocks of the fused row kernel (D > 20); resets the totals."""

@@ -77,6 +77,8 @@ struct als_ctx {
   int64_t *d_col_ptr = nullptr;
   int32_t *d_row_idx = nullptr;
   uint8_t *d_val_t = nullptr;
+  float *d_w = nullptr;    // weighted ALS: per-rating weights in CSR order (null: plain ALS)
+  float *d_w_t = nullptr;  // the same weights in CSC order
   SidePlan plan[2];
   float *d_ws = nullptr;
   size_t ws_bytes = 0;
@@ -157,6 +159,14 @@ size_t slot_bytes_of(const als_ctx *ctx) {
 }
 
 // Degree-ordered schedule of one side with hub rows split into chunks.
+// Row blocking of the device transpose: blocks of rows_per_blk rows whose per-column
+// counters (nblk x n_items int32) stay within kCscTableEntries.
+void csc_blocking(int64_t n_users, int64_t n_items, int64_t &rows_per_blk, int64_t &nblk) {
+  const int64_t max_blk = std::max<int64_t>(1, kCscTableEntries / std::max<int64_t>(n_items, 1));
+  rows_per_blk = std::max<int64_t>(16, (n_users + max_blk - 1) / max_blk);
+  nblk = (n_users + rows_per_blk - 1) / rows_per_blk;
+}
+
 als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr) {
   const int64_t n_rows = (int64_t)ptr.size() - 1;
   P = SidePlan();
@@ -270,6 +280,8 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_col_ptr);
   dfree(c->d_row_idx);
   dfree(c->d_val_t);
+  dfree(c->d_w);
+  dfree(c->d_w_t);
   for (auto &P : c->plan) {
     dfree(P.d_gitems);
     dfree(P.d_rows);
@@ -484,9 +496,8 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   }
   // ---- A2: device transpose ----
   {
-    int64_t max_blk = std::max<int64_t>(1, kCscTableEntries / n_items);
-    int64_t rows_per_blk = std::max<int64_t>(16, (n_users + max_blk - 1) / max_blk);
-    int64_t nblk = (n_users + rows_per_blk - 1) / rows_per_blk;
+    int64_t rows_per_blk = 0, nblk = 0;
+    csc_blocking(n_users, n_items, rows_per_blk, nblk);
     int32_t *cnt = nullptr;
     int64_t *tot = nullptr;
     CK(dalloc(&cnt, nblk * n_items));
@@ -563,6 +574,7 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
   const SidePlan &P = ctx->plan[side];
   const int32_t *idx = users ? ctx->d_col : ctx->d_row_idx;
   const uint8_t *val = users ? ctx->d_val : ctx->d_val_t;
+  const float *wts = users ? ctx->d_w : ctx->d_w_t;
   HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
   {
     PhaseTimer t(ctx, 0);
@@ -575,7 +587,7 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
       {
         PhaseTimer t(ctx, 1);
         HIP_OR_FAIL(ctx, als::launch_gram_ne(ctx->D, P.d_gitems + b.gitem_off, b.n_gitems,
-                                             b.n_gchunks, idx, val, ctx->d_fpad, n_fixed,
+                                             b.n_gchunks, idx, val, wts, ctx->d_fpad, n_fixed,
                                              out_factors, ctx->d_ws, ctx->d_ne, sse,
                                              ctx->stream));
       }
@@ -589,14 +601,14 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
       if (b.n_gchunks > 0) {
         PhaseTimer t(ctx, 1);
         HIP_OR_FAIL(ctx, als::launch_gram_chunks(ctx->DP, P.d_gitems + b.gitem_off, b.n_gchunks,
-                                                 idx, val, ctx->d_fpad, n_fixed, out_factors,
+                                                 idx, val, wts, ctx->d_fpad, n_fixed, out_factors,
                                                  ctx->D, ctx->d_ws, sse, ctx->stream));
       }
       {
         PhaseTimer t(ctx, 2);
         double *cg = ctx->phase_timing ? ctx->d_cyc + b.row_off : nullptr;
         double *cs = ctx->phase_timing ? ctx->d_cyc + ctx->cyc_cap + b.row_off : nullptr;
-        HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val,
+        HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val, wts,
                                           ctx->d_fpad, n_fixed, ctx->d_ws, ctx->D, lambda,
                                           out_factors, ctx->d_sse_items, ctx->d_flag, cg, cs,
                                           ctx->stream));
@@ -704,6 +716,56 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n) 
   const int64_t v[7] = {P.rows_with, P.split_rows, P.n_chunks, (int64_t)P.batches.size(),
                         P.max_deg, (int64_t)ctx->ws_bytes, (int64_t)slot_bytes_of(ctx)};
   for (int32_t i = 0; i < n && i < 7; ++i) out[i] = v[i];
+  return ALS_OK;
+}
+
+als_status als_set_weights(als_ctx *ctx, const float *weights) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  DeviceGuard g(ctx->device);
+  if (!weights) {
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    dfree(ctx->d_w);
+    dfree(ctx->d_w_t);
+    return ALS_OK;
+  }
+  for (int64_t p = 0; p < ctx->nnz; ++p) {
+    if (!(weights[p] >= 0.f) || !std::isfinite(weights[p]))
+      return fail(ctx, ALS_ERR_INVALID_ARG, "weight %lld is not a finite non-negative number",
+                  (long long)p);
+  }
+  const int64_t nnz = ctx->nnz;
+  if (!ctx->d_w) {
+    float *w = nullptr, *wt = nullptr;
+    hipError_t e = dalloc(&w, nnz);
+    if (e == hipSuccess) e = dalloc(&wt, nnz);
+    if (e != hipSuccess) {
+      dfree(w);
+      dfree(wt);
+      return fail(ctx, e == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP,
+                  "weight buffers: %s", hipGetErrorString(e));
+    }
+    ctx->d_w = w;
+    ctx->d_w_t = wt;
+  }
+  if (nnz == 0) return ALS_OK;
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->d_w, weights, sizeof(float) * nnz, hipMemcpyHostToDevice,
+                                  ctx->stream));
+  int64_t rows_per_blk = 0, nblk = 0;
+  csc_blocking(ctx->M, ctx->N, rows_per_blk, nblk);
+  int32_t *cnt = nullptr;
+  int64_t *tot = nullptr;
+  hipError_t e = dalloc(&cnt, nblk * ctx->N);
+  if (e == hipSuccess) e = dalloc(&tot, ctx->N);
+  if (e == hipSuccess)
+    e = als::launch_csc_permute_f32(ctx->d_row_ptr, ctx->d_col, ctx->d_w, ctx->M, ctx->N,
+                                    rows_per_blk, nblk, cnt, tot, ctx->d_col_ptr, ctx->d_w_t,
+                                    ctx->stream);
+  const hipError_t e2 = hipStreamSynchronize(ctx->stream);
+  dfree(cnt);
+  dfree(tot);
+  HIP_OR_FAIL(ctx, e);
+  HIP_OR_FAIL(ctx, e2);
   return ALS_OK;
 }
 

@@ -104,14 +104,47 @@ __device__ __forceinline__ void unroll_blocks(F &f) {
 struct GroupStage {
   int32_t j[2][64];
   float r[2][64];
+  float w[2][64];  // per-rating weights (weighted ALS only)
+};
+
+// One rating per lane of a 64-rating group: column index, rating and weight.
+struct GroupLanes {
+  int j;
+  float r;
+  float w;
 };
 
 // Stage the group held one rating per lane (lane L holds rating L of the group).
-__device__ __forceinline__ void stage_group(GroupStage &st, int buf, int jv, float rv) {
+template <bool WT>
+__device__ __forceinline__ void stage_group(GroupStage &st, int buf, const GroupLanes &g) {
   const int lane = threadIdx.x & 63;
   const int at = (lane & 3) * 16 + (lane >> 2);
-  st.j[buf][at] = jv;
-  st.r[buf][at] = rv;
+  st.j[buf][at] = g.j;
+  st.r[buf][at] = g.r;
+  if constexpr (WT) st.w[buf][at] = g.w;
+}
+
+// Rating `first + lane` of an item (n ratings): clamped loads, then the all-zero row,
+// rating 0 and weight 0 past the item's end.
+template <bool WT>
+__device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip,
+                                                  const uint8_t *__restrict__ vp,
+                                                  const float *__restrict__ wp, int n, int first,
+                                                  int zrow) {
+  const int k = first + (int)(threadIdx.x & 63);
+  const int kc = min(k, n - 1);
+  const int j = ip[kc];
+  const float r = (float)vp[kc];
+  GroupLanes g;
+  g.j = k < n ? j : zrow;
+  g.r = k < n ? r : 0.f;
+  if constexpr (WT) {
+    const float w = wp[kc];
+    g.w = k < n ? w : 0.f;
+  } else {
+    g.w = 1.f;
+  }
+  return g;
 }
 
 // Gather the staged fixed rows of steps s0 .. s0 + STEPS - 1 of a 64-rating group:
@@ -125,19 +158,22 @@ __device__ __forceinline__ void stage_group(GroupStage &st, int buf, int jv, flo
 // With AUG, lane column aug_c of the last tile carries the rating instead of the
 // (zero) padded feature, so that the MFMA Gram also accumulates b = sum r f in that
 // column (and sum r^2 on its diagonal).
-template <int DP, int STEPS, bool AUG>
+template <int DP, int STEPS, bool AUG, bool WT>
 __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
-                                             const GroupStage &st, int buf, int s0,
-                                             const float *__restrict__ Fp, bool aug_lane) {
+                                             float (&wt)[STEPS], const GroupStage &st, int buf,
+                                             int s0, const float *__restrict__ Fp,
+                                             bool aug_lane) {
   constexpr int T = DP / 16;
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
   const int32_t *__restrict__ sj = &st.j[buf][kq * 16 + s0];
   const float *__restrict__ sr = &st.r[buf][kq * 16 + s0];
+  const float *__restrict__ sw = &st.w[buf][kq * 16 + s0];
 #pragma unroll
   for (int u = 0; u < STEPS; ++u) {
     const int j = sj[u];
     r[u] = sr[u];
+    wt[u] = WT ? sw[u] : 1.f;
     const uint32_t off = (uint32_t)j * (uint32_t)(DP * 4) + (uint32_t)(c * 4);
     const char *row = reinterpret_cast<const char *>(Fp) + (uint64_t)off;
 #pragma unroll
@@ -149,21 +185,27 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
 // MFMA Gram update, right-hand side and per-step partial predictions of the gathered
 // steps s0 .. s0 + STEPS - 1, in sub-blocks of up to four steps; sub-blocks past the
 // item's last step (steps of this group) are skipped. With AUG the right-hand side is
-// a column of the Gram and rhs is left alone.
-template <int DP, int STEPS, bool AUG>
+// a column of the Gram and rhs is left alone. With WT (weighted ALS) the first MFMA
+// operand carries c f, so the tiles accumulate sum c f f^T (and, in the augmented
+// column, sum c r f); predictions use the unweighted rows.
+template <int DP, int STEPS, bool AUG, bool WT>
 __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float (&rhs)[DP / 16], const float (&xo)[DP / 16],
                                           float (&pi)[16], const float (&a)[STEPS][DP / 16],
-                                          const float (&r)[STEPS], int s0, int steps) {
+                                          const float (&r)[STEPS], const float (&wt)[STEPS],
+                                          int s0, int steps) {
   constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
 #pragma unroll
   for (int u0 = 0; u0 < STEPS; u0 += SUB) {
     if (s0 + u0 < steps) {
 #pragma unroll
       for (int u = u0; u < u0 + SUB; ++u) {
+        const float rw = WT ? wt[u] * r[u] : r[u];
+        float wa[T];
 #pragma unroll
         for (int X = 0; X < T; ++X) {
-          if constexpr (!AUG) rhs[X] = fmaf(r[u], a[u][X], rhs[X]);
+          wa[X] = WT ? wt[u] * a[u][X] : a[u][X];
+          if constexpr (!AUG) rhs[X] = fmaf(rw, a[u][X], rhs[X]);
           pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
         }
 #pragma unroll
@@ -171,7 +213,7 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
 #pragma unroll
           for (int J = I; J < T; ++J)
             acc[tidx<T>(I, J)] =
-                __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
+                __builtin_amdgcn_mfma_f32_16x16x4f32(wa[I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
         }
       }
     }
@@ -220,24 +262,13 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStag
   }
 }
 
-// Column index and rating of rating `lane` of an item's first 64-rating group (the
-// all-zero row and 0 past its end).
-__device__ __forceinline__ void first_group(const int32_t *__restrict__ ip,
-                                            const uint8_t *__restrict__ vp, int n, int zrow,
-                                            int &jv, float &rv) {
-  const int lane = threadIdx.x & 63;
-  jv = lane < n ? ip[min(lane, n - 1)] : zrow;
-  const float r = (float)vp[min(lane, n - 1)];
-  rv = lane < n ? r : 0.f;
-}
-
 // Accumulate the item's Gram tiles and right-hand side and the entering-state squared
 // residuals. Without AUG the right-hand side is kept in rhs as per-lane partials over
 // the four rating groups; with AUG it is the Gram's column 16 (T - 1) + aug_c (a padding
 // column whose lane carries the ratings) and rhs is untouched.
 // xo: the row's current factor values in lane-column form (xo[X] = x[16X + c]).
-// jv / rv: the first group's column indices and ratings, one per lane
-// (first_group loads them), so that a caller can load them ahead of time.
+// wp: the item's per-rating weights (weighted ALS, WT), else unused.
+// gv: the first group's lanes (group_lanes(.., 0, ..)), loaded by the caller.
 // Ratings are taken in groups of 64, each gathered in blocks of STEPS steps (four
 // ratings per step).
 //  - Narrow rows (T <= 2): one block per group, gathered and then multiplied.
@@ -245,28 +276,25 @@ __device__ __forceinline__ void first_group(const int32_t *__restrict__ ip,
 //    the first block of the next group) is issued before the MFMAs of the current
 //    one, so that its latency hides behind them. The blocks of the last group that
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
-template <int DP, bool AUG>
+template <int DP, bool AUG, bool WT>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
                                                 const float (&xo)[RowCfg<DP>::T], double &sse,
                                                 const int32_t *__restrict__ ip,
-                                                const uint8_t *__restrict__ vp, int n,
+                                                const uint8_t *__restrict__ vp,
+                                                const float *__restrict__ wp, int n,
                                                 const float *__restrict__ Fp, int zrow,
-                                                int aug_c, GroupStage &st, int jv, float rv) {
+                                                int aug_c, GroupStage &st, GroupLanes gv) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
   const bool aug_lane = (lane & 15) == aug_c;
   if constexpr (T <= 2) {
     for (int g = 0; g < n; g += 64) {
-      const int gn = g + 64 + lane;
-      const int jl = ip[min(gn, n - 1)];
-      const float rl = (float)vp[min(gn, n - 1)];
-      const int jn = gn < n ? jl : zrow;
-      const float rn = gn < n ? rl : 0.f;
+      const GroupLanes gn = group_lanes<WT>(ip, vp, wp, n, g + 64, zrow);
       const int steps = min(16, (n - g + 3) >> 2);
       __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
-      stage_group(st, 0, jv, rv);
+      stage_group<WT>(st, 0, gv);
       wave_sync();
       float pi[16];
 #pragma unroll
@@ -275,29 +303,24 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
       for (int s0 = 0; s0 < 16; s0 += STEPS) {
         if (s0 < steps) {
           float a[STEPS][T];
-          float r[STEPS];
-          gather_block<DP, STEPS, AUG>(a, r, st, 0, s0, Fp, aug_lane);
-          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a, r, s0, steps);
+          float r[STEPS], w[STEPS];
+          gather_block<DP, STEPS, AUG, WT>(a, r, w, st, 0, s0, Fp, aug_lane);
+          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a, r, w, s0, steps);
         }
       }
       group_residuals(pi, st, 0, g, n, sse);
       wave_sync();  // the buffer is restaged by the next group
-      jv = jn;
-      rv = rn;
+      gv = gn;
     }
   } else {
     static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
-    float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS];
-    stage_group(st, 0, jv, rv);
+    float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS], w0[STEPS], w1[STEPS];
+    stage_group<WT>(st, 0, gv);
     wave_sync();
-    gather_block<DP, STEPS, AUG>(a0, r0, st, 0, 0, Fp, aug_lane);
+    gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, 0, 0, Fp, aug_lane);
     int buf = 0;
     for (int g = 0; g < n; g += 64) {
-      const int gn = g + 64 + lane;
-      const int jl = ip[min(gn, n - 1)];
-      const float rl = (float)vp[min(gn, n - 1)];
-      const int jn = gn < n ? jl : zrow;
-      const float rn = gn < n ? rl : 0.f;
+      const GroupLanes gn = group_lanes<WT>(ip, vp, wp, n, g + 64, zrow);
       const int steps = min(16, (n - g + 3) >> 2);
       __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
       float pi[16];
@@ -308,18 +331,18 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         constexpr int s0 = b * STEPS;
         if constexpr (b % 2 == 0) {
           if constexpr (b + 1 < NB)
-            gather_block<DP, STEPS, AUG>(a1, r1, st, buf, s0 + STEPS, Fp, aug_lane);
-          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a0, r0, s0, steps);
+            gather_block<DP, STEPS, AUG, WT>(a1, r1, w1, st, buf, s0 + STEPS, Fp, aug_lane);
+          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a0, r0, w0, s0, steps);
         } else {
           if constexpr (b + 1 < NB) {
-            gather_block<DP, STEPS, AUG>(a0, r0, st, buf, s0 + STEPS, Fp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, buf, s0 + STEPS, Fp, aug_lane);
           } else {
             // the next group goes to the other buffer, then its first block is gathered
-            stage_group(st, buf ^ 1, jn, rn);
+            stage_group<WT>(st, buf ^ 1, gn);
             wave_sync();
-            gather_block<DP, STEPS, AUG>(a0, r0, st, buf ^ 1, 0, Fp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, buf ^ 1, 0, Fp, aug_lane);
           }
-          mma_block<DP, STEPS, AUG>(acc, rhs, xo, pi, a1, r1, s0, steps);
+          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a1, r1, w1, s0, steps);
         }
       };
       unroll_blocks<0, NB>(block);

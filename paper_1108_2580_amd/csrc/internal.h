@@ -50,15 +50,27 @@ hipError_t launch_csc_build(const int64_t *row_ptr, const int32_t *col, const ui
                             int32_t *scratch_cnt, int64_t *tot, int64_t *col_ptr,
                             int32_t *row_idx, uint8_t *val_t, hipStream_t s);
 
+// The same transpose applied to a per-rating float array (weights): w_t[q] = w[p]
+// where q is the CSC position of CSR entry p, with col_ptr from launch_csc_build.
+// The position of (row, column) is col_ptr[column] plus the number of earlier rows
+// in that column, whatever the row blocking, so it matches the build.
+hipError_t launch_csc_permute_f32(const int64_t *row_ptr, const int32_t *col, const float *w,
+                                  int64_t n_rows, int64_t n_cols, int64_t rows_per_blk,
+                                  int64_t nblk, int32_t *scratch_cnt, int64_t *tot,
+                                  const int64_t *col_ptr, float *w_t, hipStream_t s);
+
 // Copy of the fixed factors [n x D] into a zero-padded [(n + 1) x DP] buffer whose
 // row n is all zero (rowsolve.hip).
 hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *Fp, hipStream_t s);
 
 // Partial normal equations of the chunks of split rows, into their workspace
 // slots, with the chunks' entering-state squared residuals (rowsolve.hip).
+// wts (here and below): per-rating weights aligned with idx / val for weighted ALS,
+// or null for plain ALS.
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
-                              const uint8_t *val, const float *Fp, int64_t n_fixed,
-                              const float *Xold, int D, float *ws, double *sse, hipStream_t s);
+                              const uint8_t *val, const float *wts, const float *Fp,
+                              int64_t n_fixed, const float *Xold, int D, float *ws, double *sse,
+                              hipStream_t s);
 
 // Fused per-row normal equations, regularisation, Cholesky and solves; X is read
 // (entering state) and overwritten in place (rowsolve.hip).
@@ -67,9 +79,9 @@ hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const in
 // residuals, or the sum of chunk partials) and from there on (factorisation, solves,
 // write); a measurement aid that leaves the results unchanged.
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                       const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
-                       int D, float lam, float *X, double *sse, int32_t *flag, double *cyc_gram,
-                       double *cyc_solve, hipStream_t s);
+                       const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
+                       const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
+                       double *cyc_gram, double *cyc_solve, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
 // fixed side Fp (row stride DP) (residual.hip).
@@ -86,9 +98,9 @@ constexpr int ne_floats(int ld) { return ((ld * (ld + 1) / 2 + ld) + 3) / 4 * 4;
 // Gram of rows or chunks packed into normal-equation records (lanesolve.hip):
 // items [0, n_chunk_items) write to ws at their slot, the rest to ne at their slot.
 hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
-                          const int32_t *idx, const uint8_t *val, const float *Fp,
-                          int64_t n_fixed, const float *Xold, float *ws, float *ne, double *sse,
-                          hipStream_t s);
+                          const int32_t *idx, const uint8_t *val, const float *wts,
+                          const float *Fp, int64_t n_fixed, const float *Xold, float *ws,
+                          float *ne, double *sse, hipStream_t s);
 
 // One row per lane: regularise, Cholesky, solve, write (lanesolve.hip). Row i of
 // the launch uses record base + i; its first n_split rows are split rows whose

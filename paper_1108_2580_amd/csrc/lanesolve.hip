@@ -27,12 +27,14 @@ __host__ __device__ constexpr int tri(int a, int b) {  // a <= b, row-major uppe
 
 // AUG (used for D = 17..20, LD = 20): the ratings ride in padding feature 20 of the
 // gathered rows, so the MFMA Gram delivers b in column 20 (tile column 4 of the last
-// tile) and the per-rating right-hand-side FMAs disappear.
-template <int DP, int LD, bool AUG>
+// tile) and the per-rating right-hand-side FMAs disappear. WT: weighted ALS, with the
+// per-rating weights wts aligned with idx / val.
+template <int DP, int LD, bool AUG, bool WT>
 __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ items,
                                                 int64_t n_chunk_items,
                                                 const int32_t *__restrict__ idx,
                                                 const uint8_t *__restrict__ val,
+                                                const float *__restrict__ wts,
                                                 const float *__restrict__ Fp, int zrow,
                                                 const float *__restrict__ Xold, int D,
                                                 float *__restrict__ ws, float *__restrict__ ne,
@@ -59,11 +61,10 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
     }
   }
   double sse = 0.0;
-  int jv;
-  float rv;
-  first_group(idx + it.start, val + it.start, it.len, zrow, jv, rv);
-  gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? LD - 16 * (T - 1) : -1, s_stage, jv, rv);
+  const float *__restrict__ wp = WT ? wts + it.start : nullptr;
+  const GroupLanes g0 = group_lanes<WT>(idx + it.start, val + it.start, wp, it.len, 0, zrow);
+  gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, it.len, Fp,
+                               zrow, AUG ? LD - 16 * (T - 1) : -1, s_stage, g0);
   if constexpr (!AUG) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
@@ -184,19 +185,32 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
     if (d < D) xr[d] = b[d];
 }
 
+template <int DP, int LD, bool AUG>
+static void launch_gram_ne_t(const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
+                             const int32_t *idx, const uint8_t *val, const float *wts,
+                             const float *Fp, int zrow, const float *Xold, int D, float *ws,
+                             float *ne, double *sse, hipStream_t s) {
+  if (wts)
+    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, true>), dim3((unsigned)n_items), dim3(64), 0, s,
+                       items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse);
+  else
+    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, false>), dim3((unsigned)n_items), dim3(64), 0, s,
+                       items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse);
+}
+
 hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
-                          const int32_t *idx, const uint8_t *val, const float *Fp,
-                          int64_t n_fixed, const float *Xold, float *ws, float *ne, double *sse,
-                          hipStream_t s) {
+                          const int32_t *idx, const uint8_t *val, const float *wts,
+                          const float *Fp, int64_t n_fixed, const float *Xold, float *ws,
+                          float *ne, double *sse, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
   const int zrow = (int)n_fixed;
   const int ld = lane_width(D);
   if (ld == 16)
-    hipLaunchKernelGGL((k_gram_ne<16, 16, false>), dim3((unsigned)n_items), dim3(64), 0, s, items,
-                       n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
+    launch_gram_ne_t<16, 16, false>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow, Xold,
+                                    D, ws, ne, sse, s);
   else if (ld == 20)
-    hipLaunchKernelGGL((k_gram_ne<32, 20, true>), dim3((unsigned)n_items), dim3(64), 0, s, items,
-                       n_chunk_items, idx, val, Fp, zrow, Xold, D, ws, ne, sse);
+    launch_gram_ne_t<32, 20, true>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow, Xold,
+                                   D, ws, ne, sse, s);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

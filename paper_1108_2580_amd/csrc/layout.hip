@@ -134,6 +134,46 @@ hipError_t launch_csc_build(const int64_t *row_ptr, const int32_t *col, const ui
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(64) void k_csc_scatter_f32(const int64_t *__restrict__ row_ptr,
+                                                        const int32_t *__restrict__ col,
+                                                        const float *__restrict__ w,
+                                                        int64_t n_rows, int64_t n_cols,
+                                                        int64_t rows_per_blk, int32_t *cnt,
+                                                        const int64_t *__restrict__ col_ptr,
+                                                        float *__restrict__ w_t) {
+  const int64_t b = blockIdx.x;
+  const int64_t r0 = b * rows_per_blk;
+  const int64_t r1 = r0 + rows_per_blk < n_rows ? r0 + rows_per_blk : n_rows;
+  int32_t *cb = cnt + b * n_cols;
+  for (int64_t r = r0; r < r1; ++r) {
+    const int64_t p1 = row_ptr[r + 1];
+    for (int64_t p = row_ptr[r] + threadIdx.x; p < p1; p += 64) {
+      const int32_t c = col[p];
+      const int32_t k = atomicAdd(&cb[c], 1);
+      w_t[col_ptr[c] + k] = w[p];
+    }
+    // claims of row r complete before any claim of row r + 1
+    __threadfence();
+  }
+}
+
+hipError_t launch_csc_permute_f32(const int64_t *row_ptr, const int32_t *col, const float *w,
+                                  int64_t n_rows, int64_t n_cols, int64_t rows_per_blk,
+                                  int64_t nblk, int32_t *scratch_cnt, int64_t *tot,
+                                  const int64_t *col_ptr, float *w_t, hipStream_t s) {
+  hipError_t e = launch_fill_i32(scratch_cnt, nblk * n_cols, 0, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_csc_count, dim3((unsigned)nblk), dim3(256), 0, s, row_ptr, col, n_rows,
+                     n_cols, rows_per_blk, scratch_cnt);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_csc_colscan, dim3((unsigned)((n_cols + 255) / 256)), dim3(256), 0, s,
+                     scratch_cnt, nblk, n_cols, tot);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_csc_scatter_f32, dim3((unsigned)nblk), dim3(64), 0, s, row_ptr, col, w,
+                     n_rows, n_cols, rows_per_blk, scratch_cnt, col_ptr, w_t);
+  return hipGetLastError();
+}
+
 // ---- fixed-order reduction of doubles --------------------------------------------------
 
 constexpr int kRedBlock = 256;

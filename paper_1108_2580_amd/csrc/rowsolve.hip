@@ -66,10 +66,11 @@ __host__ __device__ constexpr int aug_column(int D) {
 
 // Partial normal equations of the chunks of split rows, with the chunks'
 // entering-state squared residuals.
-template <int DP, bool AUG>
+template <int DP, bool AUG, bool WT>
 __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__ items,
                                                     const int32_t *__restrict__ idx,
                                                     const uint8_t *__restrict__ val,
+                                                    const float *__restrict__ wts,
                                                     const float *__restrict__ Fp, int zrow,
                                                     const float *__restrict__ Xold, int D,
                                                     float *__restrict__ ws,
@@ -92,11 +93,10 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
     }
   }
   double sse = 0.0;
-  int jv;
-  float rv;
-  first_group(idx + it.start, val + it.start, it.len, zrow, jv, rv);
-  gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + it.start, val + it.start, it.len, Fp, zrow,
-                           AUG ? aug_column<DP>(D) : -1, s_stage, jv, rv);
+  const float *__restrict__ wp = WT ? wts + it.start : nullptr;
+  const GroupLanes g0 = group_lanes<WT>(idx + it.start, val + it.start, wp, it.len, 0, zrow);
+  gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, it.len, Fp,
+                               zrow, AUG ? aug_column<DP>(D) : -1, s_stage, g0);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -129,10 +129,11 @@ constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 //   with one 4-term dot product per tile, and the trailing tiles are updated on MFMA
 //   (K = 4). Without the augmented column the right-hand side is eliminated along:
 //   y_p = M b_p, and b_j -= sum_r A[p0 + r][j] (M^T y_p)_r for the later columns.
-template <int DP, bool AUG>
+template <int DP, bool AUG, bool WT>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
-    const uint8_t *__restrict__ val, const float *__restrict__ Fp, int zrow,
+    const uint8_t *__restrict__ val, const float *__restrict__ wts,
+    const float *__restrict__ Fp, int zrow,
     const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
     double *__restrict__ sse_out,
     int32_t *__restrict__ flag_count, double *__restrict__ cyc_gram,
@@ -182,11 +183,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       xo[X] = 16 * X + c < D ? v : 0.f;
     }
     double sse = 0.0;
-    int jv;
-    float rv;
-    first_group(idx + rt.start, val + rt.start, rt.deg, zrow, jv, rv);
-    gram_accumulate<DP, AUG>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, rt.deg, Fp, zrow,
-                             aug_c, s_stage[wv], jv, rv);
+    const float *__restrict__ wp = WT ? wts + rt.start : nullptr;
+    const GroupLanes g0 = group_lanes<WT>(idx + rt.start, val + rt.start, wp, rt.deg, 0, zrow);
+    gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, rt.deg,
+                                 Fp, zrow, aug_c, s_stage[wv], g0);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -409,36 +409,64 @@ static constexpr bool has_aug(int D) {
   return ((D + 3) & ~3) < DP;
 }
 
+template <int DP, bool AUG, bool WT>
+static void launch_rows_k(int64_t blocks, const RowTask *rows, int64_t n_rows,
+                          const int32_t *idx, const uint8_t *val, const float *wts,
+                          const float *Fp, int zrow, const float *ws, int D, float lam, float *X,
+                          double *sse, int32_t *flag, double *cyc_gram, double *cyc_solve,
+                          hipStream_t s) {
+  hipLaunchKernelGGL((k_rows<DP, AUG, WT>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
+                     rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
+                     cyc_solve);
+}
+
 template <int DP>
 static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                                const uint8_t *val, const float *Fp, int zrow, const float *ws,
-                                int D, float lam, float *X, double *sse, int32_t *flag,
-                                double *cyc_gram, double *cyc_solve, hipStream_t s) {
+                                const uint8_t *val, const float *wts, const float *Fp, int zrow,
+                                const float *ws, int D, float lam, float *X, double *sse,
+                                int32_t *flag, double *cyc_gram, double *cyc_solve,
+                                hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
-  if (has_aug<DP>(D))
-    hipLaunchKernelGGL((k_rows<DP, true>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
-                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
-                       cyc_solve);
+  const bool aug = has_aug<DP>(D), wt = wts != nullptr;
+  if (aug && wt)
+    launch_rows_k<DP, true, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
+                                  sse, flag, cyc_gram, cyc_solve, s);
+  else if (aug)
+    launch_rows_k<DP, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
+                                   sse, flag, cyc_gram, cyc_solve, s);
+  else if (wt)
+    launch_rows_k<DP, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
+                                   sse, flag, cyc_gram, cyc_solve, s);
   else
-    hipLaunchKernelGGL((k_rows<DP, false>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
-                       rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
-                       cyc_solve);
+    launch_rows_k<DP, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
+                                    sse, flag, cyc_gram, cyc_solve, s);
   return hipGetLastError();
+}
+
+template <int DP, bool AUG, bool WT>
+static void launch_chunks_k(int64_t n, const WorkItem *items, const int32_t *idx,
+                            const uint8_t *val, const float *wts, const float *Fp, int zrow,
+                            const float *Xold, int D, float *ws, double *sse, hipStream_t s) {
+  hipLaunchKernelGGL((k_gram_chunks<DP, AUG, WT>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
+                     val, wts, Fp, zrow, Xold, D, ws, sse);
 }
 
 template <int DP>
 static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_t *idx,
-                                  const uint8_t *val, const float *Fp, int zrow,
-                                  const float *Xold, int D, float *ws, double *sse,
+                                  const uint8_t *val, const float *wts, const float *Fp,
+                                  int zrow, const float *Xold, int D, float *ws, double *sse,
                                   hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  if (has_aug<DP>(D))
-    hipLaunchKernelGGL((k_gram_chunks<DP, true>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
-                       val, Fp, zrow, Xold, D, ws, sse);
+  const bool aug = has_aug<DP>(D), wt = wts != nullptr;
+  if (aug && wt)
+    launch_chunks_k<DP, true, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+  else if (aug)
+    launch_chunks_k<DP, true, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+  else if (wt)
+    launch_chunks_k<DP, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
   else
-    hipLaunchKernelGGL((k_gram_chunks<DP, false>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
-                       val, Fp, zrow, Xold, D, ws, sse);
+    launch_chunks_k<DP, false, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
   return hipGetLastError();
 }
 
@@ -456,21 +484,22 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
   }
 
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
-                       const uint8_t *val, const float *Fp, int64_t n_fixed, const float *ws,
-                       int D, float lam, float *X, double *sse, int32_t *flag, double *cyc_gram,
-                       double *cyc_solve, hipStream_t s) {
+                       const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
+                       const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
+                       double *cyc_gram, double *cyc_solve, hipStream_t s) {
   if ((cyc_gram == nullptr) != (cyc_solve == nullptr)) return hipErrorInvalidValue;
   const int zrow = (int)n_fixed;
-  ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, Fp, zrow, ws, D, lam, X,
-                                              sse, flag, cyc_gram, cyc_solve, s));
+  ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam,
+                                              X, sse, flag, cyc_gram, cyc_solve, s));
 }
 
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
-                              const uint8_t *val, const float *Fp, int64_t n_fixed,
-                              const float *Xold, int D, float *ws, double *sse, hipStream_t s) {
+                              const uint8_t *val, const float *wts, const float *Fp,
+                              int64_t n_fixed, const float *Xold, int D, float *ws, double *sse,
+                              hipStream_t s) {
   const int zrow = (int)n_fixed;
-  ALS_DP_SWITCH(dp, return launch_chunks_t<DPV>(items, n, idx, val, Fp, zrow, Xold, D, ws, sse,
-                                                s));
+  ALS_DP_SWITCH(dp, return launch_chunks_t<DPV>(items, n, idx, val, wts, Fp, zrow, Xold, D, ws,
+                                                sse, s));
 }
 
 }  // namespace als

@@ -63,19 +63,26 @@ def gpu_half(als, side, fixed, prev, lam, rmse=False):
     return out.cpu().numpy(), r
 
 
-def check_first_half_sweeps(M, N, ptr, col, val, D, lam, U0, V0, tuning=None, label=""):
-    """Both sides from the same init: users from V0, items from U0."""
+def check_first_half_sweeps(M, N, ptr, col, val, D, lam, U0, V0, tuning=None, label="",
+                            weights=None):
+    """Both sides from the same init: users from V0, items from U0. ``weights``: per-rating
+    weights in CSR order (weighted ALS); the oracle gets them widened to fp64."""
     csr = (ptr, col, val.astype(np.float64))
     csc = oracle.transpose(ptr, col, val, N)
+    w_csr = None if weights is None else np.asarray(weights, dtype=np.float32).astype(np.float64)
+    w_csc = None if weights is None else oracle.transpose(ptr, col, w_csr, N)[2]
     rmse0 = oracle.rmse(ptr, col, val, U0, V0)
     with make_als(M, N, ptr, col, val, D, tuning) as als:
-        for side, fixed, prev, (p, i, v) in (("users", V0, U0, csr), ("items", U0, V0, csc)):
+        if weights is not None:
+            als.set_weights(weights)
+        for side, fixed, prev, (p, i, v), w in (("users", V0, U0, csr, w_csr),
+                                                ("items", U0, V0, csc, w_csc)):
             log(f"  {label} side={side} D={D}")
             xg, rm = gpu_half(als, side, fixed, prev, lam, rmse=True)
             rin = als.rmse_in()
             log(f"    entering-state rmse gpu {rin:.9f} oracle {rmse0:.9f}")
             assert abs(rin - rmse0) <= RMSE_TOL
-            xo, fl = oracle.half_sweep(p, i, v, fixed, lam, prev)
+            xo, fl = oracle.half_sweep(p, i, v, fixed, lam, prev, w=w)
             assert not (fl == 1).any()
             rel = rel_rows(xg, xo)
             log(f"    rel p50={np.median(rel):.2e} p99={np.percentile(rel, 99):.2e} "
@@ -307,6 +314,78 @@ def test_phase_timing_leaves_results_unchanged(D):
         else:
             assert g == 0 and s == 0
     log(f"  D={D} phase cycles {cyc_b}")
+
+
+# ---- weighted ALS ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("D", [10, 20, 33, 100, 128])
+def test_weighted_widths_with_split_rows(D):
+    M, N = 400, 300
+    ptr, col, val = small_matrix(D)
+    w = workload.rating_weights(col.size, seed=31 + D)
+    U0, V0 = workload.init_factors(M, N, D, seed=41 + D)
+    with make_als(M, N, ptr, col, val, D, dict(hub_threshold=40, chunk=24)) as als:
+        slot_bytes = als.plan_stats("users")["slot_bytes"]
+    tun = dict(hub_threshold=40, chunk=24, workspace_bytes=slot_bytes * 16)
+    check_first_half_sweeps(M, N, ptr, col, val, D, 0.065, U0, V0, tuning=tun,
+                            label=f"wals{D}", weights=w)
+    check_first_half_sweeps(M, N, ptr, col, val, D, 0.065, U0, V0, label=f"wals{D}-default",
+                            weights=w)
+
+
+@pytest.mark.parametrize("D", [20, 100])
+def test_unit_weights_are_plain_als_bitwise(D):
+    M, N = 400, 300
+    ptr, col, val = small_matrix(D + 1)
+    U0, V0 = workload.init_factors(M, N, D, seed=3)
+    outs = []
+    for mode in ("plain", "ones", "detached"):
+        with make_als(M, N, ptr, col, val, D, dict(hub_threshold=40, chunk=24)) as als:
+            if mode != "plain":
+                als.set_weights(np.ones(col.size, dtype=np.float32))
+            if mode == "detached":
+                als.set_weights(np.full(col.size, 2.5, dtype=np.float32))
+                als.set_weights(None)
+            xi, ri = gpu_half(als, "items", U0, V0, 0.065, rmse=True)
+            xu, ru = gpu_half(als, "users", xi, U0, 0.065, rmse=True)
+            outs.append((xi, xu, ri, ru))
+    for other in outs[1:]:
+        assert np.array_equal(outs[0][0], other[0]) and np.array_equal(outs[0][1], other[1])
+        assert outs[0][2] == other[2] and outs[0][3] == other[3]
+
+
+def test_weighted_rmse_free_running():
+    r = cfg(1)
+    w = workload.rating_weights(r.nnz, workload.weight_seed(1))
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    t = oracle.Trajectory(r.M, r.N, r.row_ptr, r.col, r.val, U0, V0, r.lam,
+                          w=w.astype(np.float64))
+    with make_als(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        als.set_weights(w)
+        U, V = dev(U0), dev(V0)
+        for sweep in range(1, r.sweeps + 1):
+            als.half_sweep("items", U, r.lam, V)
+            rm = als.half_sweep("users", V, r.lam, U, rmse=True)
+            t.sweep()
+            ro = t.rmse()
+            log(f"  weighted sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
+        assert abs(rm - ro) <= RMSE_TOL
+
+
+def test_weight_validation():
+    from paper_1108_2580_amd import ALS_ERR_INVALID_ARG, ALSError
+
+    M, N, D = 30, 20, 5
+    ptr, col, val = small_matrix(7, M=M, N=N)
+    with make_als(M, N, ptr, col, val, D) as als:
+        for bad in (-1.0, np.nan, np.inf):
+            w = np.ones(col.size, dtype=np.float32)
+            w[col.size // 2] = bad
+            with pytest.raises(ALSError) as ei:
+                als.set_weights(w)
+            assert ei.value.status == ALS_ERR_INVALID_ARG
+        with pytest.raises(ValueError):
+            als.set_weights(np.ones(col.size + 1, dtype=np.float32))
 
 
 def test_api_errors():
