@@ -45,6 +45,8 @@ def parse():
                     help="target duration of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for HBM counter scaling)")
+    ap.add_argument("--weighted", action="store_true",
+                    help="weighted ALS: seeded per-rating weights, log-uniform on [0.25, 4)")
     return ap.parse_args()
 
 
@@ -115,7 +117,7 @@ def measured_traffic(workload_name, kernel):
     return None
 
 
-def cpu_baseline(r, side_fixed, target_s):
+def cpu_baseline(r, side_fixed, target_s, weights=None):
     """fp64 oracle on a seeded random sample of the user half-sweep's rows."""
     import numpy as np
 
@@ -127,6 +129,7 @@ def cpu_baseline(r, side_fixed, target_s):
     perm = rows[rng.permutation(rows.size)]
     csum = np.cumsum(deg[perm])
     val = r.val.astype(np.float64)
+    w = None if weights is None else weights.astype(np.float64)
     fixed = side_fixed.astype(np.float64)
     threads = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
 
@@ -135,7 +138,7 @@ def cpu_baseline(r, side_fixed, target_s):
         k = min(k, perm.size)
         sel = np.sort(perm[:k])
         t0 = time.perf_counter()
-        oracle.solve_rows(sel, r.row_ptr, r.col, val, fixed, r.lam, threads=threads)
+        oracle.solve_rows(sel, r.row_ptr, r.col, val, fixed, r.lam, threads=threads, w=w)
         dt = time.perf_counter() - t0
         return int(deg[sel].sum()), k, dt
 
@@ -153,7 +156,8 @@ def cpu_baseline(r, side_fixed, target_s):
     n1, k1, t1 = run(target)
     return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
                 cpu_model=cpu_model,
-                sample=(f"user half-sweep of {r.name}: {k1} of {rows.size} rows (seeded random), "
+                sample=(f"user half-sweep of {r.name}{' (weighted)' if w is not None else ''}: "
+                        f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
 
@@ -180,6 +184,10 @@ def main():
     dev = torch.device("cuda:0")
     t_c = time.perf_counter()
     als = ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D)
+    weights = None
+    if args.weighted:
+        weights = workload.rating_weights(r.nnz, workload.weight_seed(args.config))
+        als.set_weights(weights)
     log(f"als_create (validation, upload, device CSC, schedules): "
         f"{time.perf_counter() - t_c:.1f} s; users {als.plan_stats('users')} "
         f"items {als.plan_stats('items')}")
@@ -233,12 +241,15 @@ def main():
     rows_with = als.plan_stats("users")["rows_with_ratings"] + \
         als.plan_stats("items")["rows_with_ratings"]
     D = r.D
+    workload_name = r.name + ("_wals" if args.weighted else "")
     dominant = max(prof, key=lambda k: prof[k][0])
+    wbytes = 4 if args.weighted else 0   # a weight per rating
+    wflops = D if args.weighted else 0   # c f per rating
     if D <= 20:
-        # gather kernel: per rating the index, the rating and the gathered fixed row; per
-        # solved row the row pointer and the entering value
+        # gather kernel: per rating the index, the rating (and weight) and the gathered fixed
+        # row; per solved row the row pointer and the entering value
         k_ms, k_n = prof["gather"]
-        alg = halves * r.nnz * (5 + 4 * D) + args.steps * rows_with * (8 + 4 * D)
+        alg = halves * r.nnz * (5 + wbytes + 4 * D) + args.steps * rows_with * (8 + 4 * D)
         achieved = alg / (k_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=achieved / HBM_PEAK_GBS, kernel="k_gram_ne")
@@ -247,20 +258,20 @@ def main():
         # right-hand side and residual dot per rating, Cholesky and two solves per row
         k_ms = prof["solve"][0] + prof["gather"][0]
         k_n = prof["solve"][1]
-        alg = halves * r.nnz * (D * (D + 1) + 4 * D) + \
+        alg = halves * r.nnz * (D * (D + 1) + 4 * D + wflops) + \
             args.steps * rows_with * (D ** 3 / 3.0 + 2.0 * D * D)
         achieved = alg / (k_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=achieved, peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s",
                     frac=achieved / MFMA_F32_PEAK_TFS, kernel="k_rows+k_gram_chunks")
     roof.update(launches=k_n, avg_launch_ms=k_ms / max(k_n, 1), alg_per_launch=alg / max(k_n, 1),
-                traffic=measured_traffic(r.name, roof["kernel"]), dominant_phase=dominant)
+                traffic=measured_traffic(workload_name, roof["kernel"]), dominant_phase=dominant)
     gram_phase = None
     if gram_share is not None:
         # Gram phase: the chunk kernel plus the share of the fused row kernel's wavefront
         # time spent before the factorisation (gather, Gram, RHS, residuals); flops in
         # the SYRK convention plus the right-hand side
         g_ms = (prof["gather"][0] + gram_share * prof["solve"][0]) / args.steps
-        g_flops = 2 * r.nnz * (D * (D + 1) + 2 * D)
+        g_flops = 2 * r.nnz * (D * (D + 1) + 2 * D + wflops)
         g_tf = g_flops / (g_ms * 1e-3) / 1e12
         gram_phase = dict(ms_per_step=g_ms, flops_per_step=g_flops, achieved=g_tf,
                           peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s", frac=g_tf / MFMA_F32_PEAK_TFS,
@@ -271,11 +282,11 @@ def main():
     cpu = None
     if args.cpu_seconds > 0:
         log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
-        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds)
+        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights)
         log(f"cpu baseline: {cpu}")
 
     out = {
-        "metric": "ALS ratings/sec per half-sweep",
+        "metric": ("wALS" if args.weighted else "ALS") + " ratings/sec per half-sweep",
         "value": value,
         "unit": "ratings/s",
         "n_gpus": 1,
@@ -287,7 +298,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": r.name, "n_users": r.M, "n_items": r.N, "nnz": r.nnz, "D": r.D,
+        "config": {"workload": workload_name, "n_users": r.M, "n_items": r.N, "nnz": r.nnz, "D": r.D,
+                   "weights": ("per rating, log-uniform on [0.25, 4), seeded" if args.weighted
+                               else None),
                    "lambda": r.lam, "step": "item half-sweep + user half-sweep",
                    "parallelism": "single GPU"},
         "roofline": roof,
