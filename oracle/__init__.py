@@ -14,7 +14,8 @@ the functions taking ``w`` (one non-negative weight per stored rating, in the
 same order as ``val``) solve x_s = (sum_j c_sj f_j f_j^T + lambda n_s I)^{-1}
 sum_j c_sj r_sj f_j; ``w=None`` is plain ALS, and unit weights reproduce it bitwise.
 A prediction is u_u . v_i (Sec. 2.2); RMSE (Sec. 4.1) is taken over the stored
-ratings. One sweep solves the items with the users fixed, then the users with
+ratings (training) or over a list of held-out (user, item, rating) triples
+(validation: ``predict``, ``pair_rmse``). One sweep solves the items with the users fixed, then the users with
 the items fixed (the order of Sec. 2.2).
 
 Pins (tests/test_oracle_pins.py) tie every function here to something other
@@ -67,6 +68,10 @@ def _configure(lib):
     lib.orc_sse.restype = f64
     lib.orc_weighted_norm.argtypes = [i64, P, i32, P]
     lib.orc_weighted_norm.restype = f64
+    lib.orc_predict.argtypes = [i64, P, P, i32, P, P, P, c_int]
+    lib.orc_predict.restype = None
+    lib.orc_pair_sse.argtypes = [i64, P, P, P, i32, P, P, c_int]
+    lib.orc_pair_sse.restype = f64
     return lib
 
 
@@ -193,6 +198,43 @@ def rmse(ptr, idx, val, X, F, threads=0):
 def weighted_norm(ptr, X):
     ptr, X = _i64(ptr), _f64(X)
     return _load().orc_weighted_norm(ptr.size - 1, _p(ptr), X.shape[1], _p(X))
+
+
+def _pairs(users, items, U, V):
+    users, items, U, V = _i32(users), _i32(items), _f64(U), _f64(V)
+    if users.shape != items.shape or users.ndim != 1:
+        raise ValueError("users and items must be 1-D arrays of one length")
+    if U.shape[1] != V.shape[1]:
+        raise ValueError("U and V have different widths")
+    if users.size and (users.min() < 0 or users.max() >= U.shape[0]
+                       or items.min() < 0 or items.max() >= V.shape[0]):
+        raise ValueError("pair index out of range")
+    return users, items, U, V
+
+
+def predict(users, items, U, V, threads=0):
+    """r_hat = u_u . v_i for each (users[p], items[p]) pair (fp64)."""
+    users, items, U, V = _pairs(users, items, U, V)
+    out = np.empty(users.size)
+    _load().orc_predict(users.size, _p(users), _p(items), U.shape[1], _p(U), _p(V), _p(out),
+                        int(threads))
+    return out
+
+
+def pair_sse(users, items, r, U, V, threads=0):
+    """Sum of (r - u_u . v_i)^2 over the pairs."""
+    users, items, U, V = _pairs(users, items, U, V)
+    r = _f64(r)
+    if r.shape != users.shape:
+        raise ValueError("one rating per pair")
+    return _load().orc_pair_sse(users.size, _p(users), _p(items), _p(r), U.shape[1], _p(U),
+                                _p(V), int(threads))
+
+
+def pair_rmse(users, items, r, U, V, threads=0):
+    """Validation RMSE (Sec. 4.1) over held-out (user, item, rating) triples."""
+    n = int(np.asarray(users).size)
+    return float(np.sqrt(pair_sse(users, items, r, U, V, threads) / n)) if n else 0.0
 
 
 def objective(csr, csc, U, V, lam, threads=0, w=None):

@@ -24,6 +24,11 @@
  * regulariser keeps the count n_s, so unit weights give plain ALS. Every function
  * that takes a weight array wt treats NULL as the unweighted method.
  *
+ * Held-out prediction (Sec. 2.2 prediction; Sec. 4.1 measures the RMSE on
+ * validation ratings that training did not see): for a list of (user, item)
+ * pairs, r_hat = u_u . v_i, and the validation RMSE is
+ * sqrt(sum over the pairs of (r - r_hat)^2 / number of pairs).
+ *
  * Everything is double precision, sequential within a row, rows in parallel
  * (OpenMP). Reductions over rows are done in row order from per-row values,
  * so every result is independent of the thread count.
@@ -220,5 +225,37 @@ double orc_weighted_norm(int64_t n_rows, const int64_t *ptr, int32_t D, const do
     for (int32_t a = 0; a < D; ++a) q += X[s * D + a] * X[s * D + a];
     total += (double)(ptr[s + 1] - ptr[s]) * q;
   }
+  return total;
+}
+
+/* Predictions r_hat_p = u_{users[p]} . v_{items[p]} (Sec. 2.2) of n pairs, each a
+ * dot product over the D features in feature order. Indices must be in range
+ * (checked by the caller). */
+void orc_predict(int64_t n, const int32_t *users, const int32_t *items, int32_t D,
+                 const double *U, const double *V, double *out, int nthreads) {
+  set_threads(nthreads);
+#pragma omp parallel for schedule(static)
+  for (int64_t p = 0; p < n; ++p) {
+    const double *u = U + (int64_t)users[p] * D;
+    const double *v = V + (int64_t)items[p] * D;
+    double dot = 0.0;
+    for (int32_t a = 0; a < D; ++a) dot += u[a] * v[a];
+    out[p] = dot;
+  }
+}
+
+/* Sum over n held-out pairs of (r_p - r_hat_p)^2 (the numerator of the validation
+ * RMSE of Sec. 4.1), from per-pair predictions summed in pair order. */
+double orc_pair_sse(int64_t n, const int32_t *users, const int32_t *items, const double *r,
+                    int32_t D, const double *U, const double *V, int nthreads) {
+  double *pred = (double *)malloc(sizeof(double) * (n > 0 ? n : 1));
+  if (!pred) return NAN;
+  orc_predict(n, users, items, D, U, V, pred, nthreads);
+  double total = 0.0;
+  for (int64_t p = 0; p < n; ++p) {
+    const double e = r[p] - pred[p];
+    total += e * e;
+  }
+  free(pred);
   return total;
 }

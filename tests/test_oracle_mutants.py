@@ -10,6 +10,7 @@ import pytest
 import oracle
 from tests import test_oracle_pins as pins
 from tests import test_oracle_weighted_pins as wpins
+from tests import test_oracle_predict_pins as qpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
 
@@ -34,9 +35,19 @@ MUTANTS = [
     ("weight_offset_wrong_row", "wt ? wt + ptr[s] : NULL, F, lambda, A, b, W, xs, X + s * D);",
      "wt ? wt + ptr[s] + 1 : NULL, F, lambda, A, b, W, xs, X + s * D);"),
     ("weighted_sse_unweighted", "acc += wt ? wt[p] * (e * e) : e * e;", "acc += e * e;"),
+    ("predict_user_row_from_item", "const double *u = U + (int64_t)users[p] * D;",
+     "const double *u = U + (int64_t)items[p] * D;"),
+    ("predict_last_feature_dropped", "for (int32_t a = 0; a < D; ++a) dot += u[a] * v[a];",
+     "for (int32_t a = 0; a + 1 < D; ++a) dot += u[a] * v[a];"),
+    ("pair_error_sign", "const double e = r[p] - pred[p];", "const double e = r[p] + pred[p];"),
+    ("pair_sse_first_dropped", "for (int64_t p = 0; p < n; ++p) {\n    const double e",
+     "for (int64_t p = 1; p < n; ++p) {\n    const double e"),
 ]
 
 PIN_TESTS = [
+    qpins.test_q1_golden_predictions,
+    qpins.test_q2_dense_pairs_are_the_matrix_product,
+    qpins.test_q3_stored_positions_give_the_training_sse,
     wpins.test_w1_unit_weights_are_plain_als,
     lambda: wpins.test_w2_matches_weighted_lstsq(3),
     wpins.test_w3_weighted_gradient_zero,

@@ -59,3 +59,48 @@ def test_init_factors():
     assert abs(float(U.std()) - 0.1) < 0.02
     U2, V2 = workload.init_factors(100, 50, 7, seed=3)
     assert np.array_equal(U, U2) and np.array_equal(V, V2)
+
+
+def test_holdout_split_partitions_the_ratings():
+    r = workload.make_config(1)
+    tp, tc, tv, hu, hi, hv = workload.holdout_split(r.row_ptr, r.col, r.val, 0.1,
+                                                    workload.holdout_seed(1), min_keep=3)
+    assert tp[-1] + hu.size == r.nnz
+    assert 0.08 * r.nnz < hu.size < 0.12 * r.nnz
+    assert np.diff(tp).min() >= min(3, int(np.diff(r.row_ptr).min()))
+    # the union of the two parts is the original set of triples, with no overlap
+    rows = np.repeat(np.arange(r.M), np.diff(tp))
+    both = np.concatenate([rows.astype(np.int64) * r.N + tc, hu.astype(np.int64) * r.N + hi])
+    orig = np.repeat(np.arange(r.M), np.diff(r.row_ptr)).astype(np.int64) * r.N + r.col
+    order = np.argsort(both)
+    assert np.array_equal(both[order], np.sort(orig))
+    vals = np.concatenate([tv, hv])[order]
+    assert np.array_equal(vals, r.val[np.argsort(orig)])
+    # held-out triples in CSR order; training columns still strictly increasing per row
+    key = hu.astype(np.int64) * r.N + hi
+    assert np.all(np.diff(key) > 0)
+    for u in range(0, r.M, 97):
+        assert np.all(np.diff(tc[tp[u]:tp[u + 1]]) > 0)
+    again = workload.holdout_split(r.row_ptr, r.col, r.val, 0.1, workload.holdout_seed(1), 3)
+    assert all(np.array_equal(a, b) for a, b in zip(again, (tp, tc, tv, hu, hi, hv)))
+
+
+def test_holdout_split_keeps_min_ratings_of_light_users():
+    ptr = np.array([0, 1, 3, 8], dtype=np.int64)
+    col = np.array([0, 0, 1, 0, 1, 2, 3, 4], dtype=np.int32)
+    val = np.arange(8, dtype=np.uint8)
+    tp, tc, tv, hu, hi, hv = workload.holdout_split(ptr, col, val, 1.0, 1, min_keep=2)
+    assert list(np.diff(tp)) == [1, 2, 2]
+    assert list(hu) == [2, 2, 2] and list(hi) == [2, 3, 4] and list(hv) == [5, 6, 7]
+
+
+def test_stored_pairs_are_stored_positions():
+    r = workload.make_config(1)
+    u, i, v = workload.stored_pairs(r.row_ptr, r.col, r.val, 777, 3)
+    assert u.size == 777
+    key = u.astype(np.int64) * r.N + i
+    assert np.all(np.diff(key) > 0)
+    for a, b, c in zip(u[:50], i[:50], v[:50]):
+        s, e = r.row_ptr[a], r.row_ptr[a + 1]
+        k = s + np.searchsorted(r.col[s:e], b)
+        assert r.col[k] == b and r.val[k] == c

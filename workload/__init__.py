@@ -346,6 +346,53 @@ def weight_seed(k: int) -> int:
     return data_seed(k) + 2000
 
 
+def holdout_seed(k: int) -> int:
+    """Seed of the held-out selection of config k."""
+    return data_seed(k) + 3000
+
+
+def holdout_split(row_ptr: np.ndarray, col: np.ndarray, val: np.ndarray, frac: float, seed: int,
+                  min_keep: int = 1) -> tuple:
+    """Move a seeded random share ``frac`` of the stored ratings into a held-out list.
+
+    Every user keeps at least ``min_keep`` training ratings (fewer only where it has
+    fewer in total). Returns ``(train_ptr, train_col, train_val, users, items, ratings)``:
+    the training matrix in CSR, and the held-out triples in CSR order (by user, then
+    item), int32 / int32 / uint8."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    nnz = int(row_ptr[-1])
+    M = row_ptr.size - 1
+    rng = np.random.default_rng(seed)
+    held = rng.random(nnz) < frac
+    rows = np.repeat(np.arange(M, dtype=np.int64), np.diff(row_ptr))
+    # give back the held ratings of users that would keep too few, first ones first
+    deg = np.diff(row_ptr)
+    kept = deg - np.bincount(rows[held], minlength=M)
+    short = np.nonzero(kept < np.minimum(min_keep, deg))[0]
+    for u in short:
+        need = min(min_keep, int(deg[u])) - int(kept[u])
+        hs = np.nonzero(held[row_ptr[u]:row_ptr[u + 1]])[0][:need]
+        held[row_ptr[u] + hs] = False
+    keep = ~held
+    train_ptr = np.concatenate([[0], np.cumsum(np.bincount(rows[keep], minlength=M))]).astype(np.int64)
+    return (train_ptr, np.ascontiguousarray(col[keep], dtype=np.int32),
+            np.ascontiguousarray(val[keep], dtype=np.uint8), rows[held].astype(np.int32),
+            np.ascontiguousarray(col[held], dtype=np.int32),
+            np.ascontiguousarray(val[held], dtype=np.uint8))
+
+
+def stored_pairs(row_ptr: np.ndarray, col: np.ndarray, val: np.ndarray, n: int, seed: int) -> tuple:
+    """A seeded sample of ``n`` distinct stored positions as (users, items, ratings), in
+    CSR order: pairs with the degree distributions of the matrix on both sides."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    nnz = int(row_ptr[-1])
+    rng = np.random.default_rng(seed)
+    pos = np.sort(rng.choice(nnz, size=min(n, nnz), replace=False))
+    users = (np.searchsorted(row_ptr, pos, side="right") - 1).astype(np.int32)
+    return users, np.ascontiguousarray(col[pos], dtype=np.int32), np.ascontiguousarray(
+        val[pos], dtype=np.uint8)
+
+
 def degree_stats(ptr: np.ndarray) -> dict:
     d = np.diff(ptr)
     return dict(n=int(d.size), total=int(d.sum()), max=int(d.max()), p99=float(np.percentile(d, 99)),
