@@ -45,6 +45,8 @@ def parse():
                     help="target duration of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for HBM counter scaling)")
+    ap.add_argument("--heldout-share", type=int, default=64,
+                    help="held-out prediction leg on 1/K of the stored positions (0 disables)")
     ap.add_argument("--weighted", action="store_true",
                     help="weighted ALS: seeded per-rating weights, log-uniform on [0.25, 4)")
     return ap.parse_args()
@@ -159,6 +161,48 @@ def cpu_baseline(r, side_fixed, target_s, weights=None):
                 sample=(f"user half-sweep of {r.name}{' (weighted)' if w is not None else ''}: "
                         f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
+
+
+def heldout_leg(args, r, als, U, V, workload_name, reps=20):
+    """Held-out predictions r_hat = u . v on a seeded sample of the stored positions (the
+    degree distributions of both sides), timed over back-to-back launches of the predict
+    kernel; plus the validation RMSE of the same pairs through the registered-set path."""
+    import torch
+    import workload
+
+    n = r.nnz // args.heldout_share
+    hu, hi, hr = workload.stored_pairs(r.row_ptr, r.col, r.val, n,
+                                       workload.holdout_seed(args.config))
+    dev = U.device
+    du = torch.from_numpy(hu).to(dev)
+    di = torch.from_numpy(hi).to(dev)
+    pred = torch.empty(n, dtype=torch.float32, device=dev)
+    als.predict(U, V, du, di, out=pred)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        als.predict(U, V, du, di, out=pred)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    als.set_holdout(hu, hi, hr)
+    vr = als.holdout_rmse(U, V)
+    # algorithmic bytes per pair: two 4-byte indices, the 4-byte prediction written and
+    # the two gathered D-vectors
+    alg = n * (12 + 8 * r.D)
+    achieved = alg / (ms * 1e-3) / 1e9
+    log(f"held-out leg: {n} pairs, {ms:.4f} ms per launch, {achieved:.0f} GB/s algorithmic")
+    return dict(metric="held-out predictions/sec", value=n / (ms * 1e-3), unit="pairs/s",
+                pairs=n, launches=reps, ms_per_launch=ms,
+                sample=(f"1/{args.heldout_share} of the stored positions of {r.name}, seeded, "
+                        f"in CSR order; factors after the timed sweeps"),
+                roofline=dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                              frac=achieved / HBM_PEAK_GBS, kernel="k_predict",
+                              alg_per_launch=alg,
+                              traffic=measured_traffic(workload_name + "_heldout", "k_predict")),
+                rmse_same_pairs=vr)
 
 
 def main():
@@ -279,6 +323,8 @@ def main():
                           method="chunk-kernel time plus the row kernel's time scaled by the "
                                  "share of wavefront clock cycles before the factorisation")
 
+    heldout = heldout_leg(args, r, als, U, V, workload_name) if args.heldout_share > 0 else None
+
     cpu = None
     if args.cpu_seconds > 0:
         log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
@@ -310,6 +356,7 @@ def main():
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
         "rmse": rmse,
         "rmse_entering_last_half_sweep": rmse_in,
+        "heldout": heldout,
     }
     print(json.dumps(out), flush=True)
     als.close()

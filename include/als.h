@@ -186,6 +186,39 @@ als_status als_set_phase_timing(als_ctx *ctx, int32_t enable);
 als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles,
                                 double *solve_cycles);
 
+/*
+ * Held-out prediction (paper Sec. 2.2: a prediction is the dot product of the user's
+ * and the item's vector) for n_pairs (user, item) pairs:
+ *   pred[p] = U[users[p], :] . V[items[p], :]   (fp32, features summed in order).
+ *   U, V          device fp32 [n_users x D], [n_items x D], 16-byte aligned.
+ *   users, items  device int32[n_pairs]; a pair with an index outside the tables gets
+ *                 pred = NaN and reads nothing.
+ *   pred          device fp32[n_pairs], caller-owned, overlapping none of the inputs.
+ * Enqueued on the context's stream without synchronisation. n_pairs = 0 does nothing;
+ * n_pairs above 2^31 * 256 - 256 is ALS_ERR_INVALID_ARG.
+ */
+als_status als_predict(als_ctx *ctx, const float *U, const float *V, int64_t n_pairs,
+                       const int32_t *users, const int32_t *items, float *pred);
+
+/*
+ * Register a validation set (Sec. 4.1 reports RMSE on ratings held out of training):
+ * host arrays of n_pairs users, items and ratings. Every index is checked against the
+ * matrix shape (ALS_ERR_INVALID_ARG, nothing registered). The library copies the pairs
+ * to the device, grouped by user (stable, so the caller's order within a user stays),
+ * and replaces any earlier set; n_pairs = 0 registers an empty set. Duplicates and
+ * pairs that are also training ratings are allowed. Synchronises the stream.
+ */
+als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
+                           const int32_t *items, const uint8_t *ratings);
+
+/*
+ * Validation RMSE of (U, V) on the registered pairs:
+ * sqrt(sum over pairs of (r - u_u . v_i)^2 / n_pairs), squared errors summed in fp64 in a
+ * fixed order (bitwise reproducible). 0 for an empty set; ALS_ERR_INVALID_ARG when no set
+ * is registered. U, V as for als_predict. Synchronises the stream.
+ */
+als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
+
 void als_destroy(als_ctx *ctx);
 
 const char *als_status_str(als_status s);

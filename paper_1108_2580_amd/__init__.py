@@ -24,8 +24,8 @@ _SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
 EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_flagged_rows",
            "als_get_csc",
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_weights",
-           "als_set_phase_timing", "als_get_phase_cycles", "als_destroy", "als_status_str",
-           "als_last_error")
+           "als_set_phase_timing", "als_get_phase_cycles", "als_predict", "als_set_holdout",
+           "als_holdout_rmse", "als_destroy", "als_status_str", "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
 
@@ -75,6 +75,12 @@ def _load_library(path=LIB_PATH):
     lib.als_get_phase_cycles.argtypes = [P, st, ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_double)]
     lib.als_get_phase_cycles.restype = st
+    lib.als_predict.argtypes = [P, P, P, i64, P, P, P]
+    lib.als_predict.restype = st
+    lib.als_set_holdout.argtypes = [P, i64, P, P, P]
+    lib.als_set_holdout.restype = st
+    lib.als_holdout_rmse.argtypes = [P, P, P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_holdout_rmse.restype = st
     lib.als_destroy.argtypes = [P]
     lib.als_destroy.restype = None
     lib.als_status_str.argtypes = [st]
@@ -213,6 +219,48 @@ class ALS:
         v = ctypes.c_double(0.0)
         self._check(lib.als_get_phase_cycles(self._h, _SIDES[side], ctypes.byref(g), ctypes.byref(v)))
         return g.value, v.value
+
+    def predict(self, U, V, users, items, out=None):
+        """r_hat = u_u . v_i for device int32 tensors ``users`` and ``items`` (one pair per
+        element); returns ``out`` (a new fp32 tensor unless given). NaN marks a pair whose
+        index is outside the tables."""
+        import torch
+
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        for t, name in ((users, "users"), (items, "items")):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or \
+                    t.dtype != torch.int32 or not t.is_contiguous() or t.dim() != 1:
+                raise TypeError(f"{name} must be a contiguous 1-D int32 CUDA tensor")
+        n = users.numel()
+        if items.numel() != n:
+            raise ValueError("users and items differ in length")
+        if out is None:
+            out = torch.empty(n, dtype=torch.float32, device=users.device)
+        elif out.dtype != torch.float32 or not out.is_contiguous() or out.numel() != n or \
+                out.device.type != "cuda":
+            raise TypeError("out must be a contiguous fp32 CUDA tensor with one element per pair")
+        self._check(lib.als_predict(self._h, up, vp, n, ctypes.c_void_p(users.data_ptr()),
+                                    ctypes.c_void_p(items.data_ptr()),
+                                    ctypes.c_void_p(out.data_ptr())))
+        return out
+
+    def set_holdout(self, users, items, ratings):
+        """Register held-out (user, item, rating) triples (host arrays) for holdout_rmse."""
+        u = np.ascontiguousarray(users, dtype=np.int32)
+        i = np.ascontiguousarray(items, dtype=np.int32)
+        r = np.ascontiguousarray(ratings, dtype=np.uint8)
+        if not (u.shape == i.shape == r.shape) or u.ndim != 1:
+            raise ValueError("users, items and ratings must be 1-D arrays of one length")
+        self._check(lib.als_set_holdout(self._h, u.size, _np_ptr(u), _np_ptr(i), _np_ptr(r)))
+
+    def holdout_rmse(self, U, V):
+        """Validation RMSE of (U, V) on the registered held-out triples."""
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        r = ctypes.c_double(0.0)
+        self._check(lib.als_holdout_rmse(self._h, up, vp, ctypes.byref(r)))
+        return r.value
 
     def close(self):
         if getattr(self, "_h", None):

@@ -106,6 +106,13 @@ struct als_ctx {
   double *d_cyc_sum = nullptr;    // [2]
   double *h_cyc_sum = nullptr;    // pinned [2]
   double cyc[2][2] = {{0, 0}, {0, 0}};  // per side: Gram, solve
+  int64_t n_hold = -1;             // held-out pairs (-1: none registered)
+  int32_t *d_hu = nullptr;         // held-out users, items and ratings, in CSR order
+  int32_t *d_hi = nullptr;
+  uint8_t *d_hr = nullptr;
+  double *d_hold_blocks = nullptr; // per-block squared errors
+  double *d_hold_partials = nullptr;
+  double *d_hold_sse = nullptr;
 };
 
 namespace {
@@ -271,6 +278,24 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   return ALS_OK;
 }
 
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+// pairs of one predict call: the launch has pair_blocks(n) < 2^31 blocks
+constexpr int64_t kMaxPairs = 0x7fffffffLL * 256;
+
+void free_holdout(als_ctx *c) {
+  dfree(c->d_hu);
+  dfree(c->d_hi);
+  dfree(c->d_hr);
+  dfree(c->d_hold_blocks);
+  dfree(c->d_hold_partials);
+  dfree(c->d_hold_sse);
+  c->n_hold = -1;
+}
+
 void free_ctx(als_ctx *c) {
   if (!c) return;
   DeviceGuard g(c->device);
@@ -299,6 +324,7 @@ void free_ctx(als_ctx *c) {
   if (c->h_flag) (void)hipHostFree(c->h_flag);
   dfree(c->d_cyc);
   dfree(c->d_cyc_sum);
+  free_holdout(c);
   if (c->h_cyc_sum) (void)hipHostFree(c->h_cyc_sum);
   for (auto &pe : c->prof_pending) {
     (void)hipEventDestroy(pe.a);
@@ -805,6 +831,108 @@ als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles
   if (!gram_cycles || !solve_cycles) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
   *gram_cycles = ctx->cyc[side][0];
   *solve_cycles = ctx->cyc[side][1];
+  return ALS_OK;
+}
+
+// ---- held-out predictions ----------------------------------------------------------
+
+als_status als_predict(als_ctx *ctx, const float *U, const float *V, int64_t n_pairs,
+                       const int32_t *users, const int32_t *items, float *pred) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (n_pairs < 0 || n_pairs > kMaxPairs)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "n_pairs out of range");
+  if (n_pairs == 0) return ALS_OK;
+  if (!U || !V || !users || !items || !pred) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  const size_t pb = sizeof(float) * (size_t)n_pairs;
+  if (overlaps(pred, pb, U, sizeof(float) * ctx->M * ctx->D) ||
+      overlaps(pred, pb, V, sizeof(float) * ctx->N * ctx->D) ||
+      overlaps(pred, pb, users, sizeof(int32_t) * n_pairs) ||
+      overlaps(pred, pb, items, sizeof(int32_t) * n_pairs))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "pred overlaps an input");
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, als::launch_predict(U, V, ctx->M, ctx->N, ctx->D, n_pairs, users, items,
+                                       nullptr, pred, nullptr, ctx->stream));
+  return ALS_OK;
+}
+
+als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
+                           const int32_t *items, const uint8_t *ratings) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (n_pairs < 0 || n_pairs > kMaxPairs)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "n_pairs out of range");
+  if (n_pairs > 0 && (!users || !items || !ratings))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  for (int64_t p = 0; p < n_pairs; ++p) {
+    if (users[p] < 0 || users[p] >= ctx->M || items[p] < 0 || items[p] >= ctx->N)
+      return fail(ctx, ALS_ERR_INVALID_ARG, "pair %lld: (%d, %d) outside %lld x %lld",
+                  (long long)p, users[p], items[p], (long long)ctx->M, (long long)ctx->N);
+  }
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  free_holdout(ctx);
+  if (n_pairs == 0) {
+    ctx->n_hold = 0;
+    return ALS_OK;
+  }
+  // counting sort by user, stable: pairs of one user become adjacent (their u rows are
+  // then read once from memory), in the caller's order within a user
+  std::vector<int64_t> start(ctx->M + 1, 0);
+  for (int64_t p = 0; p < n_pairs; ++p) start[users[p] + 1] += 1;
+  for (int64_t u = 0; u < ctx->M; ++u) start[u + 1] += start[u];
+  std::vector<int32_t> hu(n_pairs), hi(n_pairs);
+  std::vector<uint8_t> hr(n_pairs);
+  for (int64_t p = 0; p < n_pairs; ++p) {
+    const int64_t q = start[users[p]]++;
+    hu[q] = users[p];
+    hi[q] = items[p];
+    hr[q] = ratings[p];
+  }
+  const int64_t nb = als::pair_blocks(n_pairs);
+  hipError_t e = dalloc(&ctx->d_hu, n_pairs);
+  if (e == hipSuccess) e = dalloc(&ctx->d_hi, n_pairs);
+  if (e == hipSuccess) e = dalloc(&ctx->d_hr, n_pairs);
+  if (e == hipSuccess) e = dalloc(&ctx->d_hold_blocks, nb);
+  if (e == hipSuccess) e = dalloc(&ctx->d_hold_partials, als::reduce_partials(nb));
+  if (e == hipSuccess) e = dalloc(&ctx->d_hold_sse, 1);
+  if (e == hipSuccess)
+    e = hipMemcpy(ctx->d_hu, hu.data(), sizeof(int32_t) * n_pairs, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(ctx->d_hi, hi.data(), sizeof(int32_t) * n_pairs, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(ctx->d_hr, hr.data(), n_pairs, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    free_holdout(ctx);
+    return fail(ctx, e == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP,
+                "held-out pairs: %s", hipGetErrorString(e));
+  }
+  ctx->n_hold = n_pairs;
+  return ALS_OK;
+}
+
+als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!U || !V || !rmse_out) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (ctx->n_hold < 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no held-out pairs registered");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  if (ctx->n_hold == 0) {
+    *rmse_out = 0.0;
+    return ALS_OK;
+  }
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, als::launch_predict(U, V, ctx->M, ctx->N, ctx->D, ctx->n_hold, ctx->d_hu,
+                                       ctx->d_hi, ctx->d_hr, nullptr, ctx->d_hold_blocks,
+                                       ctx->stream));
+  HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_hold_blocks, als::pair_blocks(ctx->n_hold),
+                                      ctx->d_hold_partials, ctx->d_hold_sse, ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_hold_sse, sizeof(double),
+                                  hipMemcpyDeviceToHost, ctx->stream));
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  *rmse_out = std::sqrt(*ctx->h_sse / (double)ctx->n_hold);
   return ALS_OK;
 }
 
