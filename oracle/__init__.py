@@ -68,6 +68,12 @@ def _configure(lib):
     lib.orc_sse.restype = f64
     lib.orc_weighted_norm.argtypes = [i64, P, i32, P]
     lib.orc_weighted_norm.restype = f64
+    lib.orc_gibbs_rows.argtypes = [i64, P, P, P, i32, P, f64, P, P, P, P, P, c_int]
+    lib.orc_gibbs_rows.restype = i64
+    lib.orc_nw_posterior.argtypes = [i64, i32, P, P, f64, P, f64, P, P, P, P]
+    lib.orc_nw_posterior.restype = None
+    lib.orc_nw_sample.argtypes = [i32, P, f64, P, P, P, P, P, P]
+    lib.orc_nw_sample.restype = c_int
     lib.orc_predict.argtypes = [i64, P, P, i32, P, P, P, c_int]
     lib.orc_predict.restype = None
     lib.orc_pair_sse.argtypes = [i64, P, P, P, i32, P, P, c_int]
@@ -280,3 +286,50 @@ class Trajectory:
 
     def objective(self):
         return objective(self.csr, self.csc, self.U, self.V, self.lam, self.threads, w=self.w)
+
+
+# ---- Bayesian (BPMF / BPTF) Gibbs step -------------------------------------------------------
+
+def gibbs_rows(ptr, idx, val, F, alpha, Lam, mu, z, X_prev, threads=0):
+    """Conditional draw of every row: Lambda* = Lambda + alpha sum f f^T,
+    x = mu* + L*^{-T} z. Returns (X, flags); flagged rows (not SPD) keep X_prev."""
+    ptr, idx, val, F = _i64(ptr), _i32(idx), _f64(val), _f64(F)
+    Lam, mu, z = _f64(Lam), _f64(mu), _f64(z)
+    n_rows = ptr.size - 1
+    D = F.shape[1]
+    if Lam.shape != (D, D) or mu.shape != (D,) or z.shape != (n_rows, D):
+        raise ValueError("Lambda must be D x D, mu of length D, z n_rows x D")
+    X = np.array(X_prev, dtype=np.float64, order="C", copy=True)
+    assert X.shape == (n_rows, D)
+    flags = np.empty(n_rows, dtype=np.int8)
+    _load().orc_gibbs_rows(n_rows, _p(ptr), _p(idx), _p(val), D, _p(F), float(alpha), _p(Lam),
+                           _p(mu), _p(z), _p(X), _p(flags), int(threads))
+    return X, flags
+
+
+def nw_posterior(X, mu0, beta0, W0inv, nu0):
+    """Normal-Wishart posterior given the rows of X: (mu*, beta*, W*^{-1}, nu*)."""
+    X, mu0, W0inv = _f64(X), _f64(mu0), _f64(W0inv)
+    n, D = X.shape
+    mu_s = np.empty(D)
+    Winv = np.empty((D, D))
+    b = ctypes.c_double()
+    v = ctypes.c_double()
+    _load().orc_nw_posterior(n, D, _p(X), _p(mu0), float(beta0), _p(W0inv), float(nu0),
+                             _p(mu_s), _p(Winv), ctypes.byref(b), ctypes.byref(v))
+    return mu_s, b.value, Winv, v.value
+
+
+def nw_sample(mu_s, beta_s, Winv_s, chi2, offd, zmu):
+    """Bartlett draw of (mu, Lambda) from the Normal-Wishart with the given parameters;
+    chi2[i] ~ chi-square(nu* - i), offd: D (D - 1) / 2 standard normals (strict lower
+    triangle, row order), zmu: D standard normals. None if a factorisation fails."""
+    mu_s, Winv_s, chi2, zmu = _f64(mu_s), _f64(Winv_s), _f64(chi2), _f64(zmu)
+    D = mu_s.size
+    offd = _f64(offd) if D > 1 else np.zeros(1)
+    mu = np.empty(D)
+    Lam = np.empty((D, D))
+    if _load().orc_nw_sample(D, _p(mu_s), float(beta_s), _p(Winv_s), _p(chi2), _p(offd),
+                             _p(zmu), _p(mu), _p(Lam)) != 0:
+        return None
+    return mu, Lam

@@ -29,6 +29,18 @@
  * pairs, r_hat = u_u . v_i, and the validation RMSE is
  * sqrt(sum over the pairs of (r - r_hat)^2 / number of pairs).
  *
+ * Bayesian factorisation (BPTF, named in Sec. 2.2 as least squares plus sampling from the
+ * hyperpriors of U and V; the published BPMF/BPTF Gibbs sampler): ratings are Gaussian
+ * with precision alpha around u . v, each row of a side has the prior N(mu, Lambda^{-1}),
+ * and (mu, Lambda) have a Normal-Wishart hyperprior. One Gibbs step for a side draws
+ *   - the hyperparameters from their Normal-Wishart posterior given the side's rows
+ *     (orc_nw_posterior, orc_nw_sample: Bartlett's construction of the Wishart draw);
+ *   - every row from its Gaussian conditional (orc_gibbs_rows):
+ *     Lambda* = Lambda + alpha sum_j f_j f_j^T, mu* = Lambda*^{-1} (alpha sum_j r_sj f_j
+ *     + Lambda mu), x = mu* + L*^{-T} z with Lambda* = L* L*^T and z standard normal.
+ * The standard normal, chi-square and normal variates are inputs, so a draw is a
+ * deterministic function of them.
+ *
  * Everything is double precision, sequential within a row, rows in parallel
  * (OpenMP). Reductions over rows are done in row order from per-row values,
  * so every result is independent of the thread count.
@@ -258,4 +270,187 @@ double orc_pair_sse(int64_t n, const int32_t *users, const int32_t *items, const
   }
   free(pred);
   return total;
+}
+
+/* ---- Bayesian (BPMF / BPTF) Gibbs step ------------------------------------------------ */
+
+/* Lower Cholesky factor: A = L L^T (A full D x D row-major, lower triangle read; L written
+ * to the lower triangle of L, upper triangle zeroed). Returns 0, or 1 if not SPD. */
+static int chol_lower(int32_t D, const double *A, double *L) {
+  for (int32_t i = 0; i < D; ++i)
+    for (int32_t j = 0; j < D; ++j) L[i * D + j] = 0.0;
+  for (int32_t i = 0; i < D; ++i) {
+    for (int32_t j = 0; j <= i; ++j) {
+      double s = A[i * D + j];
+      for (int32_t m = 0; m < j; ++m) s -= L[i * D + m] * L[j * D + m];
+      if (i == j) {
+        if (!(s > 0.0) || !isfinite(s)) return 1;
+        L[i * D + i] = sqrt(s);
+      } else {
+        L[i * D + j] = s / L[j * D + j];
+      }
+    }
+  }
+  return 0;
+}
+
+/* y = L^{-1} b (forward substitution, L lower). */
+static void solve_lower(int32_t D, const double *L, const double *b, double *y) {
+  for (int32_t i = 0; i < D; ++i) {
+    double s = b[i];
+    for (int32_t m = 0; m < i; ++m) s -= L[i * D + m] * y[m];
+    y[i] = s / L[i * D + i];
+  }
+}
+
+/* x = L^{-T} y (back substitution with the transpose of the lower factor). */
+static void solve_lower_t(int32_t D, const double *L, const double *y, double *x) {
+  for (int32_t i = D - 1; i >= 0; --i) {
+    double s = y[i];
+    for (int32_t m = i + 1; m < D; ++m) s -= L[m * D + i] * x[m];
+    x[i] = s / L[i * D + i];
+  }
+}
+
+/* Conditional draw of every row s of the solved side given the fixed side F:
+ *   Lambda* = Lambda + alpha sum_j f_j f_j^T,  h = alpha sum_j r_sj f_j + Lambda mu,
+ *   Lambda* = L L^T,  X[s] = L^{-T} (L^{-1} h + z_s)  (= mu* + L^{-T} z_s),
+ * with z the n_rows x D standard normal variates. A row without ratings is drawn from the
+ * prior. flags[s]: 0 drawn, 1 Lambda* not numerically SPD (row left unchanged). Returns
+ * the number of flagged rows. */
+int64_t orc_gibbs_rows(int64_t n_rows, const int64_t *ptr, const int32_t *idx, const double *val,
+                       int32_t D, const double *F, double alpha, const double *Lambda,
+                       const double *mu, const double *z, double *X, int8_t *flags,
+                       int nthreads) {
+  set_threads(nthreads);
+  int64_t nflag = 0;
+#pragma omp parallel reduction(+ : nflag)
+  {
+    double *A = (double *)malloc(sizeof(double) * D * D);
+    double *L = (double *)malloc(sizeof(double) * D * D);
+    double *h = (double *)malloc(sizeof(double) * D);
+    double *y = (double *)malloc(sizeof(double) * D);
+    double *x = (double *)malloc(sizeof(double) * D);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t s = 0; s < n_rows; ++s) {
+      for (int32_t a = 0; a < D * D; ++a) A[a] = 0.0;
+      for (int32_t a = 0; a < D; ++a) h[a] = 0.0;
+      for (int64_t k = ptr[s]; k < ptr[s + 1]; ++k) {
+        const double *f = F + (int64_t)idx[k] * D;
+        for (int32_t a = 0; a < D; ++a) {
+          for (int32_t e = 0; e < D; ++e) A[a * D + e] += f[a] * f[e];
+          h[a] += val[k] * f[a];
+        }
+      }
+      for (int32_t a = 0; a < D; ++a) {
+        double lm = 0.0;
+        for (int32_t e = 0; e < D; ++e) lm += Lambda[a * D + e] * mu[e];
+        h[a] = alpha * h[a] + lm;
+        for (int32_t e = 0; e < D; ++e) A[a * D + e] = alpha * A[a * D + e] + Lambda[a * D + e];
+      }
+      int st = chol_lower(D, A, L);
+      if (st == 0) {
+        solve_lower(D, L, h, y);
+        for (int32_t a = 0; a < D; ++a) y[a] += z[s * D + a];
+        solve_lower_t(D, L, y, x);
+        for (int32_t a = 0; a < D; ++a) {
+          if (!isfinite(x[a])) st = 1;
+        }
+      }
+      if (st == 0) {
+        for (int32_t a = 0; a < D; ++a) X[s * D + a] = x[a];
+      }
+      if (flags) flags[s] = (int8_t)st;
+      nflag += st;
+    }
+    free(A); free(L); free(h); free(y); free(x);
+  }
+  return nflag;
+}
+
+/* Normal-Wishart posterior of (mu, Lambda) given the n rows of X (n x D) and the prior
+ * (mu0, beta0, W0^{-1}, nu0), with xbar = mean of the rows and S = sum_s (x_s - xbar)
+ * (x_s - xbar)^T:
+ *   beta* = beta0 + n,  nu* = nu0 + n,  mu0* = (beta0 mu0 + n xbar) / (beta0 + n),
+ *   W*^{-1} = W0^{-1} + S + beta0 n / (beta0 + n) (mu0 - xbar)(mu0 - xbar)^T.
+ * Outputs mu_s[D], Winv_s[D x D], *beta_s, *nu_s. */
+void orc_nw_posterior(int64_t n, int32_t D, const double *X, const double *mu0, double beta0,
+                      const double *W0inv, double nu0, double *mu_s, double *Winv_s,
+                      double *beta_s, double *nu_s) {
+  double *xbar = (double *)malloc(sizeof(double) * (D > 0 ? D : 1));
+  for (int32_t a = 0; a < D; ++a) {
+    double t = 0.0;
+    for (int64_t s = 0; s < n; ++s) t += X[s * D + a];
+    xbar[a] = n > 0 ? t / (double)n : 0.0;
+  }
+  const double nn = (double)n;
+  const double shrink = (beta0 + nn) > 0.0 ? beta0 * nn / (beta0 + nn) : 0.0;
+  for (int32_t a = 0; a < D; ++a) {
+    for (int32_t e = 0; e < D; ++e) {
+      double sc = 0.0;
+      for (int64_t s = 0; s < n; ++s) sc += (X[s * D + a] - xbar[a]) * (X[s * D + e] - xbar[e]);
+      Winv_s[a * D + e] = W0inv[a * D + e] + sc + shrink * (mu0[a] - xbar[a]) * (mu0[e] - xbar[e]);
+    }
+    mu_s[a] = (beta0 * mu0[a] + nn * xbar[a]) / (beta0 + nn);
+  }
+  *beta_s = beta0 + nn;
+  *nu_s = nu0 + nn;
+  free(xbar);
+}
+
+/* Draw (mu, Lambda) from NW(mu_s, beta_s, W_s, nu_s) given W_s^{-1} (Winv_s) and the
+ * variates: chi2[i] ~ chi-square with nu_s - i degrees of freedom (i = 0..D-1),
+ * offd[k] ~ N(0,1) for the strict lower triangle in row order (k = i (i - 1) / 2 + j, j < i),
+ * zmu[i] ~ N(0,1). Bartlett: W_s = F F^T (lower Cholesky), B lower triangular with
+ * B_ii = sqrt(chi2[i]) and B_ij = offd, Lambda = (F B)(F B)^T; then with
+ * beta_s Lambda = R R^T (lower Cholesky), mu = mu_s + R^{-T} zmu. Returns 0, or 1 if a
+ * factorisation fails. */
+int orc_nw_sample(int32_t D, const double *mu_s, double beta_s, const double *Winv_s,
+                  const double *chi2, const double *offd, const double *zmu, double *mu_out,
+                  double *Lambda_out) {
+  const size_t DD = (size_t)D * D;
+  double *R = (double *)malloc(sizeof(double) * DD);
+  double *W = (double *)malloc(sizeof(double) * DD);
+  double *Fm = (double *)malloc(sizeof(double) * DD);
+  double *FB = (double *)malloc(sizeof(double) * DD);
+  double *col = (double *)malloc(sizeof(double) * D);
+  double *tmp = (double *)malloc(sizeof(double) * D);
+  int st = 0;
+  /* W_s = (W_s^{-1})^{-1}, column by column through the Cholesky factor of W_s^{-1} */
+  if (chol_lower(D, Winv_s, R) != 0) st = 1;
+  for (int32_t e = 0; e < D && st == 0; ++e) {
+    for (int32_t a = 0; a < D; ++a) col[a] = a == e ? 1.0 : 0.0;
+    solve_lower(D, R, col, tmp);
+    solve_lower_t(D, R, tmp, col);
+    for (int32_t a = 0; a < D; ++a) W[a * D + e] = col[a];
+  }
+  if (st == 0 && chol_lower(D, W, Fm) != 0) st = 1;
+  if (st == 0) {
+    /* F B, with B lower triangular */
+    for (int32_t a = 0; a < D; ++a) {
+      for (int32_t e = 0; e < D; ++e) {
+        double t = 0.0;
+        for (int32_t m = e; m <= a; ++m) {
+          const double b = m == e ? sqrt(chi2[e]) : offd[(int64_t)m * (m - 1) / 2 + e];
+          t += Fm[a * D + m] * b;
+        }
+        FB[a * D + e] = t;
+      }
+    }
+    for (int32_t a = 0; a < D; ++a) {
+      for (int32_t e = 0; e < D; ++e) {
+        double t = 0.0;
+        for (int32_t m = 0; m < D; ++m) t += FB[a * D + m] * FB[e * D + m];
+        Lambda_out[a * D + e] = t;
+      }
+    }
+    for (size_t q = 0; q < DD; ++q) W[q] = beta_s * Lambda_out[q];
+    if (chol_lower(D, W, R) != 0) st = 1;
+  }
+  if (st == 0) {
+    solve_lower_t(D, R, zmu, tmp);
+    for (int32_t a = 0; a < D; ++a) mu_out[a] = mu_s[a] + tmp[a];
+  }
+  free(R); free(W); free(Fm); free(FB); free(col); free(tmp);
+  return st;
 }

@@ -11,6 +11,7 @@ import oracle
 from tests import test_oracle_pins as pins
 from tests import test_oracle_weighted_pins as wpins
 from tests import test_oracle_predict_pins as qpins
+from tests import test_oracle_bayes_pins as bpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
 
@@ -39,12 +40,38 @@ MUTANTS = [
      "const double *u = U + (int64_t)items[p] * D;"),
     ("predict_last_feature_dropped", "for (int32_t a = 0; a < D; ++a) dot += u[a] * v[a];",
      "for (int32_t a = 0; a + 1 < D; ++a) dot += u[a] * v[a];"),
+    ("gibbs_prior_mean_dropped", "h[a] = alpha * h[a] + lm;", "h[a] = alpha * h[a];"),
+    ("gibbs_gram_without_alpha",
+     "for (int32_t e = 0; e < D; ++e) A[a * D + e] = alpha * A[a * D + e] + Lambda[a * D + e];",
+     "for (int32_t e = 0; e < D; ++e) A[a * D + e] = A[a * D + e] + Lambda[a * D + e];"),
+    ("gibbs_noise_halved", "for (int32_t a = 0; a < D; ++a) y[a] += z[s * D + a];",
+     "for (int32_t a = 0; a < D; ++a) y[a] += 0.5 * z[s * D + a];"),
+    ("gibbs_noise_lower_solve", "solve_lower_t(D, L, y, x);\n        for (int32_t a = 0; a < D; ++a) {\n          if (!isfinite",
+     "solve_lower_t(D, L, y, x);\n        solve_lower(D, L, y, x);\n        for (int32_t a = 0; a < D; ++a) {\n          if (!isfinite"),
+    ("nw_shrinkage_dropped",
+     "+ sc + shrink * (mu0[a] - xbar[a]) * (mu0[e] - xbar[e]);", "+ sc;"),
+    ("nw_mean_unshrunk", "mu_s[a] = (beta0 * mu0[a] + nn * xbar[a]) / (beta0 + nn);",
+     "mu_s[a] = xbar[a];"),
+    ("nw_wishart_transposed_product", "for (int32_t m = 0; m < D; ++m) t += FB[a * D + m] * FB[e * D + m];",
+     "for (int32_t m = 0; m < D; ++m) t += FB[m * D + a] * FB[m * D + e];"),
+    ("nw_bartlett_diagonal_not_rooted", "const double b = m == e ? sqrt(chi2[e]) :",
+     "const double b = m == e ? chi2[e] :"),
+    ("nw_mean_noise_wrong_solve", "solve_lower_t(D, R, zmu, tmp);", "solve_lower(D, R, zmu, tmp);"),
     ("pair_error_sign", "const double e = r[p] - pred[p];", "const double e = r[p] + pred[p];"),
     ("pair_sse_first_dropped", "for (int64_t p = 0; p < n; ++p) {\n    const double e",
      "for (int64_t p = 1; p < n; ++p) {\n    const double e"),
 ]
 
 PIN_TESTS = [
+    lambda: bpins.test_b1_zero_noise_isotropic_prior_is_ridge(3),
+    bpins.test_b2_zero_noise_is_the_posterior_mode,
+    bpins.test_b3_noise_has_the_conditional_covariance,
+    bpins.test_b4_row_without_ratings_is_a_prior_draw,
+    bpins.test_b6_conjugate_update_batch_equals_sequential,
+    bpins.test_b7_flat_prior_gives_the_sample_scatter,
+    bpins.test_b8_unit_variates_give_the_scale_matrix,
+    bpins.test_b9_mean_draw_has_covariance_of_beta_lambda_inverse,
+    bpins.test_b10_wishart_moments,
     qpins.test_q1_golden_predictions,
     qpins.test_q2_dense_pairs_are_the_matrix_product,
     qpins.test_q3_stored_positions_give_the_training_sse,
