@@ -219,6 +219,64 @@ als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
  */
 als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
 
+/*
+ * Bayesian factorisation (BPTF, paper Sec. 2.2: the least-squares step plus sampling from
+ * the hyperpriors of U and V), as the published BPMF / BPTF Gibbs sampler: ratings are
+ * Gaussian with precision alpha around u . v; each row of a side has the prior
+ * N(mu, Lambda^{-1}); (mu, Lambda) has the Normal-Wishart hyperprior NW(mu0, beta0, W0, nu0).
+ * One Gibbs step for a side: als_sample_hyper draws (mu, Lambda) given the side's rows,
+ * then als_gibbs_half_sweep draws every row given the other side. Every random variate
+ * is an input (device memory), so a step is a deterministic function of them.
+ *
+ * als_set_nw_prior: the hyperprior of one side (host arrays, copied): mu0[D], beta0 >= 0,
+ * W0_inv[D x D] row-major, finite and symmetric (the inverse of the Wishart scale W0),
+ * nu0 > D - 1. ALS_ERR_INVALID_ARG otherwise. Synchronises the stream.
+ */
+als_status als_set_nw_prior(als_ctx *ctx, als_side side, const double *mu0, double beta0,
+                            const double *W0_inv, double nu0);
+
+/*
+ * Draw the side's hyperparameters from their Normal-Wishart posterior given its n rows
+ * X (device fp32 [n x D], 16-byte aligned; n = n_users or n_items):
+ *   beta* = beta0 + n, nu* = nu0 + n, mu0* = (beta0 mu0 + n xbar) / beta*,
+ *   W*^{-1} = W0^{-1} + sum_s (x_s - xbar)(x_s - xbar)^T + beta0 n / beta* (mu0 - xbar)(mu0 - xbar)^T;
+ * Bartlett's construction: W* = F F^T (lower Cholesky), B lower triangular with
+ * B_ii = sqrt(chi2[i]) and B_ij = offdiag[i (i - 1) / 2 + j] (j < i), Lambda = (F B)(F B)^T;
+ * then mu = mu0* + R^{-T} z_mu with beta* Lambda = R R^T.
+ *   chi2      device fp64[D], chi2[i] drawn from the chi-square law with nu* - i degrees
+ *             of freedom (i = 0 .. D-1);
+ *   offdiag   device fp64[D (D - 1) / 2] standard normals (may be NULL when D = 1);
+ *   z_mu      device fp64[D] standard normals;
+ *   mu_out, Lambda_out  device fp64[D], [D x D], caller-owned.
+ * Everything runs in fp64 on the device, enqueued without synchronisation. status_out
+ * (host, nullable): if non-NULL the call synchronises and stores 0, or 1 when a
+ * factorisation failed (then the return is ALS_ERR_NOT_SPD). ALS_ERR_INVALID_ARG when no
+ * prior was set for the side.
+ */
+als_status als_sample_hyper(als_ctx *ctx, als_side side, const float *X, const double *chi2,
+                            const double *offdiag, const double *z_mu, double *mu_out,
+                            double *Lambda_out, int32_t *status_out);
+
+/*
+ * Gibbs half-sweep: every row s of the side drawn from its Gaussian conditional
+ *   Lambda* = Lambda + alpha sum_j f_j f_j^T,  mu* = Lambda*^{-1} (alpha sum_j r_sj f_j + Lambda mu),
+ *   x_s = mu* + L*^{-T} z_s  (Lambda* = L* L*^T),
+ * with the same gather, Gram and factorisation kernels as als_half_sweep (the system is
+ * solved as (G + Lambda / alpha) with z_s / sqrt(alpha) added before the back
+ * substitution). Rows without ratings are drawn from the prior, x_s = mu + L^{-T} z_s
+ * (Lambda = L L^T).
+ *   alpha          rating precision, finite and > 0.
+ *   Lambda, mu     device fp64 [D x D] (symmetric positive definite), [D] (e.g. the
+ *                  outputs of als_sample_hyper).
+ *   z              device fp32 [n_rows x D] standard normals, one row per row of the side.
+ *   fixed_factors, out_factors, rmse_out: as for als_half_sweep (flagged rows, whose
+ *                  Lambda* is not numerically SPD, keep their previous value).
+ * The context must have no rating weights attached (ALS_ERR_INVALID_ARG).
+ */
+als_status als_gibbs_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors,
+                                float alpha, const double *Lambda, const double *mu,
+                                const float *z, float *out_factors, double *rmse_out);
+
 void als_destroy(als_ctx *ctx);
 
 const char *als_status_str(als_status s);

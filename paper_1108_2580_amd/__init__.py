@@ -25,7 +25,8 @@ EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_
            "als_get_csc",
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_weights",
            "als_set_phase_timing", "als_get_phase_cycles", "als_predict", "als_set_holdout",
-           "als_holdout_rmse", "als_destroy", "als_status_str", "als_last_error")
+           "als_holdout_rmse", "als_set_nw_prior", "als_sample_hyper", "als_gibbs_half_sweep",
+           "als_destroy", "als_status_str", "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
 
@@ -81,6 +82,14 @@ def _load_library(path=LIB_PATH):
     lib.als_set_holdout.restype = st
     lib.als_holdout_rmse.argtypes = [P, P, P, ctypes.POINTER(ctypes.c_double)]
     lib.als_holdout_rmse.restype = st
+    f64 = ctypes.c_double
+    lib.als_set_nw_prior.argtypes = [P, st, P, f64, P, f64]
+    lib.als_set_nw_prior.restype = st
+    lib.als_sample_hyper.argtypes = [P, st, P, P, P, P, P, P, ctypes.POINTER(ctypes.c_int32)]
+    lib.als_sample_hyper.restype = st
+    lib.als_gibbs_half_sweep.argtypes = [P, st, P, f32, P, P, P, P,
+                                         ctypes.POINTER(ctypes.c_double)]
+    lib.als_gibbs_half_sweep.restype = st
     lib.als_destroy.argtypes = [P]
     lib.als_destroy.restype = None
     lib.als_status_str.argtypes = [st]
@@ -261,6 +270,69 @@ class ALS:
         r = ctypes.c_double(0.0)
         self._check(lib.als_holdout_rmse(self._h, up, vp, ctypes.byref(r)))
         return r.value
+
+    # ---- Bayesian (BPMF / BPTF) Gibbs step ----------------------------------------------
+
+    def set_nw_prior(self, side, mu0, beta0, W0_inv, nu0):
+        """Normal-Wishart hyperprior of one side (host arrays)."""
+        mu0 = np.ascontiguousarray(mu0, dtype=np.float64)
+        W = np.ascontiguousarray(W0_inv, dtype=np.float64)
+        if mu0.shape != (self.D,) or W.shape != (self.D, self.D):
+            raise ValueError("mu0 must have D entries and W0_inv be D x D")
+        self._check(lib.als_set_nw_prior(self._h, _SIDES[side], _np_ptr(mu0), float(beta0),
+                                         _np_ptr(W), float(nu0)))
+
+    def sample_hyper(self, side, X, chi2, offdiag, z_mu, mu_out=None, Lambda_out=None,
+                     check=False):
+        """Draw (mu, Lambda) of ``side`` given its rows X; variates are fp64 CUDA tensors.
+        Returns (mu, Lambda) as fp64 CUDA tensors."""
+        import torch
+
+        sd = _SIDES[side]
+        n = self.M if sd == ALS_ROWS_USERS else self.N
+        xp = _dev_ptr(X, self.D, n, "X")
+        D = self.D
+        for t, name, size in ((chi2, "chi2", D), (offdiag, "offdiag", D * (D - 1) // 2),
+                              (z_mu, "z_mu", D)):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or \
+                    t.dtype != torch.float64 or not t.is_contiguous() or t.numel() != size:
+                raise TypeError(f"{name} must be a contiguous fp64 CUDA tensor of {size} values")
+        if mu_out is None:
+            mu_out = torch.empty(D, dtype=torch.float64, device=X.device)
+        if Lambda_out is None:
+            Lambda_out = torch.empty((D, D), dtype=torch.float64, device=X.device)
+        status = ctypes.c_int32(0)
+        self._check(lib.als_sample_hyper(
+            self._h, sd, xp, ctypes.c_void_p(chi2.data_ptr()),
+            ctypes.c_void_p(offdiag.data_ptr()) if offdiag.numel() else None,
+            ctypes.c_void_p(z_mu.data_ptr()), ctypes.c_void_p(mu_out.data_ptr()),
+            ctypes.c_void_p(Lambda_out.data_ptr()), ctypes.byref(status) if check else None))
+        return mu_out, Lambda_out
+
+    def gibbs_half_sweep(self, side, fixed, alpha, Lambda, mu, z, out, rmse=False,
+                         allow_flagged=False):
+        """Draw every row of ``side`` into ``out`` from its conditional given ``fixed``."""
+        import torch
+
+        sd = _SIDES[side]
+        users = sd == ALS_ROWS_USERS
+        n_rows, n_fixed = (self.M, self.N) if users else (self.N, self.M)
+        fp = _dev_ptr(fixed, self.D, n_fixed, "fixed")
+        op = _dev_ptr(out, self.D, n_rows, "out")
+        zp = _dev_ptr(z, self.D, n_rows, "z")
+        for t, name, shape in ((Lambda, "Lambda", (self.D, self.D)), (mu, "mu", (self.D,))):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or \
+                    t.dtype != torch.float64 or not t.is_contiguous() or tuple(t.shape) != shape:
+                raise TypeError(f"{name} must be a contiguous fp64 CUDA tensor of shape {shape}")
+        r = ctypes.c_double(0.0)
+        s = lib.als_gibbs_half_sweep(self._h, sd, fp, float(alpha),
+                                     ctypes.c_void_p(Lambda.data_ptr()),
+                                     ctypes.c_void_p(mu.data_ptr()), zp, op,
+                                     ctypes.byref(r) if rmse else None)
+        if s == ALS_ERR_NOT_SPD and allow_flagged:
+            return r.value
+        self._check(s)
+        return r.value if rmse else None
 
     def close(self):
         if getattr(self, "_h", None):

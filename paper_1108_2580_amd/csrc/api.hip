@@ -53,6 +53,8 @@ struct SidePlan {
   std::vector<RowTask> rows;     // every row with ratings, batch-major, descending degree
   WorkItem *d_gitems = nullptr;
   RowTask *d_rows = nullptr;
+  std::vector<int32_t> zero_rows;  // rows without ratings (drawn from the prior when Bayesian)
+  int32_t *d_zero_rows = nullptr;
 };
 
 constexpr int kPhases = 5;  // stage, chunks, rows, residual, reduce
@@ -113,6 +115,19 @@ struct als_ctx {
   double *d_hold_blocks = nullptr; // per-block squared errors
   double *d_hold_partials = nullptr;
   double *d_hold_sse = nullptr;
+  // Bayesian Gibbs step (allocated on first use)
+  float *d_prior_init = nullptr;   // prior image of the row kernels
+  float *d_prior_K = nullptr;      // L^{-T} of the prior precision, for rows without ratings
+  float *d_prior_mu32 = nullptr;
+  int32_t *d_prior_ok = nullptr;
+  double *d_bayes_scratch = nullptr;
+  double *d_hyper_partials = nullptr;
+  int32_t *d_hyper_status = nullptr;
+  int32_t *h_hyper_status = nullptr;  // pinned
+  double *d_nw_mu0[2] = {nullptr, nullptr};    // Normal-Wishart hyperprior per side
+  double *d_nw_W0inv[2] = {nullptr, nullptr};
+  double nw_beta0[2] = {0, 0}, nw_nu0[2] = {0, 0};
+  bool nw_set[2] = {false, false};
 };
 
 namespace {
@@ -183,6 +198,7 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   for (int64_t s = 0; s < n_rows; ++s) {
     const int64_t d = ptr[s + 1] - ptr[s];
     if (d > 0) order.push_back((int32_t)s);
+    else P.zero_rows.push_back((int32_t)s);
     P.max_deg = std::max(P.max_deg, d);
   }
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
@@ -269,6 +285,10 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   for (const Batch &b : P.batches) P.max_slots = std::max(P.max_slots, b.n_slots);
   HIP_OR_FAIL(ctx, dalloc(&P.d_gitems, (int64_t)P.gitems.size()));
   HIP_OR_FAIL(ctx, dalloc(&P.d_rows, (int64_t)P.rows.size()));
+  HIP_OR_FAIL(ctx, dalloc(&P.d_zero_rows, (int64_t)P.zero_rows.size()));
+  if (!P.zero_rows.empty())
+    HIP_OR_FAIL(ctx, hipMemcpy(P.d_zero_rows, P.zero_rows.data(),
+                               sizeof(int32_t) * P.zero_rows.size(), hipMemcpyHostToDevice));
   if (!P.gitems.empty())
     HIP_OR_FAIL(ctx, hipMemcpy(P.d_gitems, P.gitems.data(), sizeof(WorkItem) * P.gitems.size(),
                                hipMemcpyHostToDevice));
@@ -276,11 +296,6 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
     HIP_OR_FAIL(ctx, hipMemcpy(P.d_rows, P.rows.data(), sizeof(RowTask) * P.rows.size(),
                                hipMemcpyHostToDevice));
   return ALS_OK;
-}
-
-bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
-  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
-  return x < y + nb && y < x + na;
 }
 
 // pairs of one predict call: the launch has pair_blocks(n) < 2^31 blocks
@@ -310,6 +325,7 @@ void free_ctx(als_ctx *c) {
   for (auto &P : c->plan) {
     dfree(P.d_gitems);
     dfree(P.d_rows);
+    dfree(P.d_zero_rows);
   }
   dfree(c->d_ws);
   dfree(c->d_fpad);
@@ -325,6 +341,18 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_cyc);
   dfree(c->d_cyc_sum);
   free_holdout(c);
+  dfree(c->d_prior_init);
+  dfree(c->d_prior_K);
+  dfree(c->d_prior_mu32);
+  dfree(c->d_prior_ok);
+  dfree(c->d_bayes_scratch);
+  dfree(c->d_hyper_partials);
+  dfree(c->d_hyper_status);
+  if (c->h_hyper_status) (void)hipHostFree(c->h_hyper_status);
+  for (int sd = 0; sd < 2; ++sd) {
+    dfree(c->d_nw_mu0[sd]);
+    dfree(c->d_nw_W0inv[sd]);
+  }
   if (c->h_cyc_sum) (void)hipHostFree(c->h_cyc_sum);
   for (auto &pe : c->prof_pending) {
     (void)hipEventDestroy(pe.a);
@@ -579,10 +607,14 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   return ALS_OK;
 }
 
-als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
-                          float *out_factors, double *rmse_out) {
-  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
-  ctx->err.clear();
+}  // extern "C"
+
+namespace {
+
+// The half-sweep of both methods: the ALS update (pr.init == nullptr, lambda used) or the
+// Gibbs draw (pr: the prior image, the variates and their scale; lambda unused).
+als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
+                           float *out_factors, double *rmse_out, const als::RowPrior &pr) {
   if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
     return fail(ctx, ALS_ERR_INVALID_ARG, "side %d is not ALS_ROWS_USERS or ALS_ROWS_ITEMS",
                 (int)side);
@@ -621,7 +653,7 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
         PhaseTimer t(ctx, 2);
         HIP_OR_FAIL(ctx, als::launch_solve_lane(ctx->D, P.d_rows + b.row_off, b.n_rows, b.n_split,
                                                 b.row_off, ctx->d_ws, ctx->d_ne, lambda,
-                                                out_factors, ctx->d_flag, ctx->stream));
+                                                out_factors, ctx->d_flag, pr, ctx->stream));
       }
     } else {
       if (b.n_gchunks > 0) {
@@ -637,9 +669,15 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
         HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val, wts,
                                           ctx->d_fpad, n_fixed, ctx->d_ws, ctx->D, lambda,
                                           out_factors, ctx->d_sse_items, ctx->d_flag, cg, cs,
-                                          ctx->stream));
+                                          pr, ctx->stream));
       }
     }
+  }
+  if (pr.init && !P.zero_rows.empty()) {
+    PhaseTimer t(ctx, 2);
+    HIP_OR_FAIL(ctx, als::launch_prior_rows(P.d_zero_rows, (int64_t)P.zero_rows.size(), ctx->D,
+                                            ctx->d_prior_K, ctx->d_prior_mu32, ctx->d_prior_ok,
+                                            pr.z, out_factors, ctx->d_flag, ctx->stream));
   }
   {
     PhaseTimer t(ctx, 4);
@@ -673,6 +711,141 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
     if (*ctx->h_flag > 0)
       return fail(ctx, ALS_ERR_NOT_SPD, "%d rows were flagged and left unchanged",
                   (int)*ctx->h_flag);
+  }
+  return ALS_OK;
+}
+
+template <typename T>
+als_status ensure(als_ctx *ctx, T **p, size_t n, const char *what) {
+  if (*p) return ALS_OK;
+  const hipError_t e = dalloc(p, (int64_t)n);
+  if (e != hipSuccess)
+    return fail(ctx, e == hipErrorOutOfMemory ? ALS_ERR_OUT_OF_MEMORY : ALS_ERR_HIP, "%s: %s",
+                what, hipGetErrorString(e));
+  return ALS_OK;
+}
+
+als_status ensure_bayes(als_ctx *ctx) {
+  const int D = ctx->D;
+  als_status st = ensure(ctx, &ctx->d_prior_init, als::prior_init_floats(D, ctx->DP), "prior image");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_prior_K, (size_t)D * D, "prior factor");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_prior_mu32, (size_t)D, "prior mean");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_prior_ok, 1, "prior status");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_bayes_scratch, als::bayes_scratch_doubles(D), "scratch");
+  if (st == ALS_OK)
+    st = ensure(ctx, &ctx->d_hyper_partials,
+                (size_t)als::hyper_blocks(std::max(ctx->M, ctx->N)) * als::hyper_entries(D),
+                "moment partials");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_hyper_status, 1, "draw status");
+  if (st == ALS_OK && !ctx->h_hyper_status) {
+    const hipError_t e = hipHostMalloc((void **)&ctx->h_hyper_status, sizeof(int32_t),
+                                       hipHostMallocDefault);
+    if (e != hipSuccess) return fail(ctx, ALS_ERR_OUT_OF_MEMORY, "pinned status: %s",
+                                     hipGetErrorString(e));
+  }
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
+                          float *out_factors, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  return half_sweep_impl(ctx, side, fixed_factors, lambda, out_factors, rmse_out, als::RowPrior{});
+}
+
+als_status als_gibbs_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors,
+                                float alpha, const double *Lambda, const double *mu,
+                                const float *z, float *out_factors, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!(alpha > 0.f) || !std::isfinite(alpha))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "alpha must be finite and > 0");
+  if (!Lambda || !mu || !z) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL prior or variates");
+  if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "side %d is not ALS_ROWS_USERS or ALS_ROWS_ITEMS",
+                (int)side);
+  if ((side == ALS_ROWS_USERS ? ctx->d_w : ctx->d_w_t) != nullptr)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "the Gibbs half-sweep takes no rating weights; detach them");
+  const int64_t n_rows = side == ALS_ROWS_USERS ? ctx->M : ctx->N;
+  if (overlap(z, sizeof(float) * n_rows * ctx->D, out_factors, sizeof(float) * n_rows * ctx->D))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "z overlaps out_factors");
+  DeviceGuard g(ctx->device);
+  als_status st = ensure_bayes(ctx);
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, als::launch_prior_prepare(Lambda, mu, ctx->D, ctx->DP, (double)alpha,
+                                             ctx->d_prior_init, ctx->d_prior_K, ctx->d_prior_mu32,
+                                             ctx->d_bayes_scratch, ctx->d_prior_ok, ctx->stream));
+  als::RowPrior pr;
+  pr.init = ctx->d_prior_init;
+  pr.z = z;
+  pr.zscale = (float)(1.0 / std::sqrt((double)alpha));
+  return half_sweep_impl(ctx, side, fixed_factors, 0.f, out_factors, rmse_out, pr);
+}
+
+als_status als_set_nw_prior(als_ctx *ctx, als_side side, const double *mu0, double beta0,
+                            const double *W0_inv, double nu0) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "side must be ALS_ROWS_USERS or ALS_ROWS_ITEMS");
+  const int D = ctx->D;
+  if (!mu0 || !W0_inv) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (!(beta0 >= 0.0) || !std::isfinite(beta0) || !std::isfinite(nu0) || !(nu0 > D - 1))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "need beta0 >= 0 and nu0 > D - 1");
+  for (int a = 0; a < D; ++a) {
+    if (!std::isfinite(mu0[a])) return fail(ctx, ALS_ERR_INVALID_ARG, "mu0 is not finite");
+    for (int e = 0; e < D; ++e) {
+      if (!std::isfinite(W0_inv[a * D + e]) || W0_inv[a * D + e] != W0_inv[e * D + a])
+        return fail(ctx, ALS_ERR_INVALID_ARG, "W0_inv must be finite and symmetric");
+    }
+  }
+  DeviceGuard g(ctx->device);
+  als_status st = ensure(ctx, &ctx->d_nw_mu0[side], (size_t)D, "prior mean");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_nw_W0inv[side], (size_t)D * D, "prior scale");
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_mu0[side], mu0, sizeof(double) * D, hipMemcpyHostToDevice));
+  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_W0inv[side], W0_inv, sizeof(double) * D * D,
+                             hipMemcpyHostToDevice));
+  ctx->nw_beta0[side] = beta0;
+  ctx->nw_nu0[side] = nu0;
+  ctx->nw_set[side] = true;
+  return ALS_OK;
+}
+
+als_status als_sample_hyper(als_ctx *ctx, als_side side, const float *X, const double *chi2,
+                            const double *offdiag, const double *z_mu, double *mu_out,
+                            double *Lambda_out, int32_t *status_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "side must be ALS_ROWS_USERS or ALS_ROWS_ITEMS");
+  if (!ctx->nw_set[side]) return fail(ctx, ALS_ERR_INVALID_ARG, "no Normal-Wishart prior set for this side");
+  if (!X || !chi2 || (!offdiag && ctx->D > 1) || !z_mu || !mu_out || !Lambda_out)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if ((uintptr_t)X & 15) return fail(ctx, ALS_ERR_INVALID_ARG, "X must be 16-byte aligned");
+  const int64_t n = side == ALS_ROWS_USERS ? ctx->M : ctx->N;
+  DeviceGuard g(ctx->device);
+  als_status st = ensure_bayes(ctx);
+  if (st != ALS_OK) return st;
+  const int nblk = als::hyper_blocks(n);
+  HIP_OR_FAIL(ctx, als::launch_hyper_moments(X, n, ctx->D, ctx->d_hyper_partials, ctx->stream));
+  HIP_OR_FAIL(ctx, als::launch_hyper_sample(ctx->d_hyper_partials, nblk, n, ctx->D,
+                                            ctx->d_nw_mu0[side], ctx->nw_beta0[side],
+                                            ctx->d_nw_W0inv[side], ctx->nw_nu0[side], chi2,
+                                            offdiag, z_mu, ctx->d_bayes_scratch, mu_out,
+                                            Lambda_out, ctx->d_hyper_status, ctx->stream));
+  if (status_out) {
+    HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_hyper_status, ctx->d_hyper_status, sizeof(int32_t),
+                                    hipMemcpyDeviceToHost, ctx->stream));
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    *status_out = *ctx->h_hyper_status;
+    if (*status_out != 0)
+      return fail(ctx, ALS_ERR_NOT_SPD, "a factorisation of the Normal-Wishart draw failed");
   }
   return ALS_OK;
 }
@@ -847,10 +1020,10 @@ als_status als_predict(als_ctx *ctx, const float *U, const float *V, int64_t n_p
   if (((uintptr_t)U & 15) || ((uintptr_t)V & 15))
     return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
   const size_t pb = sizeof(float) * (size_t)n_pairs;
-  if (overlaps(pred, pb, U, sizeof(float) * ctx->M * ctx->D) ||
-      overlaps(pred, pb, V, sizeof(float) * ctx->N * ctx->D) ||
-      overlaps(pred, pb, users, sizeof(int32_t) * n_pairs) ||
-      overlaps(pred, pb, items, sizeof(int32_t) * n_pairs))
+  if (overlap(pred, pb, U, sizeof(float) * ctx->M * ctx->D) ||
+      overlap(pred, pb, V, sizeof(float) * ctx->N * ctx->D) ||
+      overlap(pred, pb, users, sizeof(int32_t) * n_pairs) ||
+      overlap(pred, pb, items, sizeof(int32_t) * n_pairs))
     return fail(ctx, ALS_ERR_INVALID_ARG, "pred overlaps an input");
   DeviceGuard g(ctx->device);
   HIP_OR_FAIL(ctx, als::launch_predict(U, V, ctx->M, ctx->N, ctx->D, n_pairs, users, items,

@@ -41,6 +41,18 @@ constexpr int num_tiles(int dp) { return (dp / 16) * (dp / 16 + 1) / 2; }
 constexpr size_t slot_floats(int dp) { return (size_t)num_tiles(dp) * 256 + (size_t)dp; }
 inline size_t slot_floats_rt(int dp) { int t = dp / 16; return (size_t)(t * (t + 1) / 2) * 256 + dp; }
 
+// Bayesian row prior of one Gibbs half-sweep (BPMF / BPTF): each row's system starts
+// from Lambda / alpha (identity on the padding) and Lambda mu / alpha instead of
+// lambda n_s I and 0, and zscale * z_s is added to the forward-substitution result, so
+// that the solve returns the conditional draw mu* + L*^{-T} z_s. init == nullptr: ALS.
+struct RowPrior {
+  const float *init = nullptr;  // the row kernel: one workspace slot (tiles in MFMA register
+                                // order, then the right-hand side); the one-lane solve: one
+                                // packed record (upper triangle, then the right-hand side)
+  const float *z = nullptr;     // standard normal variates, [rows of the side x D]
+  float zscale = 0.f;           // 1 / sqrt(alpha)
+};
+
 // ---- launchers (each returns the launch's hipError_t) ----------------------------------
 
 // Column-major copy of a CSR matrix, built on the device (layout.hip).
@@ -78,10 +90,11 @@ hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const in
 // row's wavefront clock cycles spent before the factorisation (gather, Gram and
 // residuals, or the sum of chunk partials) and from there on (factorisation, solves,
 // write); a measurement aid that leaves the results unchanged.
+// pr: the Bayesian prior (Gibbs half-sweep) or a default RowPrior (ALS; lam is used).
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
                        const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
-                       double *cyc_gram, double *cyc_solve, hipStream_t s);
+                       double *cyc_gram, double *cyc_solve, const RowPrior &pr, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
 // fixed side Fp (row stride DP) (residual.hip).
@@ -107,7 +120,7 @@ hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t
 // chunk records (in ws) are summed into their records first.
 hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t n_split,
                              int64_t base, const float *ws, float *ne, float lam, float *X,
-                             int32_t *flag, hipStream_t s);
+                             int32_t *flag, const RowPrior &pr, hipStream_t s);
 
 // Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].
 int64_t reduce_partials(int64_t n);
@@ -115,6 +128,46 @@ hipError_t launch_reduce(const double *v, int64_t n, double *partials, double *o
                          hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+
+// Packed upper triangle of an LD x LD matrix, row by row (one-lane solve records).
+template <int LD>
+__host__ __device__ constexpr int tri(int a, int b) {  // a <= b
+  return a * LD - a * (a - 1) / 2 + (b - a);
+}
+
+// ---- Bayesian Gibbs step (bayes.hip) ----------------------------------------------------
+
+// fp64 scratch (doubles) that the prior preparation and the hyperparameter draw need.
+inline size_t bayes_scratch_doubles(int D) {
+  return (size_t)5 * D * D + (size_t)(D + D * (D + 1) / 2) + 3 * (size_t)D + 8;
+}
+// Floats of the prior image: a workspace slot (D > 20) or a packed record (D <= 20).
+inline size_t prior_init_floats(int D, int DP) {
+  return lane_width(D) ? (size_t)ne_floats(lane_width(D)) : slot_floats_rt(DP);
+}
+
+// Prior image of a Gibbs half-sweep from the device hyperparameters Lambda (D x D) and mu
+// (fp64): init (prior_init_floats), and for rows without ratings K = L^{-T} (Lambda = L L^T,
+// fp32 D x D) and mu in fp32; *ok = 1, or 0 when Lambda is not numerically SPD.
+hipError_t launch_prior_prepare(const double *Lam, const double *mu, int D, int DP, double alpha,
+                                float *init, float *K, float *mu32, double *scratch, int32_t *ok,
+                                hipStream_t s);
+// Rows without ratings drawn from the prior: X[row] = mu + K z_row (flagged when !*ok).
+hipError_t launch_prior_rows(const int32_t *rows, int64_t n, int D, const float *K,
+                             const float *mu32, const int32_t *ok, const float *z, float *X,
+                             int32_t *flag, hipStream_t s);
+// Per-block fp64 sums of x and of the upper triangle of x x^T over the n rows of X
+// (n x D): hyper_blocks(n) blocks, hyper_entries(D) doubles each.
+int hyper_blocks(int64_t n);
+inline int hyper_entries(int D) { return D + D * (D + 1) / 2; }
+hipError_t launch_hyper_moments(const float *X, int64_t n, int D, double *partials, hipStream_t s);
+// Normal-Wishart posterior from the moments and a Bartlett draw of (mu, Lambda) from it,
+// in fp64 on one workgroup; *status = 0, or 1 when a factorisation fails.
+hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int D,
+                               const double *mu0, double beta0, const double *W0inv, double nu0,
+                               const double *chi2, const double *offd, const double *zmu,
+                               double *scratch, double *mu_out, double *Lam_out, int32_t *status,
+                               hipStream_t s);
 
 // Predictions u_{users[p]} . v_{items[p]} of n pairs (predict.hip). pred (nullable)
 // receives them, NaN for a pair with an index outside [0, M) x [0, N). With

@@ -13,17 +13,16 @@
 //                diagonal, factors
 //                A = U^T U in registers, solves U^T y = b and U x = y
 //                (Sec. 2.2; the per-update inversion of Sec. 4.1) and
-//                writes x unless a pivot is not positive and finite.
+//                writes x unless a pivot is not positive and finite. In a Gibbs
+//                half-sweep (BAYES) the record gets the prior image added instead
+//                (Lambda / alpha and Lambda mu / alpha), and y gets z / sqrt(alpha)
+//                before the back substitution, which turns the solve into the
+//                conditional draw mu* + L*^{-T} z.
 // Records hold LD(LD+1)/2 + LD floats (LD = 16 or 20, the width the solve is
 // compiled for; padded features solve to zero), rounded up to a multiple of 4.
 #include "gram.h"
 
 namespace als {
-
-template <int LD>
-__host__ __device__ constexpr int tri(int a, int b) {  // a <= b, row-major upper triangle
-  return a * LD - a * (a - 1) / 2 + (b - a);
-}
 
 // AUG (used for D = 17..20, LD = 20): the ratings ride in padding feature 20 of the
 // gathered rows, so the MFMA Gram delivers b in column 20 (tile column 4 of the last
@@ -114,11 +113,12 @@ __global__ __launch_bounds__(256) void k_sum_records(const RowTask *__restrict__
   }
 }
 
-template <int LD>
+template <int LD, bool BAYES>
 __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ rows, int64_t n_rows,
                                                    int64_t base, const float *__restrict__ ne,
                                                    int D, float lam, float *__restrict__ X,
-                                                   int32_t *__restrict__ flag_count) {
+                                                   int32_t *__restrict__ flag_count,
+                                                   RowPrior pr) {
   constexpr int NTRI = LD * (LD + 1) / 2;
   constexpr int NES = ne_floats(LD);
   const int64_t i = (int64_t)blockIdx.x * 64 + threadIdx.x;
@@ -137,9 +137,17 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
       else if (e < NTRI + LD) b[e - NTRI] = w[j];
     }
   }
-  const float lam_n = (float)((double)lam * (double)rt.deg);
+  if constexpr (BAYES) {
+    // the prior image carries the identity on the padding
 #pragma unroll
-  for (int d = 0; d < LD; ++d) A[tri<LD>(d, d)] = d < D ? A[tri<LD>(d, d)] + lam_n : 1.f;
+    for (int e = 0; e < NTRI; ++e) A[e] += pr.init[e];
+#pragma unroll
+    for (int d = 0; d < LD; ++d) b[d] += pr.init[NTRI + d];
+  } else {
+    const float lam_n = (float)((double)lam * (double)rt.deg);
+#pragma unroll
+    for (int d = 0; d < LD; ++d) A[tri<LD>(d, d)] = d < D ? A[tri<LD>(d, d)] + lam_n : 1.f;
+  }
 
   // A = U^T U in place (upper triangle); the diagonal keeps 1 / u_kk
   bool bad = false;
@@ -164,6 +172,12 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
     b[k] *= A[tri<LD>(k, k)];
 #pragma unroll
     for (int j = k + 1; j < LD; ++j) b[j] = fmaf(-A[tri<LD>(k, j)], b[k], b[j]);
+  }
+  if constexpr (BAYES) {
+    const float *__restrict__ zr = pr.z + (int64_t)rt.row * D;
+#pragma unroll
+    for (int d = 0; d < LD; ++d)
+      if (d < D) b[d] = fmaf(pr.zscale, zr[d], b[d]);
   }
   // U x = y (x overwrites b)
 #pragma unroll
@@ -216,9 +230,21 @@ hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t
   return hipGetLastError();
 }
 
+template <int LD>
+static void launch_solve_lane_t(unsigned blocks, const RowTask *rows, int64_t n_rows, int64_t base,
+                                const float *ne, int D, float lam, float *X, int32_t *flag,
+                                const RowPrior &pr, hipStream_t s) {
+  if (pr.init)
+    hipLaunchKernelGGL((k_solve_lane<LD, true>), dim3(blocks), dim3(64), 0, s, rows, n_rows, base,
+                       ne, D, lam, X, flag, pr);
+  else
+    hipLaunchKernelGGL((k_solve_lane<LD, false>), dim3(blocks), dim3(64), 0, s, rows, n_rows,
+                       base, ne, D, lam, X, flag, pr);
+}
+
 hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t n_split,
                              int64_t base, const float *ws, float *ne, float lam, float *X,
-                             int32_t *flag, hipStream_t s) {
+                             int32_t *flag, const RowPrior &pr, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int ld = lane_width(D);
   if (ld != 16 && ld != 20) return hipErrorInvalidValue;
@@ -234,11 +260,9 @@ hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t
   }
   const unsigned blocks = (unsigned)((n_rows + 63) / 64);
   if (ld == 16)
-    hipLaunchKernelGGL(k_solve_lane<16>, dim3(blocks), dim3(64), 0, s, rows, n_rows, base, ne, D,
-                       lam, X, flag);
+    launch_solve_lane_t<16>(blocks, rows, n_rows, base, ne, D, lam, X, flag, pr, s);
   else
-    hipLaunchKernelGGL(k_solve_lane<20>, dim3(blocks), dim3(64), 0, s, rows, n_rows, base, ne, D,
-                       lam, X, flag);
+    launch_solve_lane_t<20>(blocks, rows, n_rows, base, ne, D, lam, X, flag, pr, s);
   return hipGetLastError();
 }
 

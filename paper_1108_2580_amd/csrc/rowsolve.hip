@@ -129,7 +129,12 @@ constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 //   with one 4-term dot product per tile, and the trailing tiles are updated on MFMA
 //   (K = 4). Without the augmented column the right-hand side is eliminated along:
 //   y_p = M b_p, and b_j -= sum_r A[p0 + r][j] (M^T y_p)_r for the later columns.
-template <int DP, bool AUG, bool WT>
+//
+// BAYES (a Gibbs half-sweep): the accumulators start from the prior image (Lambda /
+// alpha, identity on the padding, and Lambda mu / alpha in the right-hand side) and the
+// forward-substitution result y gets z / sqrt(alpha) before the back substitution, so
+// that the row receives the conditional draw mu* + L*^{-T} z.
+template <int DP, bool AUG, bool WT, bool BAYES>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
     const uint8_t *__restrict__ val, const float *__restrict__ wts,
@@ -137,7 +142,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
     double *__restrict__ sse_out,
     int32_t *__restrict__ flag_count, double *__restrict__ cyc_gram,
-    double *__restrict__ cyc_solve) {
+    double *__restrict__ cyc_solve, RowPrior pr) {
   const uint64_t t_start = __builtin_readcyclecounter();
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
@@ -158,16 +163,22 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   // A starts as lambda n_s I on the first D diagonal entries and I on the padding (only
   // the last tile holds padding); the Gram (or the sum of a split row's chunk partials)
   // is accumulated on top
-  const float lam_n = (float)((double)lam * (double)rt.deg);
   floatx4 acc[NT];
+  if constexpr (BAYES) {
 #pragma unroll
-  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NT; ++t)
+      acc[t] = *reinterpret_cast<const floatx4 *>(pr.init + t * 256 + lane * 4);
+  } else {
+    const float lam_n = (float)((double)lam * (double)rt.deg);
 #pragma unroll
-  for (int I = 0; I < T; ++I) {
+    for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int d = 16 * I + 4 * kq + r;
-      acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? ((I < T - 1 || d < D) ? lam_n : 1.f) : 0.f;
+    for (int I = 0; I < T; ++I) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int d = 16 * I + 4 * kq + r;
+        acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? ((I < T - 1 || d < D) ? lam_n : 1.f) : 0.f;
+      }
     }
   }
   float rhs[T];
@@ -208,6 +219,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
         for (int X = 0; X < T; ++X) rhs[X] += sl[NT * 256 + 16 * X + c];
       }
     }
+  }
+  if constexpr (BAYES && !AUG) {
+    // the prior's right-hand side (with the augmented column it sits in the tiles)
+#pragma unroll
+    for (int X = 0; X < T; ++X) rhs[X] += pr.init[NT * 256 + 16 * X + c];
   }
 
   const uint64_t t_gram = __builtin_readcyclecounter();
@@ -334,6 +350,17 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     }
   }
 
+  if constexpr (BAYES) {
+    // y += z / sqrt(alpha): the panels keep y_p in ud[p][10 .. 13]
+    const float *__restrict__ zr = pr.z + (int64_t)rt.row * D;
+#pragma unroll
+    for (int d0 = 0; d0 < DP; d0 += 64) {
+      const int d = d0 + lane;
+      if (d < D) ud[d >> 2][10 + (d & 3)] += pr.zscale * zr[d];
+    }
+    wave_sync();
+  }
+
   // ---- back substitution U x = y --------------------------------------------------------
   // Panel p: U_gg x_p = y_p - U_p,rest x_rest with U_p,rest = M A_p,rest, where the
   // accumulators still hold the panel rows A_p as they were when the panel was factored
@@ -409,15 +436,15 @@ static constexpr bool has_aug(int D) {
   return ((D + 3) & ~3) < DP;
 }
 
-template <int DP, bool AUG, bool WT>
+template <int DP, bool AUG, bool WT, bool BAYES>
 static void launch_rows_k(int64_t blocks, const RowTask *rows, int64_t n_rows,
                           const int32_t *idx, const uint8_t *val, const float *wts,
                           const float *Fp, int zrow, const float *ws, int D, float lam, float *X,
                           double *sse, int32_t *flag, double *cyc_gram, double *cyc_solve,
-                          hipStream_t s) {
-  hipLaunchKernelGGL((k_rows<DP, AUG, WT>), dim3((unsigned)blocks), dim3(64 * kRowWaves), 0, s,
-                     rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag, cyc_gram,
-                     cyc_solve);
+                          const RowPrior &pr, hipStream_t s) {
+  hipLaunchKernelGGL((k_rows<DP, AUG, WT, BAYES>), dim3((unsigned)blocks), dim3(64 * kRowWaves),
+                     0, s, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag,
+                     cyc_gram, cyc_solve, pr);
 }
 
 template <int DP>
@@ -425,22 +452,31 @@ static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32
                                 const uint8_t *val, const float *wts, const float *Fp, int zrow,
                                 const float *ws, int D, float lam, float *X, double *sse,
                                 int32_t *flag, double *cyc_gram, double *cyc_solve,
-                                hipStream_t s) {
+                                const RowPrior &pr, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
   const bool aug = has_aug<DP>(D), wt = wts != nullptr;
-  if (aug && wt)
-    launch_rows_k<DP, true, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
-                                  sse, flag, cyc_gram, cyc_solve, s);
+  if (pr.init) {
+    // the Gibbs half-sweep has no per-rating weights
+    if (wt) return hipErrorInvalidValue;
+    if (aug)
+      launch_rows_k<DP, true, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+    else
+      launch_rows_k<DP, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                            lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+  } else if (aug && wt)
+    launch_rows_k<DP, true, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                         lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
   else if (aug)
-    launch_rows_k<DP, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
-                                   sse, flag, cyc_gram, cyc_solve, s);
+    launch_rows_k<DP, true, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
   else if (wt)
-    launch_rows_k<DP, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
-                                   sse, flag, cyc_gram, cyc_solve, s);
+    launch_rows_k<DP, false, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
   else
-    launch_rows_k<DP, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X,
-                                    sse, flag, cyc_gram, cyc_solve, s);
+    launch_rows_k<DP, false, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
   return hipGetLastError();
 }
 
@@ -486,11 +522,11 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
                        const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
-                       double *cyc_gram, double *cyc_solve, hipStream_t s) {
+                       double *cyc_gram, double *cyc_solve, const RowPrior &pr, hipStream_t s) {
   if ((cyc_gram == nullptr) != (cyc_solve == nullptr)) return hipErrorInvalidValue;
   const int zrow = (int)n_fixed;
   ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam,
-                                              X, sse, flag, cyc_gram, cyc_solve, s));
+                                              X, sse, flag, cyc_gram, cyc_solve, pr, s));
 }
 
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
