@@ -49,7 +49,12 @@ def parse():
                     help="held-out prediction leg on 1/K of the stored positions (0 disables)")
     ap.add_argument("--weighted", action="store_true",
                     help="weighted ALS: seeded per-rating weights, log-uniform on [0.25, 4)")
-    return ap.parse_args()
+    ap.add_argument("--gibbs", action="store_true",
+                    help="Bayesian factorisation: one step is a BPMF Gibbs iteration")
+    args = ap.parse_args()
+    if args.gibbs and args.weighted:
+        ap.error("--gibbs and --weighted are exclusive")
+    return args
 
 
 def log(msg):
@@ -119,8 +124,9 @@ def measured_traffic(workload_name, kernel):
     return None
 
 
-def cpu_baseline(r, side_fixed, target_s, weights=None):
-    """fp64 oracle on a seeded random sample of the user half-sweep's rows."""
+def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False):
+    """fp64 oracle on a seeded random sample of the user half-sweep's rows (the Gibbs row
+    draws with ``gibbs``)."""
     import numpy as np
 
     import oracle
@@ -140,6 +146,15 @@ def cpu_baseline(r, side_fixed, target_s, weights=None):
         k = min(k, perm.size)
         sel = np.sort(perm[:k])
         t0 = time.perf_counter()
+        if gibbs:
+            sub_ptr = np.concatenate([[0], np.cumsum(deg[sel])]).astype(np.int64)
+            take = np.repeat(r.row_ptr[sel] - sub_ptr[:-1], deg[sel]) + np.arange(sub_ptr[-1])
+            Lam, mu = np.eye(r.D), np.zeros(r.D)
+            z = np.zeros((k, r.D))
+            t_a = time.perf_counter()
+            oracle.gibbs_rows(sub_ptr, r.col[take], val[take], fixed, GIBBS_ALPHA, Lam, mu, z,
+                              np.zeros((k, r.D)), threads=threads)
+            return int(deg[sel].sum()), k, time.perf_counter() - t_a
         oracle.solve_rows(sel, r.row_ptr, r.col, val, fixed, r.lam, threads=threads, w=w)
         dt = time.perf_counter() - t0
         return int(deg[sel].sum()), k, dt
@@ -158,7 +173,8 @@ def cpu_baseline(r, side_fixed, target_s, weights=None):
     n1, k1, t1 = run(target)
     return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
                 cpu_model=cpu_model,
-                sample=(f"user half-sweep of {r.name}{' (weighted)' if w is not None else ''}: "
+                sample=(f"user half-sweep of {r.name}"
+                        f"{' (weighted)' if w is not None else ' (Gibbs draws)' if gibbs else ''}: "
                         f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
@@ -205,6 +221,43 @@ def heldout_leg(args, r, als, U, V, workload_name, reps=20):
                 rmse_same_pairs=vr)
 
 
+# BPMF Gibbs iteration: the usual hyperprior (mu0 = 0, beta0 = 2, W0 = I, nu0 = D) and a
+# rating precision matching noise of standard deviation 10 on the 0..100 scale
+GIBBS_ALPHA = 0.01
+GIBBS_BETA0 = 2.0
+
+
+class GibbsSteps:
+    """Seeded variates for every Gibbs half-sweep of the run, generated on the device
+    before the timed region, and the hyperparameter buffers of both sides."""
+
+    def __init__(self, r, als, n_steps, seed):
+        import numpy as np
+        import torch
+
+        D = r.D
+        dev = torch.device("cuda:0")
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        rng = np.random.default_rng(seed)
+        self.z, self.var = {}, {}
+        for side, n in (("items", r.N), ("users", r.M)):
+            als.set_nw_prior(side, np.zeros(D), GIBBS_BETA0, np.eye(D), float(D))
+            self.z[side] = torch.randn((n_steps, n, D), generator=g, device=dev)
+            nu_s = D + n
+            self.var[side] = [tuple(torch.from_numpy(a).to(dev) for a in (
+                rng.chisquare(nu_s - np.arange(D)), rng.normal(size=D * (D - 1) // 2),
+                rng.normal(size=D))) for _ in range(n_steps)]
+        self.mu = {s: torch.empty(D, dtype=torch.float64, device=dev) for s in self.z}
+        self.Lam = {s: torch.empty((D, D), dtype=torch.float64, device=dev) for s in self.z}
+
+    def half(self, als, side, k, fixed, out):
+        chi2, offd, zmu = self.var[side][k]
+        als.sample_hyper(side, out, chi2, offd, zmu, self.mu[side], self.Lam[side])
+        als.gibbs_half_sweep(side, fixed, GIBBS_ALPHA, self.Lam[side], self.mu[side],
+                             self.z[side][k], out)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -237,9 +290,17 @@ def main():
         f"items {als.plan_stats('items')}")
     U = torch.from_numpy(U0).to(dev)
     V = torch.from_numpy(V0).to(dev)
+    gibbs = GibbsSteps(r, als, args.warmup + args.steps, r.init_seed + 77) if args.gibbs else None
+
+    def half(side, k, fixed, out):
+        if gibbs is not None:
+            gibbs.half(als, side, k, fixed, out)
+        else:
+            als.half_sweep(side, fixed, r.lam, out)
+
     for w in range(args.warmup):
-        als.half_sweep("items", U, r.lam, V)
-        als.half_sweep("users", V, r.lam, U)
+        half("items", w, U, V)
+        half("users", w, V, U)
         torch.cuda.synchronize()
         log(f"warmup {w + 1}/{args.warmup} done")
     torch.cuda.synchronize()
@@ -250,10 +311,10 @@ def main():
     t0 = time.perf_counter()
     for k in range(args.steps):
         ev["items"][k][0].record()
-        als.half_sweep("items", U, r.lam, V)
+        half("items", args.warmup + k, U, V)
         ev["items"][k][1].record()
         ev["users"][k][0].record()
-        als.half_sweep("users", V, r.lam, U)
+        half("users", args.warmup + k, V, U)
         ev["users"][k][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -271,8 +332,8 @@ def main():
     if r.D > 20:
         # one extra, untimed half-sweep per side with the row kernel's phase clocks on
         als.set_phase_timing(True)
-        als.half_sweep("items", U, r.lam, V)
-        als.half_sweep("users", V, r.lam, U)
+        half("items", args.warmup + args.steps - 1, U, V)
+        half("users", args.warmup + args.steps - 1, V, U)
         gi, si = als.phase_cycles("items")
         gu, su = als.phase_cycles("users")
         als.set_phase_timing(False)
@@ -285,7 +346,7 @@ def main():
     rows_with = als.plan_stats("users")["rows_with_ratings"] + \
         als.plan_stats("items")["rows_with_ratings"]
     D = r.D
-    workload_name = r.name + ("_wals" if args.weighted else "")
+    workload_name = r.name + ("_wals" if args.weighted else "_bpmf" if args.gibbs else "")
     dominant = max(prof, key=lambda k: prof[k][0])
     wbytes = 4 if args.weighted else 0   # a weight per rating
     wflops = D if args.weighted else 0   # c f per rating
@@ -328,11 +389,12 @@ def main():
     cpu = None
     if args.cpu_seconds > 0:
         log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
-        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights)
+        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights, gibbs=args.gibbs)
         log(f"cpu baseline: {cpu}")
 
     out = {
-        "metric": ("wALS" if args.weighted else "ALS") + " ratings/sec per half-sweep",
+        "metric": ("wALS" if args.weighted else "BPMF Gibbs" if args.gibbs else "ALS")
+        + " ratings/sec per half-sweep",
         "value": value,
         "unit": "ratings/s",
         "n_gpus": 1,
@@ -347,7 +409,12 @@ def main():
         "config": {"workload": workload_name, "n_users": r.M, "n_items": r.N, "nnz": r.nnz, "D": r.D,
                    "weights": ("per rating, log-uniform on [0.25, 4), seeded" if args.weighted
                                else None),
-                   "lambda": r.lam, "step": "item half-sweep + user half-sweep",
+                   "lambda": None if args.gibbs else r.lam,
+                   "gibbs": (dict(alpha=GIBBS_ALPHA, mu0=0.0, beta0=GIBBS_BETA0, W0="I",
+                                  nu0=r.D, variates="seeded, on the device before timing")
+                             if args.gibbs else None),
+                   "step": ("item side (hyperparameter draw, row draws) + user side"
+                            if args.gibbs else "item half-sweep + user half-sweep"),
                    "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -117,7 +117,7 @@ struct als_ctx {
   double *d_hold_sse = nullptr;
   // Bayesian Gibbs step (allocated on first use)
   float *d_prior_init = nullptr;   // prior image of the row kernels
-  float *d_prior_K = nullptr;      // L^{-T} of the prior precision, for rows without ratings
+  float *d_prior_K = nullptr;      // Cholesky factor of the prior precision (rows without ratings)
   float *d_prior_mu32 = nullptr;
   int32_t *d_prior_ok = nullptr;
   double *d_bayes_scratch = nullptr;
@@ -777,8 +777,9 @@ als_status als_gibbs_half_sweep(als_ctx *ctx, als_side side, const float *fixed_
   als_status st = ensure_bayes(ctx);
   if (st != ALS_OK) return st;
   HIP_OR_FAIL(ctx, als::launch_prior_prepare(Lambda, mu, ctx->D, ctx->DP, (double)alpha,
+                                             !ctx->plan[side].zero_rows.empty(),
                                              ctx->d_prior_init, ctx->d_prior_K, ctx->d_prior_mu32,
-                                             ctx->d_bayes_scratch, ctx->d_prior_ok, ctx->stream));
+                                             ctx->d_prior_ok, ctx->stream));
   als::RowPrior pr;
   pr.init = ctx->d_prior_init;
   pr.z = z;

@@ -7,22 +7,23 @@
 //   k_prior_prepare   one workgroup, fp64: the prior image the row kernels start from
 //                     (Lambda / alpha with the identity on the padding, and
 //                     Lambda mu / alpha), laid out as a workspace slot (D > 20) or a
-//                     packed record (D <= 20); and K = L^{-T} (Lambda = L L^T) for the
-//                     rows without ratings, which are drawn from the prior.
-//   k_prior_rows      one lane per row without ratings: x = mu + K z.
+//                     packed record (D <= 20); and, when the side has rows without
+//                     ratings, the Cholesky factor L of Lambda for them.
+//   k_prior_rows      one lane per row without ratings: x = mu + L^{-T} z.
 //   k_hyper_moments   per-block fp64 sums of x and of the upper triangle of x x^T over
 //                     the side's rows (rows staged through LDS); products of two fp32
 //                     values are exact in fp64, so only the summation order rounds.
-//   k_hyper_sample    one workgroup, fp64: sums the blocks in order, forms the
+//   k_hyper_reduce    the per-block partials summed in 16 fixed segments, in order.
+//   k_hyper_sample    one workgroup, fp64: adds the segments in order, forms the
 //                     Normal-Wishart posterior (beta* = beta0 + n, nu* = nu0 + n,
 //                     mu0* = (beta0 mu0 + n xbar) / beta*, W*^{-1} = W0^{-1} + S +
 //                     beta0 n / beta* (mu0 - xbar)(mu0 - xbar)^T with S the scatter
 //                     about the mean), then Bartlett's draw: W* = F F^T, B lower
 //                     triangular with B_ii = sqrt(chi2_i) and normal B_ij, Lambda =
 //                     (F B)(F B)^T, and mu = mu0* + R^{-T} zmu with beta* Lambda = R R^T.
-// The variates (chi-square, normals) are inputs. Matrices live in the fp64 scratch as
-// full row-major D x D arrays; the factorisations are right-looking Cholesky steps with
-// a barrier between steps.
+// The variates (chi-square, normals) are inputs. Matrices live as fp64
+// packed triangles in LDS (two of them, 132 KB at D = 128); the factorisations are
+// right-looking Cholesky steps with a barrier between steps.
 #include "internal.h"
 
 namespace als {
@@ -30,83 +31,83 @@ namespace als {
 namespace {
 
 constexpr int kBayesBlock = 256;
-constexpr int kMomentRows = 32;  // rows per LDS stage of the moment kernel
-constexpr int kMaxEntriesPerThread = (128 + 128 * 129 / 2 + kBayesBlock - 1) / kBayesBlock;
+constexpr int kStageFloats = 16384;  // LDS stage of the moment kernel (64 KB of rows)
 constexpr int kHyperBlocks = 1024;
+constexpr int kReduceSegs = 16;      // the moment partials are summed in 16 segments
+constexpr int kMaxD = 128;
+constexpr int kPacked = kMaxD * (kMaxD + 1) / 2;
+// 4 x 4 tiles of the upper block triangle of x x^T, per thread at most this many
+constexpr int kTilesPerThread = ((kMaxD / 4) * (kMaxD / 4 + 1) / 2 + kBayesBlock - 1) / kBayesBlock;
 
-// In-place lower Cholesky factor of the D x D matrix A (the lower triangle is read, the
-// strict upper triangle is zeroed). *bad is set when a pivot is not positive and finite.
-__device__ void blk_cholesky(double *A, int D, int *bad) {
+// Index of (i, j), j <= i, in a packed lower triangle.
+__device__ __forceinline__ int pl(int i, int j) { return i * (i + 1) / 2 + j; }
+
+// In-place lower Cholesky factor of the packed lower triangle P (in LDS), right-looking:
+// per column, the pivot's square root, the column scaled, then the trailing triangle
+// updated, with barriers between. *bad is set when a pivot is not positive and finite
+// (the step then continues with a unit pivot, so that every value stays defined).
+__device__ void lds_cholesky(double *P, int D, int *bad) {
   for (int k = 0; k < D; ++k) {
     __syncthreads();
-    const double p = A[k * D + k];
+    const double p = P[pl(k, k)];
     const bool ok = p > 0.0 && isfinite(p);
-    const double l = sqrt(ok ? p : 1.0);
+    const double l = ok ? sqrt(p) : 1.0;
     if (!ok && threadIdx.x == 0) *bad = 1;
     __syncthreads();
-    if (threadIdx.x == 0) A[k * D + k] = l;
-    for (int i = k + 1 + threadIdx.x; i < D; i += blockDim.x) A[i * D + k] /= l;
+    if (threadIdx.x == 0) P[pl(k, k)] = l;
+    for (int i = k + 1 + threadIdx.x; i < D; i += blockDim.x) P[pl(i, k)] /= l;
     __syncthreads();
-    const int m = D - k - 1;
-    for (int q = threadIdx.x; q < m * m; q += blockDim.x) {
-      const int i = k + 1 + q / m, j = k + 1 + q % m;
-      if (j <= i) A[i * D + j] -= A[i * D + k] * A[j * D + k];
+    // trailing triangle k < j <= i < D on a 16 x 16 grid of threads
+    for (int i = k + 1 + (int)(threadIdx.x >> 4); i < D; i += 16) {
+      const double lik = P[pl(i, k)];
+      for (int j = k + 1 + (int)(threadIdx.x & 15); j <= i; j += 16)
+        P[pl(i, j)] -= lik * P[pl(j, k)];
     }
   }
   __syncthreads();
-  for (int q = threadIdx.x; q < D * D; q += blockDim.x)
-    if (q % D > q / D) A[q] = 0.0;
-  __syncthreads();
 }
 
-// Li = L^{-1} (lower triangular), one column per thread.
-__device__ void blk_lower_inverse(const double *L, double *Li, int D) {
+// Li = L^{-1} for the packed lower triangles L and Li (in LDS), one column per thread
+// (each column's forward substitution only reads L and its own earlier entries).
+__device__ void lds_lower_inverse(const double *L, double *Li, int D) {
   for (int e = threadIdx.x; e < D; e += blockDim.x) {
-    for (int i = 0; i < D; ++i) {
-      if (i < e) {
-        Li[i * D + e] = 0.0;
-        continue;
-      }
+    for (int i = e; i < D; ++i) {
       double s = i == e ? 1.0 : 0.0;
-      for (int m = e; m < i; ++m) s -= L[i * D + m] * Li[m * D + e];
-      Li[i * D + e] = s / L[i * D + i];
+      for (int m = e; m < i; ++m) s -= L[pl(i, m)] * Li[pl(m, e)];
+      Li[pl(i, e)] = s / L[pl(i, i)];
     }
-  }
-  __syncthreads();
-}
-
-// C = A B^T for full D x D matrices (C distinct from A and B).
-__device__ void blk_mul_abt(const double *A, const double *B, double *C, int D) {
-  for (int q = threadIdx.x; q < D * D; q += blockDim.x) {
-    const int i = q / D, j = q % D;
-    double t = 0.0;
-    for (int m = 0; m < D; ++m) t += A[i * D + m] * B[j * D + m];
-    C[q] = t;
   }
   __syncthreads();
 }
 
 __global__ __launch_bounds__(kBayesBlock) void k_prior_prepare(
     const double *__restrict__ Lam, const double *__restrict__ mu, int D, int DP, int LD,
-    int aug_col, double alpha, float *__restrict__ init, float *__restrict__ K,
-    float *__restrict__ mu32, double *__restrict__ scratch, int32_t *__restrict__ ok) {
+    int aug_col, double alpha, int need_factor, float *__restrict__ init,
+    float *__restrict__ K, float *__restrict__ mu32, int32_t *__restrict__ ok) {
+  __shared__ double P1[kPacked];
+  __shared__ double c[kMaxD];  // Lambda mu / alpha
   __shared__ int bad;
   if (threadIdx.x == 0) bad = 0;
-  double *c = scratch;            // Lambda mu / alpha
-  double *L = scratch + 2 * D;    // Cholesky factor of Lambda
-  double *Li = L + D * D;         // its inverse
+  __shared__ double mus[kMaxD];
   for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    double t = 0.0;
-    for (int e = 0; e < D; ++e) t += Lam[d * D + e] * mu[e];
-    c[d] = t / alpha;
+    mus[d] = mu[d];
     mu32[d] = (float)mu[d];
   }
-  for (int q = threadIdx.x; q < D * D; q += blockDim.x) L[q] = Lam[q];
+  // the lower triangle of Lambda (symmetric by contract) into LDS
+  for (int i = (int)(threadIdx.x >> 4); i < D; i += 16)
+    for (int j = (int)(threadIdx.x & 15); j <= i; j += 16) P1[pl(i, j)] = Lam[i * D + j];
+  __syncthreads();
+  auto lam = [&](int a, int b) -> double { return a >= b ? P1[pl(a, b)] : P1[pl(b, a)]; };
+  for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    double t = 0.0;
+    for (int e = 0; e < D; ++e) t += lam(d, e) * mus[e];
+    c[d] = t / alpha;
+  }
   __syncthreads();
   // entry (r, col) of the scaled prior matrix, the identity on the padding, and with the
   // augmented column (D > 20 only) holding Lambda mu / alpha
   auto entry = [&](int r, int col) -> float {
-    if (r < D && col < D) return (float)(Lam[r * D + col] / alpha);
+    if (r < D && col < D) return (float)(lam(r, col) / alpha);
     if (col == aug_col && r < D) return (float)c[r];
     return r == col ? 1.f : 0.f;
   };
@@ -147,16 +148,21 @@ __global__ __launch_bounds__(kBayesBlock) void k_prior_prepare(
       init[q] = v;
     }
   }
-  // K = L^{-T} for the rows without ratings
-  blk_cholesky(L, D, &bad);
-  blk_lower_inverse(L, Li, D);
-  for (int q = threadIdx.x; q < D * D; q += blockDim.x) K[q] = (float)Li[(q % D) * D + q / D];
-  __syncthreads();
+  // the Cholesky factor L of Lambda for the rows without ratings, when the side has any
+  // (the image is written above, so P1 can be factored in place)
+  if (need_factor) {
+    lds_cholesky(P1, D, &bad);
+    for (int q = threadIdx.x; q < D * D; q += blockDim.x) {
+      const int i = q / D, j = q % D;
+      K[q] = j <= i ? (float)P1[pl(i, j)] : 0.f;
+    }
+    __syncthreads();
+  }
   if (threadIdx.x == 0) *ok = bad ? 0 : 1;
 }
 
 __global__ __launch_bounds__(64) void k_prior_rows(const int32_t *__restrict__ rows, int64_t n,
-                                                  int D, const float *__restrict__ K,
+                                                  int D, const float *__restrict__ L,
                                                   const float *__restrict__ mu32,
                                                   const int32_t *__restrict__ ok,
                                                   const float *__restrict__ z,
@@ -169,177 +175,256 @@ __global__ __launch_bounds__(64) void k_prior_rows(const int32_t *__restrict__ r
     atomicAdd(flag_count, 1);
     return;
   }
+  // x = mu + L^{-T} z: back substitution with L^T into the row, then the mean added
   const float *__restrict__ zr = z + row * D;
   float *__restrict__ xr = X + row * D;
-  for (int a = 0; a < D; ++a) {
-    float t = mu32[a];
-    for (int e = a; e < D; ++e) t = fmaf(K[a * D + e], zr[e], t);
-    xr[a] = t;
+  for (int a = D - 1; a >= 0; --a) {
+    float t = zr[a];
+    for (int e = a + 1; e < D; ++e) t = fmaf(-L[e * D + a], xr[e], t);
+    xr[a] = t / L[a * D + a];
   }
+  for (int a = 0; a < D; ++a) xr[a] += mu32[a];
 }
 
+// Moments: the block's rows are staged through LDS; each thread accumulates whole 4 x 4
+// tiles (I, J), I <= J, of the upper block triangle of x x^T (four values of each row
+// feed sixteen products), and thread a < D the sum of feature a. When there are fewer
+// tiles than threads, G = 256 / tiles threads share a tile, thread g of them taking the
+// staged rows r = g mod G; their partial tiles are added in order of g at the end.
+// Entries are written in the packed order: the D sums of x_a, then the upper triangle of
+// x x^T row by row.
 __global__ __launch_bounds__(kBayesBlock) void k_hyper_moments(const float *__restrict__ X,
                                                                int64_t n, int D,
                                                                double *__restrict__ partials) {
-  __shared__ float xs[kMomentRows][128];
+  __shared__ __align__(16) float xs_flat[kStageFloats];
+  const int nb = (D + 3) / 4;       // 4-wide feature blocks
+  const int w4 = 4 * nb;            // staged row width
+  const int stage_rows = min(256, kStageFloats / w4);
+  const int ntl = nb * (nb + 1) / 2;
   const int ne = D + D * (D + 1) / 2;
-  // this thread's entries: packed (a, e) pairs, e = a + (upper triangle) or e = -1 (sum of x_a)
-  int16_t ea[kMaxEntriesPerThread], ee[kMaxEntriesPerThread];
-  double acc[kMaxEntriesPerThread];
-  int cnt = 0;
+  const int G = max(1, kBayesBlock / ntl);  // threads per tile
+  const int g = (int)threadIdx.x % G, slot = (int)threadIdx.x / G, slots = kBayesBlock / G;
+  int ti[kTilesPerThread], tj[kTilesPerThread];
+  double acc[kTilesPerThread][16], sx = 0.0;
 #pragma unroll
-  for (int k = 0; k < kMaxEntriesPerThread; ++k) {
-    const int q = threadIdx.x + k * kBayesBlock;
-    ea[k] = 0;
-    ee[k] = -1;
-    acc[k] = 0.0;
-    if (q < ne) {
-      cnt = k + 1;
-      if (q < D) {
-        ea[k] = (int16_t)q;
-      } else {
-        int rem = q - D, a = 0;
-        while (rem >= D - a) {
-          rem -= D - a;
-          ++a;
-        }
-        ea[k] = (int16_t)a;
-        ee[k] = (int16_t)(a + rem);
+  for (int k = 0; k < kTilesPerThread; ++k) {
+    int t = slot + k * slots, I = 0;
+    ti[k] = -1;
+    tj[k] = -1;
+    if (slot < slots && t < ntl) {
+      while (t >= nb - I) {
+        t -= nb - I;
+        ++I;
       }
+      ti[k] = I;
+      tj[k] = I + t;
     }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[k][q] = 0.0;
   }
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
   const int64_t r0 = (int64_t)blockIdx.x * per, r1 = min(n, r0 + per);
-  for (int64_t base = r0; base < r1; base += kMomentRows) {
-    const int rows = (int)min<int64_t>(kMomentRows, r1 - base);
+  for (int64_t base = r0; base < r1; base += stage_rows) {
+    const int rows = (int)min<int64_t>(stage_rows, r1 - base);
     __syncthreads();
-    for (int q = threadIdx.x; q < rows * D; q += kBayesBlock)
-      xs[q / D][q % D] = X[(base + q / D) * D + q % D];
+    for (int q = threadIdx.x; q < rows * w4; q += kBayesBlock) {
+      const int r = q / w4, d = q % w4;
+      xs_flat[q] = d < D ? X[(base + r) * D + d] : 0.f;
+    }
     __syncthreads();
+    if ((int)threadIdx.x < D) {
+      for (int r = 0; r < rows; ++r) sx += (double)xs_flat[r * w4 + threadIdx.x];
+    }
 #pragma unroll
-    for (int k = 0; k < kMaxEntriesPerThread; ++k) {
-      if (k < cnt) {
-        const int a = ea[k], e = ee[k];
-        double t = acc[k];
-        if (e < 0) {
-          for (int r = 0; r < rows; ++r) t += (double)xs[r][a];
-        } else {
-          for (int r = 0; r < rows; ++r) t = fma((double)xs[r][a], (double)xs[r][e], t);
+    for (int k = 0; k < kTilesPerThread; ++k) {
+      if (ti[k] >= 0) {
+        const int a0 = 4 * ti[k], e0 = 4 * tj[k];
+        for (int r = g; r < rows; r += G) {
+          const float4 va = *reinterpret_cast<const float4 *>(xs_flat + r * w4 + a0);
+          const float4 ve = *reinterpret_cast<const float4 *>(xs_flat + r * w4 + e0);
+          const double xa[4] = {va.x, va.y, va.z, va.w};
+          const double xe[4] = {ve.x, ve.y, ve.z, ve.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) acc[k][4 * q + w] = fma(xa[q], xe[w], acc[k][4 * q + w]);
+          }
         }
-        acc[k] = t;
       }
     }
   }
+  double *__restrict__ out = partials + (int64_t)blockIdx.x * ne;
+  if ((int)threadIdx.x < D) out[threadIdx.x] = sx;
+  // the G partial tiles of a slot are added in order of g through LDS (G > 1 means one
+  // tile per thread)
+  double *red = reinterpret_cast<double *>(xs_flat);  // 256 x 16 doubles = 32 KB
 #pragma unroll
-  for (int k = 0; k < kMaxEntriesPerThread; ++k) {
-    const int q = threadIdx.x + k * kBayesBlock;
-    if (q < ne) partials[(int64_t)blockIdx.x * ne + q] = acc[k];
+  for (int k = 0; k < kTilesPerThread; ++k) {
+    if (G > 1) {
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 16; ++q) red[threadIdx.x * 16 + q] = acc[k][q];
+      __syncthreads();
+      if (g == 0 && ti[k] >= 0) {
+        for (int h = 1; h < G; ++h) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) acc[k][q] += red[(threadIdx.x + h) * 16 + q];
+        }
+      }
+    }
+    if (g == 0 && ti[k] >= 0) {
+      const int a0 = 4 * ti[k], e0 = 4 * tj[k];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const int a = a0 + q, e = e0 + w;
+          if (a <= e && e < D) out[D + a * D - a * (a - 1) / 2 + (e - a)] = acc[k][4 * q + w];
+        }
+      }
+    }
   }
 }
 
+// Segment sums of the moment partials: thread (q, seg) adds entry q of the blocks of
+// segment seg in block order (the loads of one thread are independent, so many are in
+// flight); the draw kernel adds the segments in order.
+__global__ __launch_bounds__(64) void k_hyper_reduce(const double *__restrict__ partials, int nblk,
+                                                     int ne, double *__restrict__ seg_sums) {
+  const int q = blockIdx.x * 64 + threadIdx.x;
+  const int seg = blockIdx.y;
+  if (q >= ne) return;
+  const int per = (nblk + kReduceSegs - 1) / kReduceSegs;
+  const int b0 = seg * per, b1 = min(nblk, b0 + per);
+  double t = 0.0;
+#pragma unroll 16
+  for (int b = b0; b < b1; ++b) t += partials[(int64_t)b * ne + q];
+  seg_sums[(int64_t)seg * ne + q] = t;
+}
+
+// Normal-Wishart posterior and Bartlett draw on two packed triangles in LDS:
+//   P1 = W*^{-1} -> R (Cholesky);  P2 = R^{-1};  P1 = W* = R^{-T} R^{-1} -> F (Cholesky);
+//   P2 = F B (lower times lower is lower);  P1 = Lambda = (F B)(F B)^T, written out;
+//   P1 = beta* Lambda -> its Cholesky factor;  mu = mu0* + R^{-T} zmu.
 __global__ __launch_bounds__(kBayesBlock) void k_hyper_sample(
-    const double *__restrict__ partials, int nblk, int64_t n, int D,
+    const double *__restrict__ seg_sums, int64_t n, int D,
     const double *__restrict__ mu0, double beta0, const double *__restrict__ W0inv, double nu0,
     const double *__restrict__ chi2, const double *__restrict__ offd,
-    const double *__restrict__ zmu, double *__restrict__ scratch, double *__restrict__ mu_out,
+    const double *__restrict__ zmu, double *__restrict__ H, double *__restrict__ mu_out,
     double *__restrict__ Lam_out, int32_t *__restrict__ status) {
+  __shared__ double P1[kPacked], P2[kPacked];
+  __shared__ double xbar[kMaxD], dv[kMaxD], tmp[kMaxD];
   __shared__ int bad;
   if (threadIdx.x == 0) bad = 0;
-  const int ne = D + D * (D + 1) / 2, DD = D * D;
-  double *A = scratch;        // W*^{-1}, then its factor R
-  double *B = A + DD;         // R^{-1}
-  double *C = B + DD;         // W*, then its factor F
-  double *E = C + DD;         // F B
-  double *G = E + DD;         // beta* Lambda, then its factor
-  double *H = G + DD;         // moments: sums of x_a, then of x_a x_e (upper triangle)
-  double *xbar = H + ne;      // mean, then mu0*
-  double *dv = xbar + D;      // mu0 - xbar
-  double *tmp = dv + D;
+  const int ne = D + D * (D + 1) / 2;
+  // the moments: segment sums added in segment order (H: global scratch of ne doubles)
   for (int q = threadIdx.x; q < ne; q += blockDim.x) {
     double t = 0.0;
-    for (int b = 0; b < nblk; ++b) t += partials[(int64_t)b * ne + q];
+#pragma unroll
+    for (int g = 0; g < kReduceSegs; ++g) t += seg_sums[(int64_t)g * ne + q];
     H[q] = t;
   }
   __syncthreads();
   const double nn = (double)n;
-  const double beta_s = beta0 + nn, nu_s = nu0 + nn;
+  const double beta_s = beta0 + nn;
   const double shrink = beta_s > 0.0 ? beta0 * nn / beta_s : 0.0;
   for (int a = threadIdx.x; a < D; a += blockDim.x) {
     xbar[a] = n > 0 ? H[a] / nn : 0.0;
     dv[a] = mu0[a] - xbar[a];
   }
   __syncthreads();
-  // W*^{-1} = W0^{-1} + (sum x x^T - n xbar xbar^T) + shrink dv dv^T (full matrix)
-  for (int q = threadIdx.x; q < DD; q += blockDim.x) {
-    const int i = q / D, j = q % D;
-    const int a = min(i, j), e = max(i, j);
-    const double sxx = H[D + a * D - a * (a - 1) / 2 + (e - a)];
-    A[q] = W0inv[q] + (sxx - nn * xbar[i] * xbar[j]) + shrink * dv[i] * dv[j];
+  // W*^{-1} = W0^{-1} + (sum x x^T - n xbar xbar^T) + shrink dv dv^T (lower triangle)
+  for (int i = (int)(threadIdx.x >> 4); i < D; i += 16) {
+    for (int j = (int)(threadIdx.x & 15); j <= i; j += 16) {
+      const double sxx = H[D + j * D - j * (j - 1) / 2 + (i - j)];
+      P1[pl(i, j)] = W0inv[i * D + j] + (sxx - nn * xbar[i] * xbar[j]) + shrink * dv[i] * dv[j];
+    }
   }
   __syncthreads();
   for (int a = threadIdx.x; a < D; a += blockDim.x)
     xbar[a] = (beta0 * mu0[a] + nn * xbar[a]) / beta_s;  // mu0*
-  // W* = R^{-T} R^{-1}, F = chol(W*)
-  blk_cholesky(A, D, &bad);
-  blk_lower_inverse(A, B, D);
-  for (int q = threadIdx.x; q < DD; q += blockDim.x) {
-    const int i = q / D, j = q % D;
-    double t = 0.0;
-    for (int m = max(i, j); m < D; ++m) t += B[m * D + i] * B[m * D + j];
-    C[q] = t;
+  lds_cholesky(P1, D, &bad);
+  lds_lower_inverse(P1, P2, D);
+  // W* = R^{-T} R^{-1}: entry (i, j), j <= i, sums over m >= i
+  for (int i = (int)(threadIdx.x >> 4); i < D; i += 16) {
+    for (int j = (int)(threadIdx.x & 15); j <= i; j += 16) {
+      double t = 0.0;
+      for (int m = i; m < D; ++m) t += P2[pl(m, i)] * P2[pl(m, j)];
+      P1[pl(i, j)] = t;
+    }
+  }
+  lds_cholesky(P1, D, &bad);  // F
+  // Bartlett's B into P2 (packed in the same order: row m, column j < m: offd[pl(m, j) - m])
+  for (int q = threadIdx.x; q < D * (D + 1) / 2; q += blockDim.x) {
+    int m = (int)((sqrt(8.0 * q + 1.0) - 1.0) * 0.5);
+    while (pl(m, 0) > q) --m;
+    while (pl(m + 1, 0) <= q) ++m;
+    const int j = q - pl(m, 0);
+    P2[q] = j == m ? sqrt(chi2[m]) : offd[q - m];
   }
   __syncthreads();
-  blk_cholesky(C, D, &bad);
-  // E = F B with Bartlett's lower triangular B
-  for (int q = threadIdx.x; q < DD; q += blockDim.x) {
-    const int i = q / D, j = q % D;
-    double t = 0.0;
-    for (int m = j; m <= i; ++m) {
-      const double bm = m == j ? sqrt(chi2[j]) : offd[(int64_t)m * (m - 1) / 2 + j];
-      t += C[i * D + m] * bm;
+  // E = F B in place of F, one row per thread: entry (i, j) needs F[i][m] for m >= j only,
+  // so a row is overwritten in increasing j
+  for (int i = threadIdx.x; i < D; i += blockDim.x) {
+    for (int j = 0; j <= i; ++j) {
+      double t = 0.0;
+      for (int m = j; m <= i; ++m) t += P1[pl(i, m)] * P2[pl(m, j)];
+      P1[pl(i, j)] = t;
     }
-    E[q] = t;
   }
   __syncthreads();
-  blk_mul_abt(E, E, Lam_out, D);
-  for (int q = threadIdx.x; q < DD; q += blockDim.x) G[q] = beta_s * Lam_out[q];
-  blk_cholesky(G, D, &bad);
-  // mu = mu0* + R^{-T} zmu (back substitution, one thread)
-  if (threadIdx.x == 0) {
-    for (int i = D - 1; i >= 0; --i) {
-      double t = zmu[i];
-      for (int m = i + 1; m < D; ++m) t -= G[m * D + i] * tmp[m];
-      tmp[i] = t / G[i * D + i];
+  // Lambda = E E^T into P2
+  for (int i = (int)(threadIdx.x >> 4); i < D; i += 16) {
+    for (int j = (int)(threadIdx.x & 15); j <= i; j += 16) {
+      double t = 0.0;
+      for (int m = 0; m <= j; ++m) t += P1[pl(i, m)] * P1[pl(j, m)];
+      P2[pl(i, j)] = t;
+      Lam_out[i * D + j] = t;
+      Lam_out[j * D + i] = t;
     }
-    for (int i = 0; i < D; ++i) mu_out[i] = xbar[i] + tmp[i];
-    *status = bad ? 1 : 0;
   }
+  __syncthreads();
+  for (int q = threadIdx.x; q < D * (D + 1) / 2; q += blockDim.x) P2[q] *= beta_s;
+  lds_cholesky(P2, D, &bad);
+  // mu = mu0* + R^{-T} zmu: back substitution with R^T, column by column (tmp holds the
+  // right-hand side still to be reduced)
+  for (int i = threadIdx.x; i < D; i += blockDim.x) tmp[i] = zmu[i];
+  for (int i = D - 1; i >= 0; --i) {
+    __syncthreads();
+    const double ti = tmp[i] / P2[pl(i, i)];
+    __syncthreads();
+    if (threadIdx.x == 0) tmp[i] = ti;
+    for (int m = threadIdx.x; m < i; m += blockDim.x) tmp[m] -= P2[pl(i, m)] * ti;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < D; i += blockDim.x) mu_out[i] = xbar[i] + tmp[i];
+  if (threadIdx.x == 0) *status = bad ? 1 : 0;
 }
 
 }  // namespace
 
 hipError_t launch_prior_prepare(const double *Lam, const double *mu, int D, int DP, double alpha,
-                                float *init, float *K, float *mu32, double *scratch, int32_t *ok,
+                                bool need_factor, float *init, float *L, float *mu32, int32_t *ok,
                                 hipStream_t s) {
   if (D < 1 || D > 128 || !(alpha > 0.0)) return hipErrorInvalidValue;
   const int LD = lane_width(D);
   const int aug_col = (!LD && ((D + 3) & ~3) < DP) ? ((D + 3) & ~3) : -1;
   hipLaunchKernelGGL(k_prior_prepare, dim3(1), dim3(kBayesBlock), 0, s, Lam, mu, D, DP, LD,
-                     aug_col, alpha, init, K, mu32, scratch, ok);
+                     aug_col, alpha, need_factor ? 1 : 0, init, L, mu32, ok);
   return hipGetLastError();
 }
 
-hipError_t launch_prior_rows(const int32_t *rows, int64_t n, int D, const float *K,
+hipError_t launch_prior_rows(const int32_t *rows, int64_t n, int D, const float *L,
                              const float *mu32, const int32_t *ok, const float *z, float *X,
                              int32_t *flag, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_prior_rows, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, s, rows, n, D, K,
+  hipLaunchKernelGGL(k_prior_rows, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, s, rows, n, D, L,
                      mu32, ok, z, X, flag);
   return hipGetLastError();
 }
 
 int hyper_blocks(int64_t n) {
-  return (int)std::max<int64_t>(1, std::min<int64_t>(kHyperBlocks, (n + kMomentRows - 1) / kMomentRows));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(kHyperBlocks, (n + 63) / 64));
 }
 
 hipError_t launch_hyper_moments(const float *X, int64_t n, int D, double *partials, hipStream_t s) {
@@ -354,8 +439,14 @@ hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int 
                                const double *chi2, const double *offd, const double *zmu,
                                double *scratch, double *mu_out, double *Lam_out, int32_t *status,
                                hipStream_t s) {
-  if (D < 1 || D > 128) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_hyper_sample, dim3(1), dim3(kBayesBlock), 0, s, partials, nblk, n, D, mu0,
+  if (D < 1 || D > 128 || nblk < 1) return hipErrorInvalidValue;
+  const int ne = hyper_entries(D);
+  double *seg_sums = scratch + ne + 8;
+  hipLaunchKernelGGL(k_hyper_reduce, dim3((unsigned)((ne + 63) / 64), kReduceSegs), dim3(64), 0, s,
+                     partials, nblk, ne, seg_sums);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_hyper_sample, dim3(1), dim3(kBayesBlock), 0, s, seg_sums, n, D, mu0,
                      beta0, W0inv, nu0, chi2, offd, zmu, scratch, mu_out, Lam_out, status);
   return hipGetLastError();
 }

@@ -137,23 +137,23 @@ __host__ __device__ constexpr int tri(int a, int b) {  // a <= b
 
 // ---- Bayesian Gibbs step (bayes.hip) ----------------------------------------------------
 
-// fp64 scratch (doubles) that the prior preparation and the hyperparameter draw need.
-inline size_t bayes_scratch_doubles(int D) {
-  return (size_t)5 * D * D + (size_t)(D + D * (D + 1) / 2) + 3 * (size_t)D + 8;
-}
+// fp64 scratch (doubles) of the hyperparameter draw: the summed moments and 16 segment
+// sums of them.
+inline size_t bayes_scratch_doubles(int D) { return (size_t)17 * (D + D * (D + 1) / 2) + 8; }
 // Floats of the prior image: a workspace slot (D > 20) or a packed record (D <= 20).
 inline size_t prior_init_floats(int D, int DP) {
   return lane_width(D) ? (size_t)ne_floats(lane_width(D)) : slot_floats_rt(DP);
 }
 
 // Prior image of a Gibbs half-sweep from the device hyperparameters Lambda (D x D) and mu
-// (fp64): init (prior_init_floats), and for rows without ratings K = L^{-T} (Lambda = L L^T,
-// fp32 D x D) and mu in fp32; *ok = 1, or 0 when Lambda is not numerically SPD.
+// (fp64): init (prior_init_floats) and mu in fp32; with need_factor (the side has rows
+// without ratings) also the lower Cholesky factor L of Lambda (fp32 D x D) and *ok = 1,
+// or 0 when Lambda is not numerically SPD.
 hipError_t launch_prior_prepare(const double *Lam, const double *mu, int D, int DP, double alpha,
-                                float *init, float *K, float *mu32, double *scratch, int32_t *ok,
+                                bool need_factor, float *init, float *L, float *mu32, int32_t *ok,
                                 hipStream_t s);
-// Rows without ratings drawn from the prior: X[row] = mu + K z_row (flagged when !*ok).
-hipError_t launch_prior_rows(const int32_t *rows, int64_t n, int D, const float *K,
+// Rows without ratings drawn from the prior: X[row] = mu + L^{-T} z_row (flagged when !*ok).
+hipError_t launch_prior_rows(const int32_t *rows, int64_t n, int D, const float *L,
                              const float *mu32, const int32_t *ok, const float *z, float *X,
                              int32_t *flag, hipStream_t s);
 // Per-block fp64 sums of x and of the upper triangle of x x^T over the n rows of X
