@@ -74,6 +74,10 @@ def _configure(lib):
     lib.orc_nw_posterior.restype = None
     lib.orc_nw_sample.argtypes = [i32, P, f64, P, P, P, P, P, P]
     lib.orc_nw_sample.restype = c_int
+    lib.orc_tensor_rows.argtypes = [i64, P, P, P, P, i32, P, P, f64, P, P, c_int]
+    lib.orc_tensor_rows.restype = i64
+    lib.orc_tensor_sse.argtypes = [i64, P, P, P, P, i32, P, P, P, c_int]
+    lib.orc_tensor_sse.restype = f64
     lib.orc_predict.argtypes = [i64, P, P, i32, P, P, P, c_int]
     lib.orc_predict.restype = None
     lib.orc_pair_sse.argtypes = [i64, P, P, P, i32, P, P, c_int]
@@ -333,3 +337,80 @@ def nw_sample(mu_s, beta_s, Winv_s, chi2, offd, zmu):
                              _p(zmu), _p(mu), _p(Lam)) != 0:
         return None
     return mu, Lam
+
+
+# ---- tensor ALS (time bins) -----------------------------------------------------------------
+
+def tensor_rows(ptr, idx1, idx2, val, F1, F2, lam, X_prev, threads=0):
+    """One mode's half-sweep of tensor ALS: the ALS update with fixed vectors
+    F1[idx1] * F2[idx2] (elementwise). Returns (X, flags)."""
+    ptr, idx1, idx2, val = _i64(ptr), _i32(idx1), _i32(idx2), _f64(val)
+    F1, F2 = _f64(F1), _f64(F2)
+    if F1.shape[1] != F2.shape[1]:
+        raise ValueError("F1 and F2 differ in width")
+    if idx1.size and (idx1.min() < 0 or idx1.max() >= F1.shape[0] or idx2.min() < 0
+                      or idx2.max() >= F2.shape[0]):
+        raise ValueError("index out of range")
+    X = np.array(X_prev, dtype=np.float64, order="C", copy=True)
+    n_rows = ptr.size - 1
+    D = F1.shape[1]
+    assert X.shape == (n_rows, D)
+    flags = np.empty(n_rows, dtype=np.int8)
+    _load().orc_tensor_rows(n_rows, _p(ptr), _p(idx1), _p(idx2), _p(val), D, _p(F1), _p(F2),
+                            float(lam), _p(X), _p(flags), int(threads))
+    return X, flags
+
+
+def tensor_sse(ptr, idx1, idx2, val, X, F1, F2, threads=0):
+    ptr, idx1, idx2, val = _i64(ptr), _i32(idx1), _i32(idx2), _f64(val)
+    X, F1, F2 = _f64(X), _f64(F1), _f64(F2)
+    return _load().orc_tensor_sse(ptr.size - 1, _p(ptr), _p(idx1), _p(idx2), _p(val), X.shape[1],
+                                  _p(X), _p(F1), _p(F2), int(threads))
+
+
+def _group_by(keys, n_keys, *payload):
+    """Stable counting sort of the ratings by key: (ptr, payload arrays reordered)."""
+    keys = np.asarray(keys, dtype=np.int64)
+    order = np.argsort(keys, kind="stable")
+    ptr = np.zeros(n_keys + 1, dtype=np.int64)
+    np.add.at(ptr, keys + 1, 1)
+    return (np.cumsum(ptr),) + tuple(np.asarray(a)[order] for a in payload)
+
+
+class TensorTrajectory:
+    """Free-running fp64 tensor ALS over (user, item, time bin) ratings; one sweep solves
+    the items, then the users, then the time bins (each with the other two fixed)."""
+
+    def __init__(self, M, N, n_bins, row_ptr, col, bins, val, U0, V0, T0, lam, threads=0):
+        row_ptr, col, bins, val = _i64(row_ptr), _i32(col), _i32(bins), _f64(val)
+        users = np.repeat(np.arange(M, dtype=np.int32), np.diff(row_ptr))
+        self.by_user = (row_ptr, col, bins, val)
+        ip, iu, ib, iv = _group_by(col, N, users, bins, val)
+        self.by_item = (ip, _i32(iu), _i32(ib), iv)
+        tp, tu, ti, tv = _group_by(bins, n_bins, users, col, val)
+        self.by_bin = (tp, _i32(tu), _i32(ti), tv)
+        self.U, self.V, self.T = _f64(U0).copy(), _f64(V0).copy(), _f64(T0).copy()
+        self.lam = float(lam)
+        self.threads = threads
+        self.nnz = int(row_ptr[-1])
+
+    def step(self, mode):
+        if mode == "items":
+            p, i1, i2, v = self.by_item
+            self.V, fl = tensor_rows(p, i1, i2, v, self.U, self.T, self.lam, self.V, self.threads)
+        elif mode == "users":
+            p, i1, i2, v = self.by_user
+            self.U, fl = tensor_rows(p, i1, i2, v, self.V, self.T, self.lam, self.U, self.threads)
+        else:
+            p, i1, i2, v = self.by_bin
+            self.T, fl = tensor_rows(p, i1, i2, v, self.U, self.V, self.lam, self.T, self.threads)
+        self.nflag = int((fl == 1).sum())
+        return self
+
+    def sweep(self):
+        return self.step("items").step("users").step("bins")
+
+    def rmse(self):
+        p, i1, i2, v = self.by_user
+        return float(np.sqrt(tensor_sse(p, i1, i2, v, self.U, self.V, self.T, self.threads)
+                             / self.nnz)) if self.nnz else 0.0

@@ -41,6 +41,12 @@
  * The standard normal, chi-square and normal variates are inputs, so a draw is a
  * deterministic function of them.
  *
+ * Tensor ALS (Sec. 2.2: the ALS model extended to the tensor case with the rating's time;
+ * the data carry time bins, Sec. 1): each rating has a time bin t, the prediction is the
+ * three-way product sum_d U_ud V_id T_td, and the update of one mode is the ALS update
+ * whose fixed vectors are the elementwise products of the other two modes' rows
+ * (orc_tensor_rows: f = F1[idx1] * F2[idx2]), with the same regulariser lambda n_s.
+ *
  * Everything is double precision, sequential within a row, rows in parallel
  * (OpenMP). Reductions over rows are done in row order from per-row values,
  * so every result is independent of the thread count.
@@ -453,4 +459,70 @@ int orc_nw_sample(int32_t D, const double *mu_s, double beta_s, const double *Wi
   }
   free(R); free(W); free(Fm); free(FB); free(col); free(tmp);
   return st;
+}
+
+/* ---- tensor ALS ------------------------------------------------------------------------ */
+
+/* One mode's half-sweep of tensor ALS: for every row s, the ALS update (solve_one) with the
+ * fixed vectors f_k = F1[idx1[k]] * F2[idx2[k]] (elementwise) of its ratings. Rows with no
+ * ratings and flagged rows keep their previous X; flags as orc_half_sweep. */
+int64_t orc_tensor_rows(int64_t n_rows, const int64_t *ptr, const int32_t *idx1,
+                        const int32_t *idx2, const double *val, int32_t D, const double *F1,
+                        const double *F2, double lambda, double *X, int8_t *flags, int nthreads) {
+  set_threads(nthreads);
+  int64_t maxdeg = 0;
+  for (int64_t s = 0; s < n_rows; ++s) {
+    if (ptr[s + 1] - ptr[s] > maxdeg) maxdeg = ptr[s + 1] - ptr[s];
+  }
+  int64_t nflag = 0;
+#pragma omp parallel reduction(+ : nflag)
+  {
+    double *A = (double *)malloc(sizeof(double) * D * D);
+    double *W = (double *)malloc(sizeof(double) * D * D);
+    double *b = (double *)malloc(sizeof(double) * D);
+    double *xs = (double *)malloc(sizeof(double) * D);
+    double *Fs = (double *)malloc(sizeof(double) * D * (maxdeg > 0 ? maxdeg : 1));
+    int32_t *seq = (int32_t *)malloc(sizeof(int32_t) * (maxdeg > 0 ? maxdeg : 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t s = 0; s < n_rows; ++s) {
+      const int64_t n = ptr[s + 1] - ptr[s];
+      for (int64_t q = 0; q < n; ++q) {
+        const double *f1 = F1 + (int64_t)idx1[ptr[s] + q] * D;
+        const double *f2 = F2 + (int64_t)idx2[ptr[s] + q] * D;
+        for (int32_t a = 0; a < D; ++a) Fs[q * D + a] = f1[a] * f2[a];
+        seq[q] = (int32_t)q;
+      }
+      int st = solve_one(D, n, seq, val + ptr[s], NULL, Fs, lambda, A, b, W, xs, X + s * D);
+      if (flags) flags[s] = (int8_t)st;
+      nflag += (st == 1);
+    }
+    free(A); free(W); free(b); free(xs); free(Fs); free(seq);
+  }
+  return nflag;
+}
+
+/* Sum over the rows' ratings of (r - sum_d X[s][d] F1[idx1][d] F2[idx2][d])^2, per row in
+ * rating order and over rows in row order. */
+double orc_tensor_sse(int64_t n_rows, const int64_t *ptr, const int32_t *idx1, const int32_t *idx2,
+                      const double *val, int32_t D, const double *X, const double *F1,
+                      const double *F2, int nthreads) {
+  set_threads(nthreads);
+  double *per = (double *)malloc(sizeof(double) * (n_rows > 0 ? n_rows : 1));
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int64_t s = 0; s < n_rows; ++s) {
+    double acc = 0.0;
+    for (int64_t p = ptr[s]; p < ptr[s + 1]; ++p) {
+      const double *f1 = F1 + (int64_t)idx1[p] * D;
+      const double *f2 = F2 + (int64_t)idx2[p] * D;
+      double pred = 0.0;
+      for (int32_t a = 0; a < D; ++a) pred += X[s * D + a] * f1[a] * f2[a];
+      const double e = val[p] - pred;
+      acc += e * e;
+    }
+    per[s] = acc;
+  }
+  double total = 0.0;
+  for (int64_t s = 0; s < n_rows; ++s) total += per[s];
+  free(per);
+  return total;
 }

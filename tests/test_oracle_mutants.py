@@ -12,6 +12,7 @@ from tests import test_oracle_pins as pins
 from tests import test_oracle_weighted_pins as wpins
 from tests import test_oracle_predict_pins as qpins
 from tests import test_oracle_bayes_pins as bpins
+from tests import test_oracle_tensor_pins as tpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
 
@@ -57,12 +58,23 @@ MUTANTS = [
     ("nw_bartlett_diagonal_not_rooted", "const double b = m == e ? sqrt(chi2[e]) :",
      "const double b = m == e ? chi2[e] :"),
     ("nw_mean_noise_wrong_solve", "solve_lower_t(D, R, zmu, tmp);", "solve_lower(D, R, zmu, tmp);"),
+    ("tensor_product_dropped", "for (int32_t a = 0; a < D; ++a) Fs[q * D + a] = f1[a] * f2[a];",
+     "for (int32_t a = 0; a < D; ++a) Fs[q * D + a] = f1[a];"),
+    ("tensor_second_index_wrong", "const double *f2 = F2 + (int64_t)idx2[ptr[s] + q] * D;",
+     "const double *f2 = F2 + (int64_t)idx2[ptr[s]] * D;"),
+    ("tensor_sse_without_time", "for (int32_t a = 0; a < D; ++a) pred += X[s * D + a] * f1[a] * f2[a];",
+     "for (int32_t a = 0; a < D; ++a) pred += X[s * D + a] * f1[a];"),
     ("pair_error_sign", "const double e = r[p] - pred[p];", "const double e = r[p] + pred[p];"),
     ("pair_sse_first_dropped", "for (int64_t p = 0; p < n; ++p) {\n    const double e",
      "for (int64_t p = 1; p < n; ++p) {\n    const double e"),
 ]
 
 PIN_TESTS = [
+    tpins.test_t1_unit_time_factors_give_matrix_als,
+    lambda: tpins.test_t2_matches_least_squares_on_the_product_design(3),
+    tpins.test_t3_objective_gradient_vanishes_after_each_mode,
+    tpins.test_t4_objective_never_increases,
+    tpins.test_t6_unit_time_factors_give_the_training_sse,
     lambda: bpins.test_b1_zero_noise_isotropic_prior_is_ridge(3),
     bpins.test_b2_zero_noise_is_the_posterior_mode,
     bpins.test_b3_noise_has_the_conditional_covariance,

@@ -346,6 +346,29 @@ def weight_seed(k: int) -> int:
     return data_seed(k) + 2000
 
 
+# Time bins of the paper's data set (Sec. 1): the ratings span 6649 bins.
+N_TIME_BINS = 6649
+
+
+def time_seed(k: int) -> int:
+    """Seed of the time-bin stream of config k."""
+    return data_seed(k) + 4000
+
+
+def time_bins(row_ptr: np.ndarray, n_bins: int, seed: int, spread: float = 300.0) -> np.ndarray:
+    """Seeded time bin of every rating (int32, CSR order): user u becomes active at a bin
+    s_u drawn uniformly, and each of its ratings falls s_u + floor(E) bins later, E
+    exponential with mean ``spread``, clipped to the last bin. The data set's own time
+    stamps are not available; this gives every user a contiguous active period."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    M = row_ptr.size - 1
+    rng = np.random.default_rng(seed)
+    start = rng.integers(0, n_bins, size=M)
+    off = rng.standard_exponential(int(row_ptr[-1]), dtype=np.float32) * np.float32(spread)
+    bins = np.repeat(start, np.diff(row_ptr)) + off.astype(np.int64)
+    return np.minimum(bins, n_bins - 1).astype(np.int32)
+
+
 def holdout_seed(k: int) -> int:
     """Seed of the held-out selection of config k."""
     return data_seed(k) + 3000
