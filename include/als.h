@@ -58,6 +58,12 @@ typedef enum {
   ALS_ROWS_ITEMS = 1  /* solve V (rows of the CSC) with U fixed */
 } als_side;
 
+typedef enum {
+  ALS_MODE_USERS = 0, /* tensor ALS: solve U with V and T fixed */
+  ALS_MODE_ITEMS = 1, /* solve V with U and T fixed */
+  ALS_MODE_TIME = 2   /* solve T (one row per time bin) with U and V fixed */
+} als_mode;
+
 /* Tunables of the degree-bucketed schedule. Zero fields select defaults. */
 typedef struct {
   int32_t hub_threshold;   /* rows with more ratings are split into chunks (default 8192) */
@@ -276,6 +282,38 @@ als_status als_sample_hyper(als_ctx *ctx, als_side side, const float *X, const d
 als_status als_gibbs_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factors,
                                 float alpha, const double *Lambda, const double *mu,
                                 const float *z, float *out_factors, double *rmse_out);
+
+/*
+ * Tensor ALS (paper Sec. 2.2: the ALS model extended to the tensor case, with the time of
+ * each rating; the data's ratings fall into time bins, Sec. 1). Every rating gets a time
+ * bin t; the prediction is sum_d U[u][d] V[i][d] T[t][d] with T [n_bins x D] row-major fp32.
+ * A mode's half-sweep is the ALS update of that mode's rows, whose fixed vectors are the
+ * elementwise products of the other two modes' rows (V[i] * T[t] for a user, U[u] * T[t]
+ * for an item, U[u] * V[i] for a time bin), with the same regulariser lambda * n_s.
+ *
+ * als_set_time_bins: bins = host int32[nnz], the time bin of every rating in CSR order
+ * (the order of col_idx at create), each in [0, n_bins). The library keeps them on the
+ * device in user, item and time-bin order (the last built by a stable counting sort on
+ * the host, about 13 bytes per rating of host memory while it runs) and schedules the
+ * time-bin rows like the other sides. Replaces an earlier set; ALS_ERR_INVALID_ARG for a
+ * bin out of range (nothing changes). Synchronises the stream.
+ */
+als_status als_set_time_bins(als_ctx *ctx, int32_t n_bins, const int32_t *bins);
+
+/*
+ * One mode's half-sweep of tensor ALS: the rows of the mode's factor (U, V or T, device fp32,
+ * 16-byte aligned, pairwise non-overlapping) are overwritten with their regularised
+ * least-squares solutions given the other two (rows without ratings and flagged rows keep
+ * their values). The gather of the same pass yields the squared residuals of the entering
+ * state (als_last_rmse_in); rmse_out (host, nullable) as for als_half_sweep, over the
+ * three-way predictions. ALS_ERR_INVALID_ARG without time bins or with weights attached.
+ */
+als_status als_tensor_half_sweep(als_ctx *ctx, als_mode mode, float *U, float *V, float *T,
+                                 float lambda, double *rmse_out);
+
+/* Training RMSE of the three-way predictions over all stored ratings; synchronises. */
+als_status als_tensor_rmse(als_ctx *ctx, const float *U, const float *V, const float *T,
+                           double *rmse_out);
 
 void als_destroy(als_ctx *ctx);
 

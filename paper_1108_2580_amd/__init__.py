@@ -18,6 +18,9 @@ LIB_PATH = os.path.join(_HERE, "libals.so")
 ALS_OK, ALS_ERR_INVALID_ARG, ALS_ERR_BAD_MATRIX, ALS_ERR_OUT_OF_MEMORY, ALS_ERR_HIP, \
     ALS_ERR_NOT_SPD = range(6)
 ALS_ROWS_USERS, ALS_ROWS_ITEMS = 0, 1
+ALS_MODE_USERS, ALS_MODE_ITEMS, ALS_MODE_TIME = 0, 1, 2
+_MODES = {"users": ALS_MODE_USERS, "items": ALS_MODE_ITEMS, "bins": ALS_MODE_TIME,
+          "time": ALS_MODE_TIME}
 _SIDES = {"users": ALS_ROWS_USERS, "items": ALS_ROWS_ITEMS,
           ALS_ROWS_USERS: ALS_ROWS_USERS, ALS_ROWS_ITEMS: ALS_ROWS_ITEMS}
 
@@ -26,6 +29,7 @@ EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_weights",
            "als_set_phase_timing", "als_get_phase_cycles", "als_predict", "als_set_holdout",
            "als_holdout_rmse", "als_set_nw_prior", "als_sample_hyper", "als_gibbs_half_sweep",
+           "als_set_time_bins", "als_tensor_half_sweep", "als_tensor_rmse",
            "als_destroy", "als_status_str", "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
@@ -90,6 +94,12 @@ def _load_library(path=LIB_PATH):
     lib.als_gibbs_half_sweep.argtypes = [P, st, P, f32, P, P, P, P,
                                          ctypes.POINTER(ctypes.c_double)]
     lib.als_gibbs_half_sweep.restype = st
+    lib.als_set_time_bins.argtypes = [P, i32, P]
+    lib.als_set_time_bins.restype = st
+    lib.als_tensor_half_sweep.argtypes = [P, st, P, P, P, f32, ctypes.POINTER(ctypes.c_double)]
+    lib.als_tensor_half_sweep.restype = st
+    lib.als_tensor_rmse.argtypes = [P, P, P, P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_tensor_rmse.restype = st
     lib.als_destroy.argtypes = [P]
     lib.als_destroy.restype = None
     lib.als_status_str.argtypes = [st]
@@ -333,6 +343,38 @@ class ALS:
             return r.value
         self._check(s)
         return r.value if rmse else None
+
+    # ---- tensor ALS over time bins ---------------------------------------------------------
+
+    def set_time_bins(self, n_bins, bins):
+        """Time bin of every rating (host int array, CSR order), each in [0, n_bins)."""
+        b = np.ascontiguousarray(bins, dtype=np.int32)
+        if b.shape != (self.nnz,):
+            raise ValueError(f"bins have shape {b.shape}, expected ({self.nnz},)")
+        self._check(lib.als_set_time_bins(self._h, int(n_bins), _np_ptr(b)))
+        self.n_bins = int(n_bins)
+
+    def tensor_half_sweep(self, mode, U, V, T, lam, rmse=False, allow_flagged=False):
+        """Solve the rows of ``mode`` ("users", "items" or "bins") in place given the other
+        two factors."""
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        tp = _dev_ptr(T, self.D, getattr(self, "n_bins", 0), "T")
+        r = ctypes.c_double(0.0)
+        s = lib.als_tensor_half_sweep(self._h, _MODES[mode], up, vp, tp, float(lam),
+                                      ctypes.byref(r) if rmse else None)
+        if s == ALS_ERR_NOT_SPD and allow_flagged:
+            return r.value
+        self._check(s)
+        return r.value if rmse else None
+
+    def tensor_rmse(self, U, V, T):
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        tp = _dev_ptr(T, self.D, getattr(self, "n_bins", 0), "T")
+        r = ctypes.c_double(0.0)
+        self._check(lib.als_tensor_rmse(self._h, up, vp, tp, ctypes.byref(r)))
+        return r.value
 
     def close(self):
         if getattr(self, "_h", None):

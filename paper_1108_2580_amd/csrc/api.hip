@@ -81,7 +81,7 @@ struct als_ctx {
   uint8_t *d_val_t = nullptr;
   float *d_w = nullptr;    // weighted ALS: per-rating weights in CSR order (null: plain ALS)
   float *d_w_t = nullptr;  // the same weights in CSC order
-  SidePlan plan[2];
+  SidePlan plan[3];  // users, items, and (tensor ALS) time bins
   float *d_ws = nullptr;
   size_t ws_bytes = 0;
   float *d_fpad = nullptr;       // staged fixed side [(max(M, N) + 1) x DP], last row zero
@@ -115,6 +115,15 @@ struct als_ctx {
   double *d_hold_blocks = nullptr; // per-block squared errors
   double *d_hold_partials = nullptr;
   double *d_hold_sse = nullptr;
+  // tensor ALS over time bins (als_set_time_bins)
+  int32_t n_bins = 0;
+  int32_t *d_tbin = nullptr;       // time bin of every rating, CSR order
+  int32_t *d_tbin_t = nullptr;     // the same in CSC order
+  std::vector<int64_t> h_tb_ptr;   // ratings grouped by time bin
+  int64_t *d_tb_ptr = nullptr;
+  int32_t *d_tb_user = nullptr, *d_tb_item = nullptr;
+  uint8_t *d_tb_val = nullptr;
+  float *d_fpad2 = nullptr;        // second staged table [(max(M, N, bins) + 1) x DP]
   // Bayesian Gibbs step (allocated on first use)
   float *d_prior_init = nullptr;   // prior image of the row kernels
   float *d_prior_K = nullptr;      // Cholesky factor of the prior precision (rows without ratings)
@@ -341,6 +350,13 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_cyc);
   dfree(c->d_cyc_sum);
   free_holdout(c);
+  dfree(c->d_tbin);
+  dfree(c->d_tbin_t);
+  dfree(c->d_tb_ptr);
+  dfree(c->d_tb_user);
+  dfree(c->d_tb_item);
+  dfree(c->d_tb_val);
+  dfree(c->d_fpad2);
   dfree(c->d_prior_init);
   dfree(c->d_prior_K);
   dfree(c->d_prior_mu32);
@@ -415,12 +431,12 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 // New-state residual pass over a side's pieces + fixed-order reduction into
 // d_sse_total; the fixed side must already be staged in d_fpad.
 als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, const uint8_t *val,
-                         const float *X) {
+                         const float *X, const als::Hadamard &hd = als::Hadamard{}) {
   const int64_t n = (int64_t)P.gitems.size();
   {
     PhaseTimer t(c, 3);
     HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_gitems, n, idx, val, c->d_fpad, X, c->D,
-                                     c->d_sse_items, c->stream));
+                                     c->d_sse_items, hd, c->stream));
   }
   {
     PhaseTimer t(c, 4);
@@ -613,6 +629,21 @@ namespace {
 
 // The half-sweep of both methods: the ALS update (pr.init == nullptr, lambda used) or the
 // Gibbs draw (pr: the prior image, the variates and their scale; lambda unused).
+// What a half-sweep reads: the plan (0 users, 1 items, 2 time bins), the side's index,
+// rating and weight arrays, the rows of the staged table (its zero row) and, for tensor
+// ALS, the second index and staged table.
+struct SweepSpec {
+  int plan = 0;
+  const int32_t *idx = nullptr;
+  const uint8_t *val = nullptr;
+  const float *wts = nullptr;
+  int64_t n_fixed = 0;
+  als::Hadamard hd;
+};
+
+als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out_factors,
+                     double *rmse_out, const als::RowPrior &pr);
+
 als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_factors, float lambda,
                            float *out_factors, double *rmse_out, const als::RowPrior &pr) {
   if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
@@ -629,16 +660,33 @@ als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_facto
               sizeof(float) * n_rows * ctx->D))
     return fail(ctx, ALS_ERR_INVALID_ARG, "out_factors overlaps fixed_factors");
   DeviceGuard g(ctx->device);
-  const SidePlan &P = ctx->plan[side];
-  const int32_t *idx = users ? ctx->d_col : ctx->d_row_idx;
-  const uint8_t *val = users ? ctx->d_val : ctx->d_val_t;
-  const float *wts = users ? ctx->d_w : ctx->d_w_t;
-  HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
+  SweepSpec sp;
+  sp.plan = side;
+  sp.idx = users ? ctx->d_col : ctx->d_row_idx;
+  sp.val = users ? ctx->d_val : ctx->d_val_t;
+  sp.wts = users ? ctx->d_w : ctx->d_w_t;
+  sp.n_fixed = n_fixed;
   {
     PhaseTimer t(ctx, 0);
     HIP_OR_FAIL(ctx, als::launch_stage_fixed(fixed_factors, n_fixed, ctx->D, ctx->DP,
                                              ctx->d_fpad, ctx->stream));
   }
+  return run_sweep(ctx, sp, lambda, out_factors, rmse_out, pr);
+}
+
+// The batches of one half-sweep on an already staged fixed side (d_fpad, and d_fpad2 for
+// tensor ALS), the entering-state reduction, the flag count and, on request, the
+// new-state RMSE.
+als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out_factors,
+                     double *rmse_out, const als::RowPrior &pr) {
+  const SidePlan &P = ctx->plan[sp.plan];
+  const int32_t *idx = sp.idx;
+  const uint8_t *val = sp.val;
+  const float *wts = sp.wts;
+  const int64_t n_fixed = sp.n_fixed;
+  const als::Hadamard &hd = sp.hd;
+  const int side = sp.plan;
+  HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
   for (const Batch &b : P.batches) {
     double *sse = ctx->d_sse_items + b.gitem_off;
     if (ctx->lane_solve) {
@@ -646,7 +694,7 @@ als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_facto
         PhaseTimer t(ctx, 1);
         HIP_OR_FAIL(ctx, als::launch_gram_ne(ctx->D, P.d_gitems + b.gitem_off, b.n_gitems,
                                              b.n_gchunks, idx, val, wts, ctx->d_fpad, n_fixed,
-                                             out_factors, ctx->d_ws, ctx->d_ne, sse,
+                                             out_factors, ctx->d_ws, ctx->d_ne, sse, hd,
                                              ctx->stream));
       }
       {
@@ -660,16 +708,17 @@ als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_facto
         PhaseTimer t(ctx, 1);
         HIP_OR_FAIL(ctx, als::launch_gram_chunks(ctx->DP, P.d_gitems + b.gitem_off, b.n_gchunks,
                                                  idx, val, wts, ctx->d_fpad, n_fixed, out_factors,
-                                                 ctx->D, ctx->d_ws, sse, ctx->stream));
+                                                 ctx->D, ctx->d_ws, sse, hd, ctx->stream));
       }
       {
         PhaseTimer t(ctx, 2);
-        double *cg = ctx->phase_timing ? ctx->d_cyc + b.row_off : nullptr;
-        double *cs = ctx->phase_timing ? ctx->d_cyc + ctx->cyc_cap + b.row_off : nullptr;
+        const bool clocks = ctx->phase_timing && side < 2;  // the clocks cover users and items
+        double *cg = clocks ? ctx->d_cyc + b.row_off : nullptr;
+        double *cs = clocks ? ctx->d_cyc + ctx->cyc_cap + b.row_off : nullptr;
         HIP_OR_FAIL(ctx, als::launch_rows(ctx->DP, P.d_rows + b.row_off, b.n_rows, idx, val, wts,
                                           ctx->d_fpad, n_fixed, ctx->d_ws, ctx->D, lambda,
                                           out_factors, ctx->d_sse_items, ctx->d_flag, cg, cs,
-                                          pr, ctx->stream));
+                                          pr, hd, ctx->stream));
       }
     }
   }
@@ -689,7 +738,7 @@ als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_facto
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, ctx->stream));
   ctx->last_side = side;
-  if (ctx->phase_timing && !ctx->lane_solve && !P.rows.empty()) {
+  if (ctx->phase_timing && !ctx->lane_solve && !P.rows.empty() && side < 2) {
     const int64_t nr = (int64_t)P.rows.size();
     HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_cyc, nr, ctx->d_partials, ctx->d_cyc_sum,
                                         ctx->stream));
@@ -702,7 +751,7 @@ als_status half_sweep_impl(als_ctx *ctx, als_side side, const float *fixed_facto
     ctx->cyc[side][1] += ctx->h_cyc_sum[1];
   }
   if (rmse_out) {
-    als_status st = residual_pass(ctx, P, idx, val, out_factors);
+    als_status st = residual_pass(ctx, P, idx, val, out_factors, hd);
     if (st != ALS_OK) return st;
     HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                     hipMemcpyDeviceToHost, ctx->stream));
@@ -1005,6 +1054,206 @@ als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles
   if (!gram_cycles || !solve_cycles) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
   *gram_cycles = ctx->cyc[side][0];
   *solve_cycles = ctx->cyc[side][1];
+  return ALS_OK;
+}
+
+// ---- tensor ALS over time bins ----------------------------------------------------------
+
+als_status als_set_time_bins(als_ctx *ctx, int32_t n_bins, const int32_t *bins) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (n_bins < 1) return fail(ctx, ALS_ERR_INVALID_ARG, "n_bins must be >= 1");
+  if ((int64_t)(n_bins + 1) * ctx->DP * 4 > als::kMaxStagedBytes)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "too many time bins for the staged-table limit");
+  if (ctx->nnz > 0 && !bins) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL bins");
+  for (int64_t p = 0; p < ctx->nnz; ++p) {
+    if (bins[p] < 0 || bins[p] >= n_bins)
+      return fail(ctx, ALS_ERR_INVALID_ARG, "time bin %d of rating %lld outside [0, %d)",
+                  bins[p], (long long)p, n_bins);
+  }
+  DeviceGuard g(ctx->device);
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  dfree(ctx->d_tbin);
+  dfree(ctx->d_tbin_t);
+  dfree(ctx->d_tb_ptr);
+  dfree(ctx->d_tb_user);
+  dfree(ctx->d_tb_item);
+  dfree(ctx->d_tb_val);
+  dfree(ctx->d_fpad2);
+  SidePlan &TP = ctx->plan[2];
+  dfree(TP.d_gitems);
+  dfree(TP.d_rows);
+  dfree(TP.d_zero_rows);
+  TP = SidePlan();
+  ctx->n_bins = 0;
+  const int64_t nnz = ctx->nnz, M = ctx->M;
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tbin, nnz));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tbin_t, nnz));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tb_ptr, (int64_t)n_bins + 1));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tb_user, nnz));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tb_item, nnz));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_tb_val, nnz));
+  HIP_OR_FAIL(ctx, dalloc(&ctx->d_fpad2,
+                          (std::max({ctx->M, ctx->N, (int64_t)n_bins}) + 1) * (int64_t)ctx->DP));
+  // ratings grouped by time bin: a stable counting sort on the host (users ascending, then
+  // the CSR order within a user), so the layout is the same on every run
+  std::vector<int32_t> col(nnz);
+  std::vector<uint8_t> val(nnz);
+  if (nnz > 0) {
+    HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_tbin, bins, sizeof(int32_t) * nnz, hipMemcpyHostToDevice));
+    HIP_OR_FAIL(ctx, hipMemcpy(col.data(), ctx->d_col, sizeof(int32_t) * nnz,
+                               hipMemcpyDeviceToHost));
+    HIP_OR_FAIL(ctx, hipMemcpy(val.data(), ctx->d_val, nnz, hipMemcpyDeviceToHost));
+  }
+  std::vector<int64_t> &ptr = ctx->h_tb_ptr;
+  ptr.assign((size_t)n_bins + 1, 0);
+  for (int64_t p = 0; p < nnz; ++p) ptr[bins[p] + 1] += 1;
+  for (int32_t t = 0; t < n_bins; ++t) ptr[t + 1] += ptr[t];
+  {
+    std::vector<int64_t> next(ptr.begin(), ptr.end() - 1);
+    std::vector<int32_t> tu(nnz), ti(nnz);
+    std::vector<uint8_t> tv(nnz);
+    for (int64_t u = 0; u < M; ++u) {
+      for (int64_t p = ctx->h_row_ptr[u]; p < ctx->h_row_ptr[u + 1]; ++p) {
+        const int64_t q = next[bins[p]]++;
+        tu[q] = (int32_t)u;
+        ti[q] = col[p];
+        tv[q] = val[p];
+      }
+    }
+    HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_tb_ptr, ptr.data(), sizeof(int64_t) * ptr.size(),
+                               hipMemcpyHostToDevice));
+    if (nnz > 0) {
+      HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_tb_user, tu.data(), sizeof(int32_t) * nnz,
+                                 hipMemcpyHostToDevice));
+      HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_tb_item, ti.data(), sizeof(int32_t) * nnz,
+                                 hipMemcpyHostToDevice));
+      HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_tb_val, tv.data(), nnz, hipMemcpyHostToDevice));
+    }
+  }
+  // the bins in CSC (item) order, through the transpose's own permutation (columns are
+  // distinct within a row, so the positions are those of the CSC build)
+  if (nnz > 0) {
+    int64_t rows_per_blk = 0, nblk = 0;
+    csc_blocking(ctx->M, ctx->N, rows_per_blk, nblk);
+    int32_t *cnt = nullptr;
+    int64_t *tot = nullptr;
+    hipError_t e = dalloc(&cnt, nblk * ctx->N);
+    if (e == hipSuccess) e = dalloc(&tot, ctx->N);
+    if (e == hipSuccess)
+      e = als::launch_csc_permute_f32(ctx->d_row_ptr, ctx->d_col,
+                                      reinterpret_cast<const float *>(ctx->d_tbin), ctx->M,
+                                      ctx->N, rows_per_blk, nblk, cnt, tot, ctx->d_col_ptr,
+                                      reinterpret_cast<float *>(ctx->d_tbin_t), ctx->stream);
+    const hipError_t e2 = hipStreamSynchronize(ctx->stream);
+    dfree(cnt);
+    dfree(tot);
+    HIP_OR_FAIL(ctx, e);
+    HIP_OR_FAIL(ctx, e2);
+  }
+  als_status st = build_plan(ctx, TP, ptr);
+  if (st != ALS_OK) return st;
+  // shared buffers sized for the third plan too
+  int64_t max_slots = 0, max_sse = 0, max_rows = 0;
+  for (auto &P : ctx->plan) {
+    max_slots = std::max(max_slots, P.max_slots);
+    max_sse = std::max(max_sse, (int64_t)P.gitems.size());
+    max_rows = std::max(max_rows, (int64_t)P.rows.size());
+  }
+  if ((size_t)max_slots * slot_bytes_of(ctx) > ctx->ws_bytes) {
+    dfree(ctx->d_ws);
+    ctx->ws_bytes = (size_t)max_slots * slot_bytes_of(ctx);
+    HIP_OR_FAIL(ctx, dalloc(&ctx->d_ws, (int64_t)(ctx->ws_bytes / sizeof(float))));
+  }
+  if (ctx->lane_solve && (int64_t)TP.rows.size() > 0) {
+    // records: one per row of the largest plan (already sized at create for users/items)
+    const int64_t have = std::max((int64_t)ctx->plan[0].rows.size(),
+                                  (int64_t)ctx->plan[1].rows.size());
+    if (max_rows > have) {
+      dfree(ctx->d_ne);
+      HIP_OR_FAIL(ctx, dalloc(&ctx->d_ne, max_rows * (int64_t)als::ne_floats(als::lane_width(ctx->D))));
+    }
+  }
+  const int64_t had_sse = std::max((int64_t)ctx->plan[0].gitems.size(),
+                                   (int64_t)ctx->plan[1].gitems.size());
+  if (max_sse > had_sse) {
+    dfree(ctx->d_sse_items);
+    dfree(ctx->d_partials);
+    HIP_OR_FAIL(ctx, dalloc(&ctx->d_sse_items, max_sse));
+    HIP_OR_FAIL(ctx, dalloc(&ctx->d_partials, als::reduce_partials(max_sse)));
+  }
+  ctx->n_bins = n_bins;
+  return ALS_OK;
+}
+
+als_status als_tensor_half_sweep(als_ctx *ctx, als_mode mode, float *U, float *V, float *T,
+                                 float lambda, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (ctx->n_bins <= 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no time bins set");
+  if (mode != ALS_MODE_USERS && mode != ALS_MODE_ITEMS && mode != ALS_MODE_TIME)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "mode %d is not a tensor mode", (int)mode);
+  if (!U || !V || !T) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL factor buffer");
+  if (!std::isfinite(lambda) || lambda < 0.f)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15) || ((uintptr_t)T & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  if (ctx->d_w) return fail(ctx, ALS_ERR_INVALID_ARG, "tensor ALS takes no rating weights; detach them");
+  const size_t bu = sizeof(float) * ctx->M * ctx->D, bv = sizeof(float) * ctx->N * ctx->D;
+  const size_t bt = sizeof(float) * (size_t)ctx->n_bins * ctx->D;
+  if (overlap(U, bu, V, bv) || overlap(U, bu, T, bt) || overlap(V, bv, T, bt))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "U, V and T must not overlap");
+  DeviceGuard g(ctx->device);
+  // the solved mode's fixed vectors are F1[idx] * F2[idx2]
+  const float *F1, *F2;
+  int64_t n1, n2;
+  float *out;
+  SweepSpec sp;
+  sp.plan = (int)mode;
+  if (mode == ALS_MODE_USERS) {
+    F1 = V; n1 = ctx->N; F2 = T; n2 = ctx->n_bins; out = U;
+    sp.idx = ctx->d_col; sp.val = ctx->d_val; sp.hd.idx2 = ctx->d_tbin;
+  } else if (mode == ALS_MODE_ITEMS) {
+    F1 = U; n1 = ctx->M; F2 = T; n2 = ctx->n_bins; out = V;
+    sp.idx = ctx->d_row_idx; sp.val = ctx->d_val_t; sp.hd.idx2 = ctx->d_tbin_t;
+  } else {
+    F1 = U; n1 = ctx->M; F2 = V; n2 = ctx->N; out = T;
+    sp.idx = ctx->d_tb_user; sp.val = ctx->d_tb_val; sp.hd.idx2 = ctx->d_tb_item;
+  }
+  sp.n_fixed = n1;
+  sp.hd.Tp = ctx->d_fpad2;
+  {
+    PhaseTimer t(ctx, 0);
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(F1, n1, ctx->D, ctx->DP, ctx->d_fpad, ctx->stream));
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(F2, n2, ctx->D, ctx->DP, ctx->d_fpad2, ctx->stream));
+  }
+  return run_sweep(ctx, sp, lambda, out, rmse_out, als::RowPrior{});
+}
+
+als_status als_tensor_rmse(als_ctx *ctx, const float *U, const float *V, const float *T,
+                           double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (ctx->n_bins <= 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no time bins set");
+  if (!U || !V || !T || !rmse_out) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15) || ((uintptr_t)T & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  DeviceGuard g(ctx->device);
+  {
+    PhaseTimer t(ctx, 0);
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(V, ctx->N, ctx->D, ctx->DP, ctx->d_fpad, ctx->stream));
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(T, ctx->n_bins, ctx->D, ctx->DP, ctx->d_fpad2,
+                                             ctx->stream));
+  }
+  als::Hadamard hd;
+  hd.idx2 = ctx->d_tbin;
+  hd.Tp = ctx->d_fpad2;
+  als_status st = residual_pass(ctx, ctx->plan[ALS_ROWS_USERS], ctx->d_col, ctx->d_val, U, hd);
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
+                                  hipMemcpyDeviceToHost, ctx->stream));
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
   return ALS_OK;
 }
 

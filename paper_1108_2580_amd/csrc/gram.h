@@ -104,33 +104,38 @@ __device__ __forceinline__ void unroll_blocks(F &f) {
 struct GroupStage {
   int32_t j[2][64];
   float r[2][64];
-  float w[2][64];  // per-rating weights (weighted ALS only)
+  float w[2][64];   // per-rating weights (weighted ALS only)
+  int32_t t[2][64]; // second index of each rating (tensor ALS only)
 };
 
-// One rating per lane of a 64-rating group: column index, rating and weight.
+// One rating per lane of a 64-rating group: column index, rating, weight and (tensor
+// ALS) the index into the second fixed table.
 struct GroupLanes {
   int j;
   float r;
   float w;
+  int t;
 };
 
 // Stage the group held one rating per lane (lane L holds rating L of the group).
-template <bool WT>
+template <bool WT, bool TS = false>
 __device__ __forceinline__ void stage_group(GroupStage &st, int buf, const GroupLanes &g) {
   const int lane = threadIdx.x & 63;
   const int at = (lane & 3) * 16 + (lane >> 2);
   st.j[buf][at] = g.j;
   st.r[buf][at] = g.r;
   if constexpr (WT) st.w[buf][at] = g.w;
+  if constexpr (TS) st.t[buf][at] = g.t;
 }
 
 // Rating `first + lane` of an item (n ratings): clamped loads, then the all-zero row,
-// rating 0 and weight 0 past the item's end.
-template <bool WT>
+// rating 0, weight 0 and second index 0 past the item's end.
+template <bool WT, bool TS = false>
 __device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip,
                                                   const uint8_t *__restrict__ vp,
-                                                  const float *__restrict__ wp, int n, int first,
-                                                  int zrow) {
+                                                  const float *__restrict__ wp,
+                                                  const int32_t *__restrict__ tp, int n,
+                                                  int first, int zrow) {
   const int k = first + (int)(threadIdx.x & 63);
   const int kc = min(k, n - 1);
   const int j = ip[kc];
@@ -143,6 +148,12 @@ __device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip
     g.w = k < n ? w : 0.f;
   } else {
     g.w = 1.f;
+  }
+  if constexpr (TS) {
+    const int t = tp[kc];
+    g.t = k < n ? t : 0;
+  } else {
+    g.t = 0;
   }
   return g;
 }
@@ -158,17 +169,21 @@ __device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip
 // With AUG, lane column aug_c of the last tile carries the rating instead of the
 // (zero) padded feature, so that the MFMA Gram also accumulates b = sum r f in that
 // column (and sum r^2 on its diagonal).
-template <int DP, int STEPS, bool AUG, bool WT>
+// With TS (tensor ALS) the fixed vector is the elementwise product of the rows of two
+// staged tables, Fp[j] * Tp[t] (t the rating's second index); the padding of Fp keeps
+// the product's padding zero.
+template <int DP, int STEPS, bool AUG, bool WT, bool TS = false>
 __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
                                              float (&wt)[STEPS], const GroupStage &st, int buf,
                                              int s0, const float *__restrict__ Fp,
-                                             bool aug_lane) {
+                                             const float *__restrict__ Tp, bool aug_lane) {
   constexpr int T = DP / 16;
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
   const int32_t *__restrict__ sj = &st.j[buf][kq * 16 + s0];
   const float *__restrict__ sr = &st.r[buf][kq * 16 + s0];
   const float *__restrict__ sw = &st.w[buf][kq * 16 + s0];
+  const int32_t *__restrict__ stt = &st.t[buf][kq * 16 + s0];
 #pragma unroll
   for (int u = 0; u < STEPS; ++u) {
     const int j = sj[u];
@@ -178,6 +193,12 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
     const char *row = reinterpret_cast<const char *>(Fp) + (uint64_t)off;
 #pragma unroll
     for (int X = 0; X < T; ++X) a[u][X] = *reinterpret_cast<const float *>(row + 64 * X);
+    if constexpr (TS) {
+      const uint32_t off2 = (uint32_t)stt[u] * (uint32_t)(DP * 4) + (uint32_t)(c * 4);
+      const char *row2 = reinterpret_cast<const char *>(Tp) + (uint64_t)off2;
+#pragma unroll
+      for (int X = 0; X < T; ++X) a[u][X] *= *reinterpret_cast<const float *>(row2 + 64 * X);
+    }
     if constexpr (AUG) a[u][T - 1] = aug_lane ? r[u] : a[u][T - 1];
   }
 }
@@ -276,14 +297,17 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStag
 //    the first block of the next group) is issued before the MFMAs of the current
 //    one, so that its latency hides behind them. The blocks of the last group that
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
-template <int DP, bool AUG, bool WT>
+// tp, Tp (tensor ALS, TS): the item's second indices and the second staged table.
+template <int DP, bool AUG, bool WT, bool TS = false>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
                                                 const float (&xo)[RowCfg<DP>::T], double &sse,
                                                 const int32_t *__restrict__ ip,
                                                 const uint8_t *__restrict__ vp,
-                                                const float *__restrict__ wp, int n,
-                                                const float *__restrict__ Fp, int zrow,
+                                                const float *__restrict__ wp,
+                                                const int32_t *__restrict__ tp, int n,
+                                                const float *__restrict__ Fp,
+                                                const float *__restrict__ Tp, int zrow,
                                                 int aug_c, GroupStage &st, GroupLanes gv) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
@@ -291,10 +315,10 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
   const bool aug_lane = (lane & 15) == aug_c;
   if constexpr (T <= 2) {
     for (int g = 0; g < n; g += 64) {
-      const GroupLanes gn = group_lanes<WT>(ip, vp, wp, n, g + 64, zrow);
+      const GroupLanes gn = group_lanes<WT, TS>(ip, vp, wp, tp, n, g + 64, zrow);
       const int steps = min(16, (n - g + 3) >> 2);
       __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
-      stage_group<WT>(st, 0, gv);
+      stage_group<WT, TS>(st, 0, gv);
       wave_sync();
       float pi[16];
 #pragma unroll
@@ -304,7 +328,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         if (s0 < steps) {
           float a[STEPS][T];
           float r[STEPS], w[STEPS];
-          gather_block<DP, STEPS, AUG, WT>(a, r, w, st, 0, s0, Fp, aug_lane);
+          gather_block<DP, STEPS, AUG, WT, TS>(a, r, w, st, 0, s0, Fp, Tp, aug_lane);
           mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a, r, w, s0, steps);
         }
       }
@@ -315,12 +339,12 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
   } else {
     static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
     float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS], w0[STEPS], w1[STEPS];
-    stage_group<WT>(st, 0, gv);
+    stage_group<WT, TS>(st, 0, gv);
     wave_sync();
-    gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, 0, 0, Fp, aug_lane);
+    gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, 0, 0, Fp, Tp, aug_lane);
     int buf = 0;
     for (int g = 0; g < n; g += 64) {
-      const GroupLanes gn = group_lanes<WT>(ip, vp, wp, n, g + 64, zrow);
+      const GroupLanes gn = group_lanes<WT, TS>(ip, vp, wp, tp, n, g + 64, zrow);
       const int steps = min(16, (n - g + 3) >> 2);
       __builtin_assume(steps >= 1);  // g < n: the group's first step always exists
       float pi[16];
@@ -331,16 +355,16 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         constexpr int s0 = b * STEPS;
         if constexpr (b % 2 == 0) {
           if constexpr (b + 1 < NB)
-            gather_block<DP, STEPS, AUG, WT>(a1, r1, w1, st, buf, s0 + STEPS, Fp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT, TS>(a1, r1, w1, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
           mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a0, r0, w0, s0, steps);
         } else {
           if constexpr (b + 1 < NB) {
-            gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, buf, s0 + STEPS, Fp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
           } else {
             // the next group goes to the other buffer, then its first block is gathered
-            stage_group<WT>(st, buf ^ 1, gn);
+            stage_group<WT, TS>(st, buf ^ 1, gn);
             wave_sync();
-            gather_block<DP, STEPS, AUG, WT>(a0, r0, w0, st, buf ^ 1, 0, Fp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf ^ 1, 0, Fp, Tp, aug_lane);
           }
           mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a1, r1, w1, s0, steps);
         }

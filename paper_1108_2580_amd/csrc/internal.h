@@ -53,6 +53,14 @@ struct RowPrior {
   float zscale = 0.f;           // 1 / sqrt(alpha)
 };
 
+// Tensor ALS: the second index of every rating (aligned with idx / val) and the second
+// staged table; a rating's fixed vector is the elementwise product Fp[idx] * Tp[idx2].
+// idx2 == nullptr: the matrix case.
+struct Hadamard {
+  const int32_t *idx2 = nullptr;
+  const float *Tp = nullptr;
+};
+
 // ---- launchers (each returns the launch's hipError_t) ----------------------------------
 
 // Column-major copy of a CSR matrix, built on the device (layout.hip).
@@ -82,7 +90,7 @@ hipError_t launch_stage_fixed(const float *F, int64_t n, int D, int DP, float *F
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
                               const uint8_t *val, const float *wts, const float *Fp,
                               int64_t n_fixed, const float *Xold, int D, float *ws, double *sse,
-                              hipStream_t s);
+                              const Hadamard &hd, hipStream_t s);
 
 // Fused per-row normal equations, regularisation, Cholesky and solves; X is read
 // (entering state) and overwritten in place (rowsolve.hip).
@@ -94,13 +102,14 @@ hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const in
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
                        const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
-                       double *cyc_gram, double *cyc_solve, const RowPrior &pr, hipStream_t s);
+                       double *cyc_gram, double *cyc_solve, const RowPrior &pr,
+                       const Hadamard &hd, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
 // fixed side Fp (row stride DP) (residual.hip).
 hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
                         const uint8_t *val, const float *Fp, const float *X, int D,
-                        double *sse_items, hipStream_t s);
+                        double *sse_items, const Hadamard &hd, hipStream_t s);
 
 // Widths solved one row per lane (registers hold the packed normal equations).
 inline int lane_width(int D) { return D <= 16 ? 16 : (D <= 20 ? 20 : 0); }
@@ -113,7 +122,7 @@ constexpr int ne_floats(int ld) { return ((ld * (ld + 1) / 2 + ld) + 3) / 4 * 4;
 hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
                           const int32_t *idx, const uint8_t *val, const float *wts,
                           const float *Fp, int64_t n_fixed, const float *Xold, float *ws,
-                          float *ne, double *sse, hipStream_t s);
+                          float *ne, double *sse, const Hadamard &hd, hipStream_t s);
 
 // One row per lane: regularise, Cholesky, solve, write (lanesolve.hip). Row i of
 // the launch uses record base + i; its first n_split rows are split rows whose

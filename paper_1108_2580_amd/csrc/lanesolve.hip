@@ -27,8 +27,9 @@ namespace als {
 // AUG (used for D = 17..20, LD = 20): the ratings ride in padding feature 20 of the
 // gathered rows, so the MFMA Gram delivers b in column 20 (tile column 4 of the last
 // tile) and the per-rating right-hand-side FMAs disappear. WT: weighted ALS, with the
-// per-rating weights wts aligned with idx / val.
-template <int DP, int LD, bool AUG, bool WT>
+// per-rating weights wts aligned with idx / val. TS: tensor ALS, whose fixed vectors are
+// the elementwise products Fp[idx] * hd.Tp[hd.idx2].
+template <int DP, int LD, bool AUG, bool WT, bool TS>
 __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ items,
                                                 int64_t n_chunk_items,
                                                 const int32_t *__restrict__ idx,
@@ -37,7 +38,7 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
                                                 const float *__restrict__ Fp, int zrow,
                                                 const float *__restrict__ Xold, int D,
                                                 float *__restrict__ ws, float *__restrict__ ne,
-                                                double *__restrict__ sse_out) {
+                                                double *__restrict__ sse_out, Hadamard hd) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
   constexpr int NTRI = LD * (LD + 1) / 2;
@@ -61,9 +62,12 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   }
   double sse = 0.0;
   const float *__restrict__ wp = WT ? wts + it.start : nullptr;
-  const GroupLanes g0 = group_lanes<WT>(idx + it.start, val + it.start, wp, it.len, 0, zrow);
-  gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, it.len, Fp,
-                               zrow, AUG ? LD - 16 * (T - 1) : -1, s_stage, g0);
+  const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
+  const GroupLanes g0 =
+      group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
+  gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp,
+                                   it.len, Fp, hd.Tp, zrow, AUG ? LD - 16 * (T - 1) : -1,
+                                   s_stage, g0);
   if constexpr (!AUG) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
@@ -200,33 +204,44 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
 }
 
 template <int DP, int LD, bool AUG>
-static void launch_gram_ne_t(const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
-                             const int32_t *idx, const uint8_t *val, const float *wts,
-                             const float *Fp, int zrow, const float *Xold, int D, float *ws,
-                             float *ne, double *sse, hipStream_t s) {
-  if (wts)
-    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, true>), dim3((unsigned)n_items), dim3(64), 0, s,
-                       items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse);
+static hipError_t launch_gram_ne_t(const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
+                                   const int32_t *idx, const uint8_t *val, const float *wts,
+                                   const float *Fp, int zrow, const float *Xold, int D, float *ws,
+                                   float *ne, double *sse, const Hadamard &hd, hipStream_t s) {
+  if (hd.idx2) {
+    // tensor ALS has no per-rating weights
+    if (wts) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, false, true>), dim3((unsigned)n_items), dim3(64),
+                       0, s, items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse,
+                       hd);
+  } else if (wts)
+    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, true, false>), dim3((unsigned)n_items), dim3(64),
+                       0, s, items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse,
+                       hd);
   else
-    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, false>), dim3((unsigned)n_items), dim3(64), 0, s,
-                       items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse);
+    hipLaunchKernelGGL((k_gram_ne<DP, LD, AUG, false, false>), dim3((unsigned)n_items), dim3(64),
+                       0, s, items, n_chunk_items, idx, val, wts, Fp, zrow, Xold, D, ws, ne, sse,
+                       hd);
+  return hipSuccess;
 }
 
 hipError_t launch_gram_ne(int D, const WorkItem *items, int64_t n_items, int64_t n_chunk_items,
                           const int32_t *idx, const uint8_t *val, const float *wts,
                           const float *Fp, int64_t n_fixed, const float *Xold, float *ws,
-                          float *ne, double *sse, hipStream_t s) {
+                          float *ne, double *sse, const Hadamard &hd, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
   const int zrow = (int)n_fixed;
   const int ld = lane_width(D);
+  hipError_t e;
   if (ld == 16)
-    launch_gram_ne_t<16, 16, false>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow, Xold,
-                                    D, ws, ne, sse, s);
+    e = launch_gram_ne_t<16, 16, false>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow,
+                                        Xold, D, ws, ne, sse, hd, s);
   else if (ld == 20)
-    launch_gram_ne_t<32, 20, true>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow, Xold,
-                                   D, ws, ne, sse, s);
+    e = launch_gram_ne_t<32, 20, true>(items, n_items, n_chunk_items, idx, val, wts, Fp, zrow,
+                                       Xold, D, ws, ne, sse, hd, s);
   else
     return hipErrorInvalidValue;
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 

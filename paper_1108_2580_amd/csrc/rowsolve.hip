@@ -66,7 +66,7 @@ __host__ __device__ constexpr int aug_column(int D) {
 
 // Partial normal equations of the chunks of split rows, with the chunks'
 // entering-state squared residuals.
-template <int DP, bool AUG, bool WT>
+template <int DP, bool AUG, bool WT, bool TS>
 __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__ items,
                                                     const int32_t *__restrict__ idx,
                                                     const uint8_t *__restrict__ val,
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
                                                     const float *__restrict__ Fp, int zrow,
                                                     const float *__restrict__ Xold, int D,
                                                     float *__restrict__ ws,
-                                                    double *__restrict__ sse_out) {
+                                                    double *__restrict__ sse_out, Hadamard hd) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
   __shared__ GroupStage s_stage;
@@ -94,9 +94,12 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   }
   double sse = 0.0;
   const float *__restrict__ wp = WT ? wts + it.start : nullptr;
-  const GroupLanes g0 = group_lanes<WT>(idx + it.start, val + it.start, wp, it.len, 0, zrow);
-  gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, it.len, Fp,
-                               zrow, AUG ? aug_column<DP>(D) : -1, s_stage, g0);
+  const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
+  const GroupLanes g0 =
+      group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
+  gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp,
+                                   it.len, Fp, hd.Tp, zrow, AUG ? aug_column<DP>(D) : -1,
+                                   s_stage, g0);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -134,7 +137,7 @@ constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 // alpha, identity on the padding, and Lambda mu / alpha in the right-hand side) and the
 // forward-substitution result y gets z / sqrt(alpha) before the back substitution, so
 // that the row receives the conditional draw mu* + L*^{-T} z.
-template <int DP, bool AUG, bool WT, bool BAYES>
+template <int DP, bool AUG, bool WT, bool BAYES, bool TS>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
     const uint8_t *__restrict__ val, const float *__restrict__ wts,
@@ -142,7 +145,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const float *__restrict__ ws, int D, float lam, float *__restrict__ X_io,
     double *__restrict__ sse_out,
     int32_t *__restrict__ flag_count, double *__restrict__ cyc_gram,
-    double *__restrict__ cyc_solve, RowPrior pr) {
+    double *__restrict__ cyc_solve, RowPrior pr, Hadamard hd) {
   const uint64_t t_start = __builtin_readcyclecounter();
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
@@ -195,9 +198,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     }
     double sse = 0.0;
     const float *__restrict__ wp = WT ? wts + rt.start : nullptr;
-    const GroupLanes g0 = group_lanes<WT>(idx + rt.start, val + rt.start, wp, rt.deg, 0, zrow);
-    gram_accumulate<DP, AUG, WT>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, rt.deg,
-                                 Fp, zrow, aug_c, s_stage[wv], g0);
+    const int32_t *__restrict__ tp = TS ? hd.idx2 + rt.start : nullptr;
+    const GroupLanes g0 =
+        group_lanes<WT, TS>(idx + rt.start, val + rt.start, wp, tp, rt.deg, 0, zrow);
+    gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp,
+                                     rt.deg, Fp, hd.Tp, zrow, aug_c, s_stage[wv], g0);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -436,15 +441,15 @@ static constexpr bool has_aug(int D) {
   return ((D + 3) & ~3) < DP;
 }
 
-template <int DP, bool AUG, bool WT, bool BAYES>
+template <int DP, bool AUG, bool WT, bool BAYES, bool TS = false>
 static void launch_rows_k(int64_t blocks, const RowTask *rows, int64_t n_rows,
                           const int32_t *idx, const uint8_t *val, const float *wts,
                           const float *Fp, int zrow, const float *ws, int D, float lam, float *X,
                           double *sse, int32_t *flag, double *cyc_gram, double *cyc_solve,
-                          const RowPrior &pr, hipStream_t s) {
-  hipLaunchKernelGGL((k_rows<DP, AUG, WT, BAYES>), dim3((unsigned)blocks), dim3(64 * kRowWaves),
-                     0, s, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag,
-                     cyc_gram, cyc_solve, pr);
+                          const RowPrior &pr, const Hadamard &hd, hipStream_t s) {
+  hipLaunchKernelGGL((k_rows<DP, AUG, WT, BAYES, TS>), dim3((unsigned)blocks),
+                     dim3(64 * kRowWaves), 0, s, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
+                     lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd);
 }
 
 template <int DP>
@@ -452,57 +457,77 @@ static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32
                                 const uint8_t *val, const float *wts, const float *Fp, int zrow,
                                 const float *ws, int D, float lam, float *X, double *sse,
                                 int32_t *flag, double *cyc_gram, double *cyc_solve,
-                                const RowPrior &pr, hipStream_t s) {
+                                const RowPrior &pr, const Hadamard &hd, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
   const bool aug = has_aug<DP>(D), wt = wts != nullptr;
-  if (pr.init) {
+  if (hd.idx2) {
+    // tensor ALS: no weights, no Bayesian prior
+    if (wt || pr.init) return hipErrorInvalidValue;
+    if (aug)
+      launch_rows_k<DP, true, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow,
+                                                  ws, D, lam, X, sse, flag, cyc_gram, cyc_solve,
+                                                  pr, hd, s);
+    else
+      launch_rows_k<DP, false, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow,
+                                                   ws, D, lam, X, sse, flag, cyc_gram, cyc_solve,
+                                                   pr, hd, s);
+  } else if (pr.init) {
     // the Gibbs half-sweep has no per-rating weights
     if (wt) return hipErrorInvalidValue;
     if (aug)
       launch_rows_k<DP, true, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
     else
       launch_rows_k<DP, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                            lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                            lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
   } else if (aug && wt)
     launch_rows_k<DP, true, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                         lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                         lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
   else if (aug)
     launch_rows_k<DP, true, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
   else if (wt)
     launch_rows_k<DP, false, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
   else
     launch_rows_k<DP, false, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, s);
+                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
   return hipGetLastError();
 }
 
-template <int DP, bool AUG, bool WT>
+template <int DP, bool AUG, bool WT, bool TS = false>
 static void launch_chunks_k(int64_t n, const WorkItem *items, const int32_t *idx,
                             const uint8_t *val, const float *wts, const float *Fp, int zrow,
-                            const float *Xold, int D, float *ws, double *sse, hipStream_t s) {
-  hipLaunchKernelGGL((k_gram_chunks<DP, AUG, WT>), dim3((unsigned)n), dim3(64), 0, s, items, idx,
-                     val, wts, Fp, zrow, Xold, D, ws, sse);
+                            const float *Xold, int D, float *ws, double *sse, const Hadamard &hd,
+                            hipStream_t s) {
+  hipLaunchKernelGGL((k_gram_chunks<DP, AUG, WT, TS>), dim3((unsigned)n), dim3(64), 0, s, items,
+                     idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd);
 }
 
 template <int DP>
 static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_t *idx,
                                   const uint8_t *val, const float *wts, const float *Fp,
                                   int zrow, const float *Xold, int D, float *ws, double *sse,
-                                  hipStream_t s) {
+                                  const Hadamard &hd, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const bool aug = has_aug<DP>(D), wt = wts != nullptr;
-  if (aug && wt)
-    launch_chunks_k<DP, true, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+  if (hd.idx2) {
+    if (wt) return hipErrorInvalidValue;
+    if (aug)
+      launch_chunks_k<DP, true, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse,
+                                             hd, s);
+    else
+      launch_chunks_k<DP, false, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse,
+                                              hd, s);
+  } else if (aug && wt)
+    launch_chunks_k<DP, true, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
   else if (aug)
-    launch_chunks_k<DP, true, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+    launch_chunks_k<DP, true, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
   else if (wt)
-    launch_chunks_k<DP, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+    launch_chunks_k<DP, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
   else
-    launch_chunks_k<DP, false, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, s);
+    launch_chunks_k<DP, false, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
   return hipGetLastError();
 }
 
@@ -522,20 +547,21 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
 hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_t *idx,
                        const uint8_t *val, const float *wts, const float *Fp, int64_t n_fixed,
                        const float *ws, int D, float lam, float *X, double *sse, int32_t *flag,
-                       double *cyc_gram, double *cyc_solve, const RowPrior &pr, hipStream_t s) {
+                       double *cyc_gram, double *cyc_solve, const RowPrior &pr,
+                       const Hadamard &hd, hipStream_t s) {
   if ((cyc_gram == nullptr) != (cyc_solve == nullptr)) return hipErrorInvalidValue;
   const int zrow = (int)n_fixed;
   ALS_DP_SWITCH(dp, return launch_rows_t<DPV>(rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam,
-                                              X, sse, flag, cyc_gram, cyc_solve, pr, s));
+                                              X, sse, flag, cyc_gram, cyc_solve, pr, hd, s));
 }
 
 hipError_t launch_gram_chunks(int dp, const WorkItem *items, int64_t n, const int32_t *idx,
                               const uint8_t *val, const float *wts, const float *Fp,
                               int64_t n_fixed, const float *Xold, int D, float *ws, double *sse,
-                              hipStream_t s) {
+                              const Hadamard &hd, hipStream_t s) {
   const int zrow = (int)n_fixed;
   ALS_DP_SWITCH(dp, return launch_chunks_t<DPV>(items, n, idx, val, wts, Fp, zrow, Xold, D, ws,
-                                                sse, s));
+                                                sse, hd, s));
 }
 
 }  // namespace als
