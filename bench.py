@@ -51,9 +51,12 @@ def parse():
                     help="weighted ALS: seeded per-rating weights, log-uniform on [0.25, 4)")
     ap.add_argument("--gibbs", action="store_true",
                     help="Bayesian factorisation: one step is a BPMF Gibbs iteration")
+    ap.add_argument("--tensor", action="store_true",
+                    help="tensor ALS over 6649 seeded time bins: one step updates the items, "
+                         "the users and the time bins")
     args = ap.parse_args()
-    if args.gibbs and args.weighted:
-        ap.error("--gibbs and --weighted are exclusive")
+    if args.gibbs + args.weighted + args.tensor > 1:
+        ap.error("--gibbs, --weighted and --tensor are exclusive")
     return args
 
 
@@ -124,9 +127,9 @@ def measured_traffic(workload_name, kernel):
     return None
 
 
-def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False):
+def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False, tensor=None):
     """fp64 oracle on a seeded random sample of the user half-sweep's rows (the Gibbs row
-    draws with ``gibbs``)."""
+    draws with ``gibbs``; the tensor user-mode update with ``tensor`` = (bins, T))."""
     import numpy as np
 
     import oracle
@@ -146,6 +149,14 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False):
         k = min(k, perm.size)
         sel = np.sort(perm[:k])
         t0 = time.perf_counter()
+        if tensor is not None:
+            bins, Tf = tensor
+            sub_ptr = np.concatenate([[0], np.cumsum(deg[sel])]).astype(np.int64)
+            take = np.repeat(r.row_ptr[sel] - sub_ptr[:-1], deg[sel]) + np.arange(sub_ptr[-1])
+            t_a = time.perf_counter()
+            oracle.tensor_rows(sub_ptr, r.col[take], bins[take], val[take], fixed, Tf, r.lam,
+                               np.zeros((k, r.D)), threads=threads)
+            return int(deg[sel].sum()), k, time.perf_counter() - t_a
         if gibbs:
             sub_ptr = np.concatenate([[0], np.cumsum(deg[sel])]).astype(np.int64)
             take = np.repeat(r.row_ptr[sel] - sub_ptr[:-1], deg[sel]) + np.arange(sub_ptr[-1])
@@ -174,7 +185,8 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False):
     return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
                 cpu_model=cpu_model,
                 sample=(f"user half-sweep of {r.name}"
-                        f"{' (weighted)' if w is not None else ' (Gibbs draws)' if gibbs else ''}: "
+                        f"{' (weighted)' if w is not None else ' (Gibbs draws)' if gibbs else ''}"
+                        f"{' (tensor user mode)' if tensor is not None else ''}: "
                         f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
@@ -291,35 +303,48 @@ def main():
     U = torch.from_numpy(U0).to(dev)
     V = torch.from_numpy(V0).to(dev)
     gibbs = GibbsSteps(r, als, args.warmup + args.steps, r.init_seed + 77) if args.gibbs else None
+    sides = ("items", "users")
+    T = bins = None
+    if args.tensor:
+        t_b = time.perf_counter()
+        nb = workload.N_TIME_BINS
+        bins = workload.time_bins(r.row_ptr, nb, workload.time_seed(args.config))
+        als.set_time_bins(nb, bins)
+        rng = np.random.default_rng(r.init_seed + 99)
+        T = torch.from_numpy((1.0 + 0.1 * rng.standard_normal((nb, r.D))).astype(np.float32)).to(dev)
+        sides = ("items", "users", "bins")
+        log(f"time bins ({nb}) and their layout: {time.perf_counter() - t_b:.1f} s")
 
-    def half(side, k, fixed, out):
+    def half(side, k):
+        if args.tensor:
+            als.tensor_half_sweep(side, U, V, T, r.lam)
+            return
+        fixed, out = (U, V) if side == "items" else (V, U)
         if gibbs is not None:
             gibbs.half(als, side, k, fixed, out)
         else:
             als.half_sweep(side, fixed, r.lam, out)
 
     for w in range(args.warmup):
-        half("items", w, U, V)
-        half("users", w, V, U)
+        for side in sides:
+            half(side, w)
         torch.cuda.synchronize()
         log(f"warmup {w + 1}/{args.warmup} done")
     torch.cuda.synchronize()
     als.set_profiling(True)
     # HIP events around each half-sweep on the stream the library enqueues on
     ev = {side: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                 for _ in range(args.steps)] for side in ("items", "users")}
+                 for _ in range(args.steps)] for side in sides}
     t0 = time.perf_counter()
     for k in range(args.steps):
-        ev["items"][k][0].record()
-        half("items", args.warmup + k, U, V)
-        ev["items"][k][1].record()
-        ev["users"][k][0].record()
-        half("users", args.warmup + k, V, U)
-        ev["users"][k][1].record()
+        for side in sides:
+            ev[side][k][0].record()
+            half(side, args.warmup + k)
+            ev[side][k][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     per_side = {}
-    for side in ("items", "users"):
+    for side in sides:
         ms = sorted(a.elapsed_time(b) for a, b in ev[side])
         med = ms[len(ms) // 2] if len(ms) % 2 else 0.5 * (ms[len(ms) // 2 - 1] + ms[len(ms) // 2])
         per_side[side] = {"ms_median": med, "ms_min": ms[0], "ratings_per_s": r.nnz / (med * 1e-3)}
@@ -327,13 +352,13 @@ def main():
     als.set_profiling(False)
     elapsed = t1 - t0
     rmse_in = als.rmse_in()
-    rmse = als.rmse(U, V)
+    rmse = als.tensor_rmse(U, V, T) if args.tensor else als.rmse(U, V)
     gram_share = None
-    if r.D > 20:
+    if r.D > 20 and not args.tensor:
         # one extra, untimed half-sweep per side with the row kernel's phase clocks on
         als.set_phase_timing(True)
-        half("items", args.warmup + args.steps - 1, U, V)
-        half("users", args.warmup + args.steps - 1, V, U)
+        half("items", args.warmup + args.steps - 1)
+        half("users", args.warmup + args.steps - 1)
         gi, si = als.phase_cycles("items")
         gu, su = als.phase_cycles("users")
         als.set_phase_timing(False)
@@ -341,15 +366,20 @@ def main():
     log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
         f"rmse entering last half-sweep {rmse_in:.6f}, final {rmse:.6f}")
 
-    value = 2.0 * r.nnz * args.steps / elapsed
-    halves = 2 * args.steps
+    value = len(sides) * r.nnz * args.steps / elapsed
+    halves = len(sides) * args.steps
     rows_with = als.plan_stats("users")["rows_with_ratings"] + \
         als.plan_stats("items")["rows_with_ratings"]
+    if args.tensor:
+        rows_with += int(np.unique(bins).size)
     D = r.D
-    workload_name = r.name + ("_wals" if args.weighted else "_bpmf" if args.gibbs else "")
+    workload_name = r.name + ("_wals" if args.weighted else "_bpmf" if args.gibbs else
+                              "_tensor" if args.tensor else "")
     dominant = max(prof, key=lambda k: prof[k][0])
-    wbytes = 4 if args.weighted else 0   # a weight per rating
-    wflops = D if args.weighted else 0   # c f per rating
+    # per rating: a weight (weighted ALS); the second index and second gathered row, and
+    # the product of the two rows (tensor ALS)
+    wbytes = 4 if args.weighted else (4 + 4 * D) if args.tensor else 0
+    wflops = D if (args.weighted or args.tensor) else 0
     if D <= 20:
         # gather kernel: per rating the index, the rating (and weight) and the gathered fixed
         # row; per solved row the row pointer and the entering value
@@ -389,12 +419,13 @@ def main():
     cpu = None
     if args.cpu_seconds > 0:
         log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
-        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights, gibbs=args.gibbs)
+        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights, gibbs=args.gibbs,
+                           tensor=(bins, T.cpu().numpy()) if args.tensor else None)
         log(f"cpu baseline: {cpu}")
 
     out = {
-        "metric": ("wALS" if args.weighted else "BPMF Gibbs" if args.gibbs else "ALS")
-        + " ratings/sec per half-sweep",
+        "metric": ("wALS" if args.weighted else "BPMF Gibbs" if args.gibbs else
+                   "tensor ALS" if args.tensor else "ALS") + " ratings/sec per half-sweep",
         "value": value,
         "unit": "ratings/s",
         "n_gpus": 1,
@@ -413,8 +444,10 @@ def main():
                    "gibbs": (dict(alpha=GIBBS_ALPHA, mu0=0.0, beta0=GIBBS_BETA0, W0="I",
                                   nu0=r.D, variates="seeded, on the device before timing")
                              if args.gibbs else None),
+                   "time_bins": workload.N_TIME_BINS if args.tensor else None,
                    "step": ("item side (hyperparameter draw, row draws) + user side"
-                            if args.gibbs else "item half-sweep + user half-sweep"),
+                            if args.gibbs else "item, user and time-bin mode updates"
+                            if args.tensor else "item half-sweep + user half-sweep"),
                    "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,
