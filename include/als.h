@@ -201,7 +201,7 @@ als_status als_get_phase_cycles(als_ctx *ctx, als_side side, double *gram_cycles
  *                 pred = NaN and reads nothing.
  *   pred          device fp32[n_pairs], caller-owned, overlapping none of the inputs.
  * Enqueued on the context's stream without synchronisation. n_pairs = 0 does nothing;
- * n_pairs above 2^31 * 256 - 256 is ALS_ERR_INVALID_ARG.
+ * n_pairs above (2^31 - 1) * 32 is ALS_ERR_INVALID_ARG.
  */
 als_status als_predict(als_ctx *ctx, const float *U, const float *V, int64_t n_pairs,
                        const int32_t *users, const int32_t *items, float *pred);

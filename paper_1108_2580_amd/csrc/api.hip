@@ -307,8 +307,9 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   return ALS_OK;
 }
 
-// pairs of one predict call: the launch has pair_blocks(n) < 2^31 blocks
-constexpr int64_t kMaxPairs = 0x7fffffffLL * 256;
+// pairs of one predict call: the launch has pair_blocks(n, D) < 2^31 blocks (with up to 8
+// lanes per pair)
+constexpr int64_t kMaxPairs = 0x7fffffffLL * 256 / 8;
 
 void free_holdout(als_ctx *c) {
   dfree(c->d_hu);
@@ -1314,7 +1315,7 @@ als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
     hi[q] = items[p];
     hr[q] = ratings[p];
   }
-  const int64_t nb = als::pair_blocks(n_pairs);
+  const int64_t nb = als::pair_blocks(n_pairs, ctx->D);
   hipError_t e = dalloc(&ctx->d_hu, n_pairs);
   if (e == hipSuccess) e = dalloc(&ctx->d_hi, n_pairs);
   if (e == hipSuccess) e = dalloc(&ctx->d_hr, n_pairs);
@@ -1350,7 +1351,7 @@ als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double
   HIP_OR_FAIL(ctx, als::launch_predict(U, V, ctx->M, ctx->N, ctx->D, ctx->n_hold, ctx->d_hu,
                                        ctx->d_hi, ctx->d_hr, nullptr, ctx->d_hold_blocks,
                                        ctx->stream));
-  HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_hold_blocks, als::pair_blocks(ctx->n_hold),
+  HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_hold_blocks, als::pair_blocks(ctx->n_hold, ctx->D),
                                       ctx->d_hold_partials, ctx->d_hold_sse, ctx->stream));
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_hold_sse, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));

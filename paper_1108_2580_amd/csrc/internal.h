@@ -180,9 +180,9 @@ hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int 
 
 // Predictions u_{users[p]} . v_{items[p]} of n pairs (predict.hip). pred (nullable)
 // receives them, NaN for a pair with an index outside [0, M) x [0, N). With
-// sse_blocks non-null, r holds the pairs' ratings and block b of pair_blocks(n)
+// sse_blocks non-null, r holds the pairs' ratings and block b of pair_blocks(n, D)
 // writes the fp64 sum of (r - r_hat)^2 over its pairs to sse_blocks[b].
-int64_t pair_blocks(int64_t n);
+int64_t pair_blocks(int64_t n, int D);
 hipError_t launch_predict(const float *U, const float *V, int64_t M, int64_t N, int D, int64_t n,
                           const int32_t *users, const int32_t *items, const uint8_t *r,
                           float *pred, double *sse_blocks, hipStream_t s);
