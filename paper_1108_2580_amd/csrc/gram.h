@@ -209,13 +209,19 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
 // a column of the Gram and rhs is left alone. With WT (weighted ALS) the first MFMA
 // operand carries c f, so the tiles accumulate sum c f f^T (and, in the augmented
 // column, sum c r f); predictions use the unweighted rows.
-template <int DP, int STEPS, bool AUG, bool WT>
+// CORNER (two tiles, features 16..20 used in the second: the one-lane widths D = 17..20):
+// the last diagonal tile would spend a 16x16 MFMA on 15 useful products, so it is skipped
+// and each lane c < 15 of a row group accumulates one product f[16 + p] f[16 + q] of the
+// group's rating instead, fetching the two values across the group's lanes with
+// ds_bpermute (byte addresses cx, cy) and adding them with one FMA.
+template <int DP, int STEPS, bool AUG, bool WT, bool CORNER = false>
 __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float (&rhs)[DP / 16], const float (&xo)[DP / 16],
                                           float (&pi)[16], const float (&a)[STEPS][DP / 16],
                                           const float (&r)[STEPS], const float (&wt)[STEPS],
-                                          int s0, int steps) {
+                                          int s0, int steps, float &corner, int cx, int cy) {
   constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
+  static_assert(!CORNER || T == 2, "the corner path is for two tiles");
 #pragma unroll
   for (int u0 = 0; u0 < STEPS; u0 += SUB) {
     if (s0 + u0 < steps) {
@@ -232,9 +238,18 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
 #pragma unroll
         for (int I = 0; I < T; ++I) {
 #pragma unroll
-          for (int J = I; J < T; ++J)
+          for (int J = I; J < T; ++J) {
+            if (CORNER && I == T - 1) continue;
             acc[tidx<T>(I, J)] =
                 __builtin_amdgcn_mfma_f32_16x16x4f32(wa[I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
+          }
+        }
+        if constexpr (CORNER) {
+          const float xv = __builtin_bit_cast(
+              float, __builtin_amdgcn_ds_bpermute(cx, __builtin_bit_cast(int, wa[T - 1])));
+          const float yv = __builtin_bit_cast(
+              float, __builtin_amdgcn_ds_bpermute(cy, __builtin_bit_cast(int, a[u][T - 1])));
+          corner = fmaf(xv, yv, corner);
         }
       }
     }
@@ -298,7 +313,8 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStag
 //    one, so that its latency hides behind them. The blocks of the last group that
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
 // tp, Tp (tensor ALS, TS): the item's second indices and the second staged table.
-template <int DP, bool AUG, bool WT, bool TS = false>
+// corner, cx, cy: the corner products of mma_block (CORNER), else unused.
+template <int DP, bool AUG, bool WT, bool TS = false, bool CORNER = false>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
                                                 const float (&xo)[RowCfg<DP>::T], double &sse,
@@ -308,7 +324,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 const int32_t *__restrict__ tp, int n,
                                                 const float *__restrict__ Fp,
                                                 const float *__restrict__ Tp, int zrow,
-                                                int aug_c, GroupStage &st, GroupLanes gv) {
+                                                int aug_c, GroupStage &st, GroupLanes gv,
+                                                float &corner, int cx, int cy) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
@@ -329,7 +346,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
           float a[STEPS][T];
           float r[STEPS], w[STEPS];
           gather_block<DP, STEPS, AUG, WT, TS>(a, r, w, st, 0, s0, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a, r, w, s0, steps);
+          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a, r, w, s0, steps, corner, cx, cy);
         }
       }
       group_residuals(pi, st, 0, g, n, sse);
@@ -356,7 +373,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         if constexpr (b % 2 == 0) {
           if constexpr (b + 1 < NB)
             gather_block<DP, STEPS, AUG, WT, TS>(a1, r1, w1, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a0, r0, w0, s0, steps);
+          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a0, r0, w0, s0, steps, corner, cx, cy);
         } else {
           if constexpr (b + 1 < NB) {
             gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
@@ -366,7 +383,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
             wave_sync();
             gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf ^ 1, 0, Fp, Tp, aug_lane);
           }
-          mma_block<DP, STEPS, AUG, WT>(acc, rhs, xo, pi, a1, r1, w1, s0, steps);
+          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a1, r1, w1, s0, steps, corner, cx, cy);
         }
       };
       unroll_blocks<0, NB>(block);

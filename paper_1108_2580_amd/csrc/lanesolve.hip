@@ -45,6 +45,8 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   constexpr int NES = ne_floats(LD);
   static_assert(!AUG || (LD < DP && LD > 16 * (T - 1) && LD % 4 == 0),
                 "the augmented column is feature LD of the last tile");
+  // the last diagonal tile holds features 16 .. LD only: its 15 products go to VALU
+  constexpr bool CORNER = AUG && T == 2 && LD == 20;
   __shared__ GroupStage s_stage;
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
@@ -65,9 +67,24 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
   const GroupLanes g0 =
       group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
-  gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp,
-                                   it.len, Fp, hd.Tp, zrow, AUG ? LD - 16 * (T - 1) : -1,
-                                   s_stage, g0);
+  // CORNER: lane c < 15 of a row group owns the product (cp, cq), cp <= cq < 5, of the
+  // features 16 + cp and 16 + cq (16 + 4 = LD is the augmented column)
+  int cp = 0, cq = 0;
+  if constexpr (CORNER) {
+    int rem = c;
+    while (cp < 4 && rem >= 5 - cp) {
+      rem -= 5 - cp;
+      ++cp;
+    }
+    cq = c < 15 ? cp + rem : 0;
+    if (c >= 15) cp = 0;
+  }
+  const int cx = (kq * 16 + cp) * 4, cy = (kq * 16 + cq) * 4;
+  float corner = 0.f;
+  gram_accumulate<DP, AUG, WT, TS, CORNER>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp,
+                                           tp, it.len, Fp, hd.Tp, zrow,
+                                           AUG ? LD - 16 * (T - 1) : -1, s_stage, g0, corner, cx,
+                                           cy);
   if constexpr (!AUG) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
@@ -78,10 +95,20 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ((int64_t)blockIdx.x < n_chunk_items ? ws : ne) + it.slot * NES;
+  if constexpr (CORNER) {
+    corner += __shfl_xor(corner, 16);
+    corner += __shfl_xor(corner, 32);
+    if (kq == 0 && c < 15) {
+      const int a = 16 + cp, b = 16 + cq;
+      if (b < LD) out[tri<LD>(a, b)] = corner;
+      else if (a < LD) out[NTRI + a] = corner;  // (a, LD): the right-hand side of feature a
+    }
+  }
 #pragma unroll
   for (int I = 0; I < T; ++I) {
 #pragma unroll
     for (int J = I; J < T; ++J) {
+      if (CORNER && I == T - 1) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int a = 16 * I + 4 * kq + r, b = 16 * J + c;

@@ -97,9 +97,10 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
   const GroupLanes g0 =
       group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
+  float no_corner = 0.f;
   gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp,
                                    it.len, Fp, hd.Tp, zrow, AUG ? aug_column<DP>(D) : -1,
-                                   s_stage, g0);
+                                   s_stage, g0, no_corner, 0, 0);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -201,8 +202,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const int32_t *__restrict__ tp = TS ? hd.idx2 + rt.start : nullptr;
     const GroupLanes g0 =
         group_lanes<WT, TS>(idx + rt.start, val + rt.start, wp, tp, rt.deg, 0, zrow);
+    float no_corner = 0.f;
     gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp,
-                                     rt.deg, Fp, hd.Tp, zrow, aug_c, s_stage[wv], g0);
+                                     rt.deg, Fp, hd.Tp, zrow, aug_c, s_stage[wv], g0, no_corner,
+                                     0, 0);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
