@@ -388,6 +388,12 @@ def main():
         # row; per solved row the row pointer and the entering value
         k_ms, k_n = prof["gather"]
         alg = halves * r.nnz * (5 + wbytes + 4 * D) + args.steps * rows_with * (8 + 4 * D)
+        if args.tensor:
+            # per step: every rating twice with one large gathered row (the user and item
+            # modes) and once with two (the time-bin mode), plus both indices and the rating
+            # each time; the time-bin table (6649 rows) once per user and item mode
+            alg = args.steps * (r.nnz * (27 + 16 * D) + 2 * workload.N_TIME_BINS * 4 * D
+                                + rows_with * (8 + 4 * D))
         achieved = alg / (k_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=achieved / HBM_PEAK_GBS, kernel="k_gram_ne")

@@ -93,3 +93,35 @@ def test_full_d20_free_running_rmse():
             ro = t.rmse()
             log(f"  sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
         assert abs(rm - ro) <= RMSE_TOL
+
+
+@pytest.mark.parametrize("k", [3, 4])
+def test_full_weighted_first_half_sweep_sampled(k):
+    """Weighted ALS at full size: seeded per-rating weights (log-uniform on [0.25, 4)), one
+    half-sweep per side from the seeded factors, sampled rows against the oracle's weighted
+    solve (the weights travel to the item side with the oracle's own transpose)."""
+    from paper_1108_2580_amd import ALS
+
+    r = workload.make_config(k)
+    w = workload.rating_weights(r.nnz, workload.weight_seed(k))
+    log(f"{r.name} weighted: nnz={r.nnz} D={r.D}")
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    val = r.val.astype(np.float64)
+    w64 = w.astype(np.float64)
+    csc = oracle.transpose(r.row_ptr, r.col, val, r.N)
+    w_t = oracle.transpose(r.row_ptr, r.col, w64, r.N)[2]
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        als.set_weights(w)
+        for side, fixed, prev, (p, i, v), ww in (("items", U0, V0, csc, w_t),
+                                                 ("users", V0, U0, (r.row_ptr, r.col, val), w64)):
+            out = dev(prev)
+            als.half_sweep(side, dev(fixed), r.lam, out)
+            assert als.flagged_rows() == 0
+            xg = out.cpu().numpy()
+            assert np.isfinite(xg).all()
+            rows = sample_rows(p, seed=10 + k)
+            xo, fl = oracle.solve_rows(rows, p, i, v, fixed, r.lam, w=ww)
+            assert (fl == 0).all()
+            rel = np.linalg.norm(xg[rows] - xo, axis=1) / np.linalg.norm(xo, axis=1)
+            log(f"  {side}: {rows.size} sampled rows, rel p50={np.median(rel):.2e} max={rel.max():.2e}")
+            assert rel.max() <= ROW_TOL
