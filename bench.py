@@ -225,6 +225,22 @@ def heldout_leg(args, r, als, U, V, workload_name, reps=20):
     alg = n * (12 + 4 * r.D) + n_users * 4 * r.D
     achieved = alg / (ms * 1e-3) / 1e9
     log(f"held-out leg: {n} pairs, {ms:.4f} ms per launch, {achieved:.0f} GB/s algorithmic")
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+
+        threads = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+        Uh = U.cpu().numpy().astype(np.float64)
+        Vh = V.cpu().numpy().astype(np.float64)
+        oracle.predict(hu[:1000], hi[:1000], Uh, Vh, threads=threads)
+        # whole passes over the pairs until about a second of host work has been timed
+        passes, t0 = 0, time.perf_counter()
+        while passes == 0 or time.perf_counter() - t0 < 1.0:
+            oracle.predict(hu, hi, Uh, Vh, threads=threads)
+            passes += 1
+        dt = time.perf_counter() - t0
+        cpu = dict(value=passes * n / dt, unit="pairs/s", cores=threads, kind="oracle",
+                   sample=f"{passes} passes over all {n} pairs, fp64, {dt:.2f} s")
     return dict(metric="held-out predictions/sec", value=n / (ms * 1e-3), unit="pairs/s",
                 pairs=n, launches=reps, ms_per_launch=ms,
                 sample=(f"1/{args.heldout_share} of the stored positions of {r.name}, seeded, "
@@ -233,7 +249,7 @@ def heldout_leg(args, r, als, U, V, workload_name, reps=20):
                               frac=achieved / HBM_PEAK_GBS, kernel="k_predict",
                               alg_per_launch=alg,
                               traffic=measured_traffic(workload_name + "_heldout", "k_predict")),
-                rmse_same_pairs=vr)
+                cpu_baseline=cpu, rmse_same_pairs=vr)
 
 
 # BPMF Gibbs iteration: the usual hyperprior (mu0 = 0, beta0 = 2, W0 = I, nu0 = D) and a
