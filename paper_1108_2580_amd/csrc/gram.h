@@ -172,10 +172,13 @@ __device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip
 // With TS (tensor ALS) the fixed vector is the elementwise product of the rows of two
 // staged tables, Fp[j] * Tp[t] (t the rating's second index); the padding of Fp keeps
 // the product's padding zero.
-template <int DP, int STEPS, bool AUG, bool WT, bool TS = false>
-__device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&r)[STEPS],
-                                             float (&wt)[STEPS], const GroupStage &st, int buf,
-                                             int s0, const float *__restrict__ Fp,
+// With STRIP, sb[u] receives feature 16 (T - 1) + (c & 3) of the lane's rating: the
+// operand that every 4x4 block of the strip products in mma_block multiplies by.
+template <int DP, int STEPS, bool AUG, bool WT, bool TS = false, bool STRIP = false>
+__device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (&sb)[STEPS],
+                                             float (&r)[STEPS], float (&wt)[STEPS],
+                                             const GroupStage &st, int buf, int s0,
+                                             const float *__restrict__ Fp,
                                              const float *__restrict__ Tp, bool aug_lane) {
   constexpr int T = DP / 16;
   const int lane = threadIdx.x & 63;
@@ -193,11 +196,15 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
     const char *row = reinterpret_cast<const char *>(Fp) + (uint64_t)off;
 #pragma unroll
     for (int X = 0; X < T; ++X) a[u][X] = *reinterpret_cast<const float *>(row + 64 * X);
+    // the strip operand sits 4 (c & 3) bytes into the last tile of the same row
+    const int strip_off = 64 * (T - 1) - 4 * (c & 12);
+    if constexpr (STRIP) sb[u] = *reinterpret_cast<const float *>(row + strip_off);
     if constexpr (TS) {
       const uint32_t off2 = (uint32_t)stt[u] * (uint32_t)(DP * 4) + (uint32_t)(c * 4);
       const char *row2 = reinterpret_cast<const char *>(Tp) + (uint64_t)off2;
 #pragma unroll
       for (int X = 0; X < T; ++X) a[u][X] *= *reinterpret_cast<const float *>(row2 + 64 * X);
+      if constexpr (STRIP) sb[u] *= *reinterpret_cast<const float *>(row2 + strip_off);
     }
     if constexpr (AUG) a[u][T - 1] = aug_lane ? r[u] : a[u][T - 1];
   }
@@ -214,14 +221,23 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
 // and each lane c < 15 of a row group accumulates one product f[16 + p] f[16 + q] of the
 // group's rating instead, fetching the two values across the group's lanes with
 // ds_bpermute (byte addresses cx, cy) and adding them with one FMA.
-template <int DP, int STEPS, bool AUG, bool WT, bool CORNER = false>
+// STRIP (only features 16 (T - 1) .. 16 (T - 1) + 3 used in the last tile): the tiles
+// (I, T - 1) of the last column would spend a 16x16 MFMA each on four useful columns, so
+// each takes one v_mfma_f32_4x4x1f32 instead. Its 16 blocks are b = 4 kq + cb: block b
+// multiplies rows 16 I + 4 cb .. + 3 (the lane's own operand) by the four used features
+// of the last tile (sb), for rating kq alone; acc[tidx(I, T - 1)] then holds these
+// per-rating strips until strip_finish sums and rearranges them.
+template <int DP, int STEPS, bool AUG, bool WT, bool CORNER = false, bool STRIP = false>
 __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float (&rhs)[DP / 16], const float (&xo)[DP / 16],
                                           float (&pi)[16], const float (&a)[STEPS][DP / 16],
-                                          const float (&r)[STEPS], const float (&wt)[STEPS],
-                                          int s0, int steps, float &corner, int cx, int cy) {
+                                          const float (&sb)[STEPS], const float (&r)[STEPS],
+                                          const float (&wt)[STEPS], int s0, int steps,
+                                          float &corner, int cx, int cy) {
   constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
   static_assert(!CORNER || T == 2, "the corner path is for two tiles");
+  static_assert(!STRIP || (T >= 3 && !AUG && !CORNER),
+                "the strip path is for three or more tiles, with the right-hand side in rhs");
 #pragma unroll
   for (int u0 = 0; u0 < STEPS; u0 += SUB) {
     if (s0 + u0 < steps) {
@@ -240,8 +256,12 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
 #pragma unroll
           for (int J = I; J < T; ++J) {
             if (CORNER && I == T - 1) continue;
-            acc[tidx<T>(I, J)] =
-                __builtin_amdgcn_mfma_f32_16x16x4f32(wa[I], a[u][J], acc[tidx<T>(I, J)], 0, 0, 0);
+            if (STRIP && J == T - 1)
+              acc[tidx<T>(I, J)] =
+                  __builtin_amdgcn_mfma_f32_4x4x1f32(wa[I], sb[u], acc[tidx<T>(I, J)], 0, 0, 0);
+            else
+              acc[tidx<T>(I, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[I], a[u][J],
+                                                                        acc[tidx<T>(I, J)], 0, 0, 0);
           }
         }
         if constexpr (CORNER) {
@@ -314,7 +334,9 @@ __device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStag
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
 // tp, Tp (tensor ALS, TS): the item's second indices and the second staged table.
 // corner, cx, cy: the corner products of mma_block (CORNER), else unused.
-template <int DP, bool AUG, bool WT, bool TS = false, bool CORNER = false>
+// STRIP: the last tile column in strip form (mma_block); the caller finishes it with
+// strip_finish.
+template <int DP, bool AUG, bool WT, bool TS = false, bool CORNER = false, bool STRIP = false>
 __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 float (&rhs)[RowCfg<DP>::T],
                                                 const float (&xo)[RowCfg<DP>::T], double &sse,
@@ -344,9 +366,10 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
       for (int s0 = 0; s0 < 16; s0 += STEPS) {
         if (s0 < steps) {
           float a[STEPS][T];
-          float r[STEPS], w[STEPS];
-          gather_block<DP, STEPS, AUG, WT, TS>(a, r, w, st, 0, s0, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a, r, w, s0, steps, corner, cx, cy);
+          float sb[STEPS], r[STEPS], w[STEPS];
+          gather_block<DP, STEPS, AUG, WT, TS>(a, sb, r, w, st, 0, s0, Fp, Tp, aug_lane);
+          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a, sb, r, w, s0, steps, corner,
+                                                cx, cy);
         }
       }
       group_residuals(pi, st, 0, g, n, sse);
@@ -355,10 +378,11 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
     }
   } else {
     static_assert(NB % 2 == 0, "block buffers alternate within and across groups");
-    float a0[STEPS][T], a1[STEPS][T], r0[STEPS], r1[STEPS], w0[STEPS], w1[STEPS];
+    float a0[STEPS][T], a1[STEPS][T], b0[STEPS], b1[STEPS], r0[STEPS], r1[STEPS], w0[STEPS],
+        w1[STEPS];
     stage_group<WT, TS>(st, 0, gv);
     wave_sync();
-    gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, 0, 0, Fp, Tp, aug_lane);
+    gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a0, b0, r0, w0, st, 0, 0, Fp, Tp, aug_lane);
     int buf = 0;
     for (int g = 0; g < n; g += 64) {
       const GroupLanes gn = group_lanes<WT, TS>(ip, vp, wp, tp, n, g + 64, zrow);
@@ -372,24 +396,72 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
         constexpr int s0 = b * STEPS;
         if constexpr (b % 2 == 0) {
           if constexpr (b + 1 < NB)
-            gather_block<DP, STEPS, AUG, WT, TS>(a1, r1, w1, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a0, r0, w0, s0, steps, corner, cx, cy);
+            gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a1, b1, r1, w1, st, buf, s0 + STEPS, Fp,
+                                                        Tp, aug_lane);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a0, b0, r0, w0, s0,
+                                                       steps, corner, cx, cy);
         } else {
           if constexpr (b + 1 < NB) {
-            gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf, s0 + STEPS, Fp, Tp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a0, b0, r0, w0, st, buf, s0 + STEPS, Fp,
+                                                        Tp, aug_lane);
           } else {
             // the next group goes to the other buffer, then its first block is gathered
             stage_group<WT, TS>(st, buf ^ 1, gn);
             wave_sync();
-            gather_block<DP, STEPS, AUG, WT, TS>(a0, r0, w0, st, buf ^ 1, 0, Fp, Tp, aug_lane);
+            gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a0, b0, r0, w0, st, buf ^ 1, 0, Fp, Tp,
+                                                        aug_lane);
           }
-          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a1, r1, w1, s0, steps, corner, cx, cy);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a1, b1, r1, w1, s0,
+                                                       steps, corner, cx, cy);
         }
       };
       unroll_blocks<0, NB>(block);
       group_residuals(pi, st, buf, g, n, sse);
       buf ^= 1;
     }
+  }
+}
+
+// Whether the last tile of width DP uses only its first four features (D in
+// 16 (T - 1) + 1 .. 16 (T - 1) + 4, three or more tiles): then the strip form of
+// mma_block serves the last tile column, and the augmented column is feature
+// 16 (T - 1) + 4.
+template <int DP>
+__host__ __device__ constexpr bool strip_width(int D) {
+  return DP / 16 >= 3 && D > DP - 16 && D <= DP - 12;
+}
+
+// Finish a strip-form Gram (mma_block with STRIP): sum each strip of the last tile
+// column over the four rating groups and move it to the tile layout (lane (kq, c), c < 4,
+// element r: G[16 I + 4 kq + r][16 (T - 1) + c], taken from lane 4 kq + c of the summed
+// strip), and write the right-hand side (per-lane partials in rhs) into lane column aug_c
+// of the same tiles (element r: b[16 I + 4 kq + r], from lane 4 kq + r of the summed rhs).
+// The other lane columns of these tiles become zero.
+template <int DP>
+__device__ __forceinline__ void strip_finish(floatx4 (&acc)[RowCfg<DP>::NT],
+                                             float (&rhs)[DP / 16], int aug_c) {
+  constexpr int T = DP / 16;
+  const int lane = threadIdx.x & 63, kq = lane >> 4, c = lane & 15;
+  const int from_strip = 4 * (4 * kq + (c & 3));
+#pragma unroll
+  for (int I = 0; I < T; ++I) {
+    floatx4 s = acc[tidx<T>(I, T - 1)];
+    float b = rhs[I];
+    b += __shfl_xor(b, 16);
+    b += __shfl_xor(b, 32);
+    floatx4 out;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = s[r];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      const float sv = __builtin_bit_cast(
+          float, __builtin_amdgcn_ds_bpermute(from_strip, __builtin_bit_cast(int, v)));
+      const float bv = __builtin_bit_cast(
+          float, __builtin_amdgcn_ds_bpermute(4 * (4 * kq + r), __builtin_bit_cast(int, b)));
+      out[r] = c < 4 ? sv : (c == aug_c ? bv : 0.f);
+    }
+    acc[tidx<T>(I, T - 1)] = out;
   }
 }
 

@@ -18,6 +18,10 @@
 // Rows with more ratings than the hub threshold have their normal equations
 // built by several wavefronts (k_gram_chunks, partials in a workspace) and are
 // only summed and solved here.
+// STRIP (the last tile holds four used features, D = 16 (T - 1) + 1 .. + 4): the
+// Gram's last tile column is accumulated as 4x4 strips (v_mfma_f32_4x4x1f32) and the
+// right-hand side on VALU, and both are moved into the augmented tile layout before
+// the factorisation, which is the same as without STRIP.
 //
 // Register layout: lane (kq, c) = (lane / 16, lane % 16). Gram operand block X
 // of rating k is feature 16 X + c of f_k in lane (k, c). Accumulator tile
@@ -66,7 +70,7 @@ __host__ __device__ constexpr int aug_column(int D) {
 
 // Partial normal equations of the chunks of split rows, with the chunks'
 // entering-state squared residuals.
-template <int DP, bool AUG, bool WT, bool TS>
+template <int DP, bool AUG, bool WT, bool TS, bool STRIP = false>
 __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__ items,
                                                     const int32_t *__restrict__ idx,
                                                     const uint8_t *__restrict__ val,
@@ -98,9 +102,11 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   const GroupLanes g0 =
       group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
   float no_corner = 0.f;
-  gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp,
-                                   it.len, Fp, hd.Tp, zrow, AUG ? aug_column<DP>(D) : -1,
-                                   s_stage, g0, no_corner, 0, 0);
+  const int aug_c = AUG ? aug_column<DP>(D) : -1;
+  gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
+      acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp, it.len, Fp, hd.Tp, zrow,
+      STRIP ? -1 : aug_c, s_stage, g0, no_corner, 0, 0);
+  if constexpr (STRIP) strip_finish<DP>(acc, rhs, aug_c);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ws + it.slot * (int64_t)slot_floats(DP);
@@ -138,7 +144,7 @@ constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 // alpha, identity on the padding, and Lambda mu / alpha in the right-hand side) and the
 // forward-substitution result y gets z / sqrt(alpha) before the back substitution, so
 // that the row receives the conditional draw mu* + L*^{-T} z.
-template <int DP, bool AUG, bool WT, bool BAYES, bool TS>
+template <int DP, bool AUG, bool WT, bool BAYES, bool TS, bool STRIP = false>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
     const uint8_t *__restrict__ val, const float *__restrict__ wts,
@@ -166,24 +172,30 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
 
   // A starts as lambda n_s I on the first D diagonal entries and I on the padding (only
   // the last tile holds padding); the Gram (or the sum of a split row's chunk partials)
-  // is accumulated on top
-  floatx4 acc[NT];
-  if constexpr (BAYES) {
+  // is accumulated on top. With STRIP the last tile column starts from zero (it holds
+  // strips during the Gram) and receives its initial value afterwards.
+  const float lam_n = (float)((double)lam * (double)rt.deg);
+  auto tile_init = [&](int I, int J) -> floatx4 {
+    if constexpr (BAYES) {
+      return *reinterpret_cast<const floatx4 *>(pr.init + tidx<T>(I, J) * 256 + lane * 4);
+    } else {
+      floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (I == J) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
-      acc[t] = *reinterpret_cast<const floatx4 *>(pr.init + t * 256 + lane * 4);
-  } else {
-    const float lam_n = (float)((double)lam * (double)rt.deg);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int I = 0; I < T; ++I) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int d = 16 * I + 4 * kq + r;
-        acc[tidx<T>(I, I)][r] = c == 4 * kq + r ? ((I < T - 1 || d < D) ? lam_n : 1.f) : 0.f;
+        for (int r = 0; r < 4; ++r) {
+          const int d = 16 * I + 4 * kq + r;
+          v[r] = c == 4 * kq + r ? ((I < T - 1 || d < D) ? lam_n : 1.f) : 0.f;
+        }
       }
+      return v;
     }
+  };
+  floatx4 acc[NT];
+#pragma unroll
+  for (int I = 0; I < T; ++I) {
+#pragma unroll
+    for (int J = I; J < T; ++J)
+      acc[tidx<T>(I, J)] = (STRIP && J == T - 1) ? floatx4{0.f, 0.f, 0.f, 0.f} : tile_init(I, J);
   }
   float rhs[T];
 #pragma unroll
@@ -203,9 +215,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const GroupLanes g0 =
         group_lanes<WT, TS>(idx + rt.start, val + rt.start, wp, tp, rt.deg, 0, zrow);
     float no_corner = 0.f;
-    gram_accumulate<DP, AUG, WT, TS>(acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp,
-                                     rt.deg, Fp, hd.Tp, zrow, aug_c, s_stage[wv], g0, no_corner,
-                                     0, 0);
+    gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
+        acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp, rt.deg, Fp, hd.Tp, zrow,
+        STRIP ? -1 : aug_c, s_stage[wv], g0, no_corner, 0, 0);
+    if constexpr (STRIP) strip_finish<DP>(acc, rhs, aug_c);
     if constexpr (!AUG) {
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -227,6 +240,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
         for (int X = 0; X < T; ++X) rhs[X] += sl[NT * 256 + 16 * X + c];
       }
     }
+  }
+  if constexpr (STRIP) {
+#pragma unroll
+    for (int I = 0; I < T; ++I) acc[tidx<T>(I, T - 1)] += tile_init(I, T - 1);
   }
   if constexpr (BAYES && !AUG) {
     // the prior's right-hand side (with the augmented column it sits in the tiles)
@@ -444,15 +461,24 @@ static constexpr bool has_aug(int D) {
   return ((D + 3) & ~3) < DP;
 }
 
-template <int DP, bool AUG, bool WT, bool BAYES, bool TS = false>
+template <int DP, bool AUG, bool WT, bool BAYES, bool TS = false, bool STRIP = false>
 static void launch_rows_k(int64_t blocks, const RowTask *rows, int64_t n_rows,
                           const int32_t *idx, const uint8_t *val, const float *wts,
                           const float *Fp, int zrow, const float *ws, int D, float lam, float *X,
                           double *sse, int32_t *flag, double *cyc_gram, double *cyc_solve,
                           const RowPrior &pr, const Hadamard &hd, hipStream_t s) {
-  hipLaunchKernelGGL((k_rows<DP, AUG, WT, BAYES, TS>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((k_rows<DP, AUG, WT, BAYES, TS, STRIP>), dim3((unsigned)blocks),
                      dim3(64 * kRowWaves), 0, s, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
                      lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd);
+}
+
+// The augmented variants, in strip form where the last tile uses four features.
+template <int DP, bool WT, bool BAYES, bool TS, class... A>
+static void launch_rows_aug(bool strip, A &&...args) {
+  if constexpr (DP >= 48) {
+    if (strip) return launch_rows_k<DP, true, WT, BAYES, TS, true>(args...);
+  }
+  launch_rows_k<DP, true, WT, BAYES, TS, false>(args...);
 }
 
 template <int DP>
@@ -463,49 +489,51 @@ static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32
                                 const RowPrior &pr, const Hadamard &hd, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int64_t blocks = (n_rows + kRowWaves - 1) / kRowWaves;
-  const bool aug = has_aug<DP>(D), wt = wts != nullptr;
+  const bool aug = has_aug<DP>(D), wt = wts != nullptr, strip = strip_width<DP>(D);
+#define ROW_ARGS blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag, \
+                 cyc_gram, cyc_solve, pr, hd, s
   if (hd.idx2) {
-    // tensor ALS: no weights, no Bayesian prior
+    // tensor ALS: no weights, no Bayesian prior; the tile form throughout (the strip
+    // form of its Gram runs out of registers)
     if (wt || pr.init) return hipErrorInvalidValue;
     if (aug)
-      launch_rows_k<DP, true, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow,
-                                                  ws, D, lam, X, sse, flag, cyc_gram, cyc_solve,
-                                                  pr, hd, s);
+      launch_rows_k<DP, true, false, false, true>(ROW_ARGS);
     else
-      launch_rows_k<DP, false, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow,
-                                                   ws, D, lam, X, sse, flag, cyc_gram, cyc_solve,
-                                                   pr, hd, s);
+      launch_rows_k<DP, false, false, false, true>(ROW_ARGS);
   } else if (pr.init) {
     // the Gibbs half-sweep has no per-rating weights
     if (wt) return hipErrorInvalidValue;
     if (aug)
-      launch_rows_k<DP, true, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+      launch_rows_aug<DP, false, true, false>(strip, ROW_ARGS);
     else
-      launch_rows_k<DP, false, false, true>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                            lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+      launch_rows_k<DP, false, false, true>(ROW_ARGS);
   } else if (aug && wt)
-    launch_rows_k<DP, true, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                         lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+    launch_rows_aug<DP, true, false, false>(strip, ROW_ARGS);
   else if (aug)
-    launch_rows_k<DP, true, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+    launch_rows_aug<DP, false, false, false>(strip, ROW_ARGS);
   else if (wt)
-    launch_rows_k<DP, false, true, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                          lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+    launch_rows_k<DP, false, true, false>(ROW_ARGS);
   else
-    launch_rows_k<DP, false, false, false>(blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D,
-                                           lam, X, sse, flag, cyc_gram, cyc_solve, pr, hd, s);
+    launch_rows_k<DP, false, false, false>(ROW_ARGS);
+#undef ROW_ARGS
   return hipGetLastError();
 }
 
-template <int DP, bool AUG, bool WT, bool TS = false>
+template <int DP, bool AUG, bool WT, bool TS = false, bool STRIP = false>
 static void launch_chunks_k(int64_t n, const WorkItem *items, const int32_t *idx,
                             const uint8_t *val, const float *wts, const float *Fp, int zrow,
                             const float *Xold, int D, float *ws, double *sse, const Hadamard &hd,
                             hipStream_t s) {
-  hipLaunchKernelGGL((k_gram_chunks<DP, AUG, WT, TS>), dim3((unsigned)n), dim3(64), 0, s, items,
-                     idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd);
+  hipLaunchKernelGGL((k_gram_chunks<DP, AUG, WT, TS, STRIP>), dim3((unsigned)n), dim3(64), 0, s,
+                     items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd);
+}
+
+template <int DP, bool WT, bool TS, class... A>
+static void launch_chunks_aug(bool strip, A &&...args) {
+  if constexpr (DP >= 48) {
+    if (strip) return launch_chunks_k<DP, true, WT, TS, true>(args...);
+  }
+  launch_chunks_k<DP, true, WT, TS, false>(args...);
 }
 
 template <int DP>
@@ -514,23 +542,23 @@ static hipError_t launch_chunks_t(const WorkItem *items, int64_t n, const int32_
                                   int zrow, const float *Xold, int D, float *ws, double *sse,
                                   const Hadamard &hd, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const bool aug = has_aug<DP>(D), wt = wts != nullptr;
+  const bool aug = has_aug<DP>(D), wt = wts != nullptr, strip = strip_width<DP>(D);
+#define CHUNK_ARGS n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s
   if (hd.idx2) {
     if (wt) return hipErrorInvalidValue;
     if (aug)
-      launch_chunks_k<DP, true, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse,
-                                             hd, s);
+      launch_chunks_k<DP, true, false, true>(CHUNK_ARGS);
     else
-      launch_chunks_k<DP, false, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse,
-                                              hd, s);
+      launch_chunks_k<DP, false, false, true>(CHUNK_ARGS);
   } else if (aug && wt)
-    launch_chunks_k<DP, true, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
+    launch_chunks_aug<DP, true, false>(strip, CHUNK_ARGS);
   else if (aug)
-    launch_chunks_k<DP, true, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
+    launch_chunks_aug<DP, false, false>(strip, CHUNK_ARGS);
   else if (wt)
-    launch_chunks_k<DP, false, true>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
+    launch_chunks_k<DP, false, true>(CHUNK_ARGS);
   else
-    launch_chunks_k<DP, false, false>(n, items, idx, val, wts, Fp, zrow, Xold, D, ws, sse, hd, s);
+    launch_chunks_k<DP, false, false>(CHUNK_ARGS);
+#undef CHUNK_ARGS
   return hipGetLastError();
 }
 

@@ -98,14 +98,25 @@ def test_tensor_split_rows_and_batches(D):
     check_modes(M, N, n_bins, ptr, col, val, bins, U, V, T, D, 0.065, tuning=tun, label="split")
 
 
-@pytest.mark.parametrize("D", [20, 100])
-def test_unit_time_factors_are_matrix_als_bitwise(D):
+def strip_width(D):
+    """Widths whose matrix Gram takes the strip form (the last 16-feature tile uses at most
+    four features, three or more tiles); the tensor Gram keeps the tile form, so there the
+    two sum the last tile column in different orders."""
+    T = (D + 15) // 16
+    return T >= 3 and D - 16 * (T - 1) <= 4
+
+
+@pytest.mark.parametrize("D", [20, 64, 100])
+def test_unit_time_factors_are_matrix_als(D):
+    """Bit for bit where both Grams take the same form; at the strip widths the rows agree
+    to fp32 summation-order rounding (relative 1e-5, far inside the 1e-4 bar)."""
     from paper_1108_2580_amd import ALS
 
     M, N, n_bins = 250, 180, 12
     ptr, col, val, bins, U, V, _ = tensor_problem(M, N, n_bins, D, 900 + D)
     ones = np.ones((n_bins, D), dtype=np.float32)
-    log(f"tensor with unit time factors D={D}")
+    exact = not strip_width(D)
+    log(f"tensor with unit time factors D={D} exact={exact}")
     with ALS(M, N, ptr, col, val, D) as als:
         als.set_time_bins(n_bins, bins)
         for mode, side, fixed, X in (("users", "users", V, U), ("items", "items", U, V)):
@@ -114,7 +125,11 @@ def test_unit_time_factors_are_matrix_als_bitwise(D):
             xt = (Ud if mode == "users" else Vd).cpu().numpy()
             out = dev(X)
             als.half_sweep(side, dev(fixed), 0.065, out)
-            assert np.array_equal(xt, out.cpu().numpy())
+            xm = out.cpu().numpy()
+            if exact:
+                assert np.array_equal(xt, xm)
+            else:
+                assert rel_rows(xt, xm).max() <= 1e-5
         r_t = als.tensor_rmse(dev(U), dev(V), dev(ones))
         r_m = als.rmse(dev(U), dev(V))
         assert r_t == r_m
