@@ -82,6 +82,12 @@ def _configure(lib):
     lib.orc_predict.restype = None
     lib.orc_pair_sse.argtypes = [i64, P, P, P, i32, P, P, c_int]
     lib.orc_pair_sse.restype = f64
+    lib.orc_tensor_gibbs_rows.argtypes = [i64, P, P, P, P, i32, P, P, f64, P, P, P, P, P, c_int]
+    lib.orc_tensor_gibbs_rows.restype = i64
+    lib.orc_time_rows.argtypes = [i64, P, P, P, P, i32, P, P, f64, P, P, P, i32, P, P, c_int]
+    lib.orc_time_rows.restype = i64
+    lib.orc_time_posterior.argtypes = [i64, i32, P, P, f64, P, f64, P, P, P, P]
+    lib.orc_time_posterior.restype = None
     return lib
 
 
@@ -414,3 +420,133 @@ class TensorTrajectory:
         p, i1, i2, v = self.by_user
         return float(np.sqrt(tensor_sse(p, i1, i2, v, self.U, self.V, self.T, self.threads)
                              / self.nnz)) if self.nnz else 0.0
+
+
+# ---- BPTF: the tensor model's Gibbs step (time factors as a Markov chain) -----------------------
+
+def _tensor_args(ptr, idx1, idx2, val, F1, F2):
+    ptr, idx1, idx2, val = _i64(ptr), _i32(idx1), _i32(idx2), _f64(val)
+    F1, F2 = _f64(F1), _f64(F2)
+    if F1.shape[1] != F2.shape[1]:
+        raise ValueError("F1 and F2 differ in width")
+    if idx1.size and (idx1.min() < 0 or idx1.max() >= F1.shape[0] or idx2.min() < 0
+                      or idx2.max() >= F2.shape[0]):
+        raise ValueError("index out of range")
+    return ptr, idx1, idx2, val, F1, F2
+
+
+def tensor_gibbs_rows(ptr, idx1, idx2, val, F1, F2, alpha, Lam, mu, z, X_prev, threads=0):
+    """Conditional draw of every user (or item) row of the tensor model: fixed vectors
+    F1[idx1] * F2[idx2], prior N(mu, Lambda^{-1}), rating precision alpha.
+    Returns (X, flags); flagged rows keep X_prev."""
+    ptr, idx1, idx2, val, F1, F2 = _tensor_args(ptr, idx1, idx2, val, F1, F2)
+    Lam, mu, z = _f64(Lam), _f64(mu), _f64(z)
+    n_rows, D = ptr.size - 1, F1.shape[1]
+    if Lam.shape != (D, D) or mu.shape != (D,) or z.shape != (n_rows, D):
+        raise ValueError("Lambda must be D x D, mu of length D, z n_rows x D")
+    X = np.array(X_prev, dtype=np.float64, order="C", copy=True)
+    assert X.shape == (n_rows, D)
+    flags = np.empty(n_rows, dtype=np.int8)
+    _load().orc_tensor_gibbs_rows(n_rows, _p(ptr), _p(idx1), _p(idx2), _p(val), D, _p(F1),
+                                  _p(F2), float(alpha), _p(Lam), _p(mu), _p(z), _p(X),
+                                  _p(flags), int(threads))
+    return X, flags
+
+
+def time_rows(ptr, idx1, idx2, val, F1, F2, alpha, Lam_T, mu_T, z, parity, T_prev, threads=0):
+    """Conditional draw of the time bins of one parity (0: bins 0, 2, ...; 1: bins 1, 3, ...)
+    under the Markov-chain prior, the other bins fixed. Returns (T, flags); bins of the
+    other parity and flagged bins keep T_prev (their flags are 0)."""
+    ptr, idx1, idx2, val, F1, F2 = _tensor_args(ptr, idx1, idx2, val, F1, F2)
+    Lam_T, mu_T, z = _f64(Lam_T), _f64(mu_T), _f64(z)
+    K, D = ptr.size - 1, F1.shape[1]
+    if K < 1 or Lam_T.shape != (D, D) or mu_T.shape != (D,) or z.shape != (K, D):
+        raise ValueError("need K >= 1, Lambda_T D x D, mu_T of length D, z K x D")
+    if parity not in (0, 1):
+        raise ValueError("parity is 0 or 1")
+    T = np.array(T_prev, dtype=np.float64, order="C", copy=True)
+    assert T.shape == (K, D)
+    flags = np.zeros(K, dtype=np.int8)
+    _load().orc_time_rows(K, _p(ptr), _p(idx1), _p(idx2), _p(val), D, _p(F1), _p(F2),
+                          float(alpha), _p(Lam_T), _p(mu_T), _p(z), int(parity), _p(T),
+                          _p(flags), int(threads))
+    return T, flags
+
+
+def time_posterior(T, mu0, beta0, W0inv, nu0):
+    """Normal-Wishart posterior of (mu_T, Lambda_T) given the chain T (K x D):
+    (mu*, beta*, W*^{-1}, nu*)."""
+    T, mu0, W0inv = _f64(T), _f64(mu0), _f64(W0inv)
+    K, D = T.shape
+    if K < 1:
+        raise ValueError("the chain needs at least one bin")
+    mu_s = np.empty(D)
+    Winv = np.empty((D, D))
+    b = ctypes.c_double()
+    v = ctypes.c_double()
+    _load().orc_time_posterior(K, D, _p(T), _p(mu0), float(beta0), _p(W0inv), float(nu0),
+                               _p(mu_s), _p(Winv), ctypes.byref(b), ctypes.byref(v))
+    return mu_s, b.value, Winv, v.value
+
+
+def alpha_posterior(sse, n, w0, nu0):
+    """Posterior of the rating precision alpha under its one-dimensional Wishart prior
+    W(w0, nu0) given the n residuals with sum of squares sse: W(w*, nu*) with
+    1 / w* = 1 / w0 + sse and nu* = nu0 + n. A draw is w* times a chi-square(nu*) variate."""
+    return 1.0 / (1.0 / float(w0) + float(sse)), float(nu0) + float(n)
+
+
+class BPTFChain:
+    """Free-running fp64 BPTF Gibbs sampler over (user, item, time bin) ratings. One
+    iteration, all variates supplied by the caller:
+      alpha from its posterior given the current U, V, T;
+      (mu, Lambda) of the items from V, of the users from U, and of the time chain from T;
+      the item rows, then the user rows, then the time bins (even, then odd)."""
+
+    def __init__(self, M, N, n_bins, row_ptr, col, bins, val, U0, V0, T0, threads=0):
+        self.t = TensorTrajectory(M, N, n_bins, row_ptr, col, bins, val, U0, V0, T0, 0.0,
+                                  threads)
+        self.threads = threads
+
+    @property
+    def U(self):
+        return self.t.U
+
+    @property
+    def V(self):
+        return self.t.V
+
+    @property
+    def T(self):
+        return self.t.T
+
+    def sse(self):
+        p, i1, i2, v = self.t.by_user
+        return tensor_sse(p, i1, i2, v, self.U, self.V, self.T, self.threads)
+
+    def iterate(self, alpha_prior, priors, variates):
+        """alpha_prior = (w0, nu0); priors = {"items"|"users"|"time": (mu0, beta0, W0inv,
+        nu0)}; variates = {"alpha_chi2": x, "hyper": {side: (chi2, offd, zmu)}, "z": {side:
+        array}}. Returns (alpha, {side: (mu, Lambda)})."""
+        t = self.t
+        w_s, _ = alpha_posterior(self.sse(), t.nnz, *alpha_prior)
+        alpha = w_s * float(variates["alpha_chi2"])
+        hyper = {}
+        for side, X in (("items", t.V), ("users", t.U), ("time", t.T)):
+            mu0, beta0, W0inv, nu0 = priors[side]
+            post = (time_posterior if side == "time" else nw_posterior)(X, mu0, beta0, W0inv, nu0)
+            drawn = nw_sample(post[0], post[1], post[2], *variates["hyper"][side])
+            if drawn is None:
+                raise FloatingPointError(f"Normal-Wishart draw failed for {side}")
+            hyper[side] = drawn
+        p, i1, i2, v = t.by_item
+        t.V, _ = tensor_gibbs_rows(p, i1, i2, v, t.U, t.T, alpha, hyper["items"][1],
+                                   hyper["items"][0], variates["z"]["items"], t.V, self.threads)
+        p, i1, i2, v = t.by_user
+        t.U, _ = tensor_gibbs_rows(p, i1, i2, v, t.V, t.T, alpha, hyper["users"][1],
+                                   hyper["users"][0], variates["z"]["users"], t.U, self.threads)
+        p, i1, i2, v = t.by_bin
+        for parity in (0, 1):
+            t.T, _ = time_rows(p, i1, i2, v, t.U, t.V, alpha, hyper["time"][1], hyper["time"][0],
+                               variates["z"]["time"], parity, t.T, self.threads)
+        return alpha, hyper

@@ -526,3 +526,164 @@ double orc_tensor_sse(int64_t n_rows, const int64_t *ptr, const int32_t *idx1, c
   free(per);
   return total;
 }
+
+/* ---- BPTF: draws under the tensor model, the time factors' Markov chain ------------------ */
+/*
+ * Bayesian probabilistic tensor factorisation (the BPTF of Sec. 2.2 and Table 3, the
+ * published sampler): the ratings are N(sum_d U_ud V_id T_td, 1/alpha); user and item rows
+ * have the Normal-Wishart-governed priors of the matrix model; the time factors form a
+ * Markov chain, T_0 ~ N(mu_T, Lambda_T^{-1}) and T_k ~ N(T_{k-1}, Lambda_T^{-1}) for
+ * k >= 1, with (mu_T, Lambda_T) Normal-Wishart; and alpha has a one-dimensional Wishart
+ * (scaled chi-square) prior.
+ *
+ * A row's full conditional is Gaussian with precision P = P0 + alpha sum_q f_q f_q^T and
+ * P mean = h0 + alpha sum_q r_q f_q, where f_q is the elementwise product of the rating's
+ * rows of the other two modes, and (P0, h0) come from the row's prior:
+ *   user or item row:  P0 = Lambda,  h0 = Lambda mu;
+ *   time bin k of K:   P0 = c_k Lambda_T with c_k = 2 if k < K - 1 (the bin is also the
+ *                      condition of bin k + 1) and 1 for the last bin, and
+ *                      h0 = Lambda_T (m_k + [k < K - 1] T_{k+1}) with m_k = mu_T for k = 0
+ *                      and T_{k-1} otherwise.
+ * The draw is x = L^{-T} (L^{-1} (P mean) + z) with P = L L^T.
+ */
+
+/* One draw as above. f_q = F1[idx1[q]] * F2[idx2[q]] over the row's n ratings; A, L, h, y
+ * and xs are D x D / D scratch. Returns 0 (x_out written) or 1 (P not numerically SPD or a
+ * non-finite result; x_out untouched). */
+static int draw_tensor_row(int32_t D, int64_t n, const int32_t *idx1, const int32_t *idx2,
+                           const double *val, const double *F1, const double *F2, double alpha,
+                           const double *P0, const double *h0, const double *z, double *A,
+                           double *L, double *h, double *y, double *xs, double *x_out) {
+  for (int32_t a = 0; a < D * D; ++a) A[a] = 0.0;
+  for (int32_t a = 0; a < D; ++a) h[a] = 0.0;
+  for (int64_t q = 0; q < n; ++q) {
+    const double *f1 = F1 + (int64_t)idx1[q] * D;
+    const double *f2 = F2 + (int64_t)idx2[q] * D;
+    for (int32_t a = 0; a < D; ++a) {
+      const double fa = f1[a] * f2[a];
+      for (int32_t e = 0; e < D; ++e) A[a * D + e] += fa * (f1[e] * f2[e]);
+      h[a] += val[q] * fa;
+    }
+  }
+  for (int32_t a = 0; a < D; ++a) {
+    h[a] = alpha * h[a] + h0[a];
+    for (int32_t e = 0; e < D; ++e) A[a * D + e] = alpha * A[a * D + e] + P0[a * D + e];
+  }
+  if (chol_lower(D, A, L) != 0) return 1;
+  solve_lower(D, L, h, y);
+  for (int32_t a = 0; a < D; ++a) y[a] += z[a];
+  solve_lower_t(D, L, y, xs);
+  for (int32_t a = 0; a < D; ++a) {
+    if (!isfinite(xs[a])) return 1;
+  }
+  for (int32_t a = 0; a < D; ++a) x_out[a] = xs[a];
+  return 0;
+}
+
+/* Conditional draw of every user (or item) row under the tensor model, prior N(mu,
+ * Lambda^{-1}); z is n_rows x D. flags[s]: 0 drawn, 1 left unchanged. Returns the number of
+ * flagged rows. */
+int64_t orc_tensor_gibbs_rows(int64_t n_rows, const int64_t *ptr, const int32_t *idx1,
+                              const int32_t *idx2, const double *val, int32_t D,
+                              const double *F1, const double *F2, double alpha,
+                              const double *Lambda, const double *mu, const double *z, double *X,
+                              int8_t *flags, int nthreads) {
+  set_threads(nthreads);
+  double *h0 = (double *)malloc(sizeof(double) * D);
+  for (int32_t a = 0; a < D; ++a) {
+    double t = 0.0;
+    for (int32_t e = 0; e < D; ++e) t += Lambda[a * D + e] * mu[e];
+    h0[a] = t;
+  }
+  int64_t nflag = 0;
+#pragma omp parallel reduction(+ : nflag)
+  {
+    double *A = (double *)malloc(sizeof(double) * D * D);
+    double *L = (double *)malloc(sizeof(double) * D * D);
+    double *h = (double *)malloc(sizeof(double) * D);
+    double *y = (double *)malloc(sizeof(double) * D);
+    double *xs = (double *)malloc(sizeof(double) * D);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t s = 0; s < n_rows; ++s) {
+      const int st = draw_tensor_row(D, ptr[s + 1] - ptr[s], idx1 + ptr[s], idx2 + ptr[s],
+                                     val + ptr[s], F1, F2, alpha, Lambda, h0, z + s * D, A, L, h,
+                                     y, xs, X + s * D);
+      if (flags) flags[s] = (int8_t)st;
+      nflag += st;
+    }
+    free(A); free(L); free(h); free(y); free(xs);
+  }
+  free(h0);
+  return nflag;
+}
+
+/* Conditional draw of the time bins k = parity, parity + 2, ... (of K) given the bins of the
+ * other parity; the other bins are read, never written. Bins of one parity are conditionally
+ * independent given the rest (each conditional involves only the two neighbours), so one call
+ * per parity, even then odd, is one Gibbs sweep over the chain. z is K x D (rows of the drawn
+ * bins used). flags[k] for the drawn bins as above. Returns the number of flagged bins. */
+int64_t orc_time_rows(int64_t K, const int64_t *ptr, const int32_t *idx1, const int32_t *idx2,
+                      const double *val, int32_t D, const double *F1, const double *F2,
+                      double alpha, const double *Lambda_T, const double *mu_T, const double *z,
+                      int32_t parity, double *T, int8_t *flags, int nthreads) {
+  set_threads(nthreads);
+  int64_t nflag = 0;
+#pragma omp parallel reduction(+ : nflag)
+  {
+    double *A = (double *)malloc(sizeof(double) * D * D);
+    double *L = (double *)malloc(sizeof(double) * D * D);
+    double *P0 = (double *)malloc(sizeof(double) * D * D);
+    double *h = (double *)malloc(sizeof(double) * D);
+    double *h0 = (double *)malloc(sizeof(double) * D);
+    double *nb = (double *)malloc(sizeof(double) * D);
+    double *y = (double *)malloc(sizeof(double) * D);
+    double *xs = (double *)malloc(sizeof(double) * D);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t k = parity; k < K; k += 2) {
+      const double ck = k < K - 1 ? 2.0 : 1.0;
+      for (int32_t a = 0; a < D; ++a) {
+        const double prev = k == 0 ? mu_T[a] : T[(k - 1) * D + a];
+        const double next = k < K - 1 ? T[(k + 1) * D + a] : 0.0;
+        nb[a] = prev + next;
+      }
+      for (int32_t a = 0; a < D; ++a) {
+        double t = 0.0;
+        for (int32_t e = 0; e < D; ++e) {
+          t += Lambda_T[a * D + e] * nb[e];
+          P0[a * D + e] = ck * Lambda_T[a * D + e];
+        }
+        h0[a] = t;
+      }
+      const int st = draw_tensor_row(D, ptr[k + 1] - ptr[k], idx1 + ptr[k], idx2 + ptr[k],
+                                     val + ptr[k], F1, F2, alpha, P0, h0, z + k * D, A, L, h, y,
+                                     xs, T + k * D);
+      if (flags) flags[k] = (int8_t)st;
+      nflag += st;
+    }
+    free(A); free(L); free(P0); free(h); free(h0); free(nb); free(y); free(xs);
+  }
+  return nflag;
+}
+
+/* Normal-Wishart posterior of (mu_T, Lambda_T) given the chain T (K x D, K >= 1) and the prior
+ * (mu0, beta0, W0^{-1}, nu0): T_0 is one draw around mu_T and each step T_k - T_{k-1} one
+ * zero-mean draw, so
+ *   beta* = beta0 + 1,  nu* = nu0 + K,  mu0* = (beta0 mu0 + T_0) / (beta0 + 1),
+ *   W*^{-1} = W0^{-1} + sum_{k>=1} (T_k - T_{k-1})(T_k - T_{k-1})^T
+ *             + beta0 / (beta0 + 1) (T_0 - mu0)(T_0 - mu0)^T. */
+void orc_time_posterior(int64_t K, int32_t D, const double *T, const double *mu0, double beta0,
+                        const double *W0inv, double nu0, double *mu_s, double *Winv_s,
+                        double *beta_s, double *nu_s) {
+  const double w1 = beta0 / (beta0 + 1.0);
+  for (int32_t a = 0; a < D; ++a) {
+    for (int32_t e = 0; e < D; ++e) {
+      double steps = 0.0;
+      for (int64_t k = 1; k < K; ++k)
+        steps += (T[k * D + a] - T[(k - 1) * D + a]) * (T[k * D + e] - T[(k - 1) * D + e]);
+      Winv_s[a * D + e] = W0inv[a * D + e] + steps + w1 * (T[a] - mu0[a]) * (T[e] - mu0[e]);
+    }
+    mu_s[a] = (beta0 * mu0[a] + T[a]) / (beta0 + 1.0);
+  }
+  *beta_s = beta0 + 1.0;
+  *nu_s = nu0 + (double)K;
+}

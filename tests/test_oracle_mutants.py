@@ -13,6 +13,7 @@ from tests import test_oracle_weighted_pins as wpins
 from tests import test_oracle_predict_pins as qpins
 from tests import test_oracle_bayes_pins as bpins
 from tests import test_oracle_tensor_pins as tpins
+from tests import test_oracle_bptf_pins as btpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "als_oracle.c")
 
@@ -64,12 +65,43 @@ MUTANTS = [
      "const double *f2 = F2 + (int64_t)idx2[ptr[s]] * D;"),
     ("tensor_sse_without_time", "for (int32_t a = 0; a < D; ++a) pred += X[s * D + a] * f1[a] * f2[a];",
      "for (int32_t a = 0; a < D; ++a) pred += X[s * D + a] * f1[a];"),
+    ("bptf_second_factor_dropped", "const double fa = f1[a] * f2[a];", "const double fa = f1[a];"),
+    ("bptf_prior_linear_term_dropped", "h[a] = alpha * h[a] + h0[a];", "h[a] = alpha * h[a];"),
+    ("bptf_noise_not_added", "for (int32_t a = 0; a < D; ++a) y[a] += z[a];",
+     "for (int32_t a = 0; a < D; ++a) y[a] += 0.0 * z[a];"),
+    ("time_last_bin_doubled", "const double ck = k < K - 1 ? 2.0 : 1.0;", "const double ck = 2.0;"),
+    ("time_interior_bin_single", "const double ck = k < K - 1 ? 2.0 : 1.0;",
+     "const double ck = k < K - 1 ? 1.0 : 1.0;"),
+    ("time_first_bin_without_mean", "const double prev = k == 0 ? mu_T[a] : T[(k - 1) * D + a];",
+     "const double prev = k == 0 ? 0.0 : T[(k - 1) * D + a];"),
+    ("time_next_neighbour_dropped", "const double next = k < K - 1 ? T[(k + 1) * D + a] : 0.0;",
+     "const double next = 0.0;"),
+    ("time_parity_stride_one", "for (int64_t k = parity; k < K; k += 2) {",
+     "for (int64_t k = parity; k < K; k += 1) {"),
+    ("time_posterior_steps_not_differenced",
+     "steps += (T[k * D + a] - T[(k - 1) * D + a]) * (T[k * D + e] - T[(k - 1) * D + e]);",
+     "steps += T[k * D + a] * T[k * D + e];"),
+    ("time_posterior_first_step_dropped", "for (int64_t k = 1; k < K; ++k)\n        steps +=",
+     "for (int64_t k = 2; k < K; ++k)\n        steps +="),
+    ("time_posterior_shrink_dropped", "+ steps + w1 * (T[a] - mu0[a]) * (T[e] - mu0[e]);", "+ steps;"),
+    ("time_posterior_mean_unshrunk", "mu_s[a] = (beta0 * mu0[a] + T[a]) / (beta0 + 1.0);",
+     "mu_s[a] = T[a];"),
+    ("time_posterior_dof_per_row", "*nu_s = nu0 + (double)K;", "*nu_s = nu0 + 1.0;"),
     ("pair_error_sign", "const double e = r[p] - pred[p];", "const double e = r[p] + pred[p];"),
     ("pair_sse_first_dropped", "for (int64_t p = 0; p < n; ++p) {\n    const double e",
      "for (int64_t p = 1; p < n; ++p) {\n    const double e"),
 ]
 
 PIN_TESTS = [
+    lambda: btpins.test_bt1_unit_time_factors_give_the_matrix_draw(4),
+    btpins.test_bt2_tensor_row_uses_the_elementwise_product,
+    lambda: btpins.test_bt3_bins_are_the_joint_gaussians_conditionals(5, 3),
+    lambda: btpins.test_bt3_bins_are_the_joint_gaussians_conditionals(8, 2),
+    btpins.test_bt4_single_bin_chain_is_the_matrix_prior_draw,
+    btpins.test_bt5_empty_interior_bin_without_noise_is_the_neighbours_mean,
+    lambda: btpins.test_bt6_time_posterior_is_conjugate(4, 2),
+    lambda: btpins.test_bt6_time_posterior_is_conjugate(9, 3),
+    btpins.test_bt7_one_bin_posterior_is_the_one_row_posterior,
     tpins.test_t1_unit_time_factors_give_matrix_als,
     lambda: tpins.test_t2_matches_least_squares_on_the_product_design(3),
     tpins.test_t3_objective_gradient_vanishes_after_each_mode,
