@@ -315,6 +315,69 @@ als_status als_tensor_half_sweep(als_ctx *ctx, als_mode mode, float *U, float *V
 als_status als_tensor_rmse(als_ctx *ctx, const float *U, const float *V, const float *T,
                            double *rmse_out);
 
+/*
+ * BPTF, the Bayesian tensor factorisation of paper Sec. 2.2 and Table 3, as the published
+ * Gibbs sampler: the ratings are N(sum_d U[u][d] V[i][d] T[t][d], 1 / alpha); user and
+ * item rows have the Normal-Wishart-governed priors N(mu, Lambda^{-1}) of the Gibbs
+ * half-sweep; the time factors form a Markov chain, T[0] ~ N(mu_T, Lambda_T^{-1}) and
+ * T[k] ~ N(T[k-1], Lambda_T^{-1}), with (mu_T, Lambda_T) Normal-Wishart; and alpha has a
+ * one-dimensional Wishart prior W(w0, nu0) (w0 times a chi-square with nu0 degrees of
+ * freedom). One iteration: als_tensor_sample_alpha; the hyperparameters of the items and
+ * users (als_sample_hyper on V and U) and of the chain (als_sample_time_hyper); then
+ * als_tensor_gibbs_half_sweep for the items, the users and the time bins.
+ *
+ * als_set_time_nw_prior: the chain's Normal-Wishart hyperprior, arguments as for
+ * als_set_nw_prior.
+ */
+als_status als_set_time_nw_prior(als_ctx *ctx, const double *mu0, double beta0,
+                                 const double *W0_inv, double nu0);
+
+/*
+ * Draw (mu_T, Lambda_T) from the chain's Normal-Wishart posterior given T (device fp32
+ * [n_bins x D]): T[0] is one draw around mu_T and every step T[k] - T[k-1] a zero-mean
+ * draw, so beta* = beta0 + 1, nu* = nu0 + n_bins, mu0* = (beta0 mu0 + T[0]) / beta*, and
+ * W*^{-1} = W0^{-1} + sum_{k>=1} (T[k] - T[k-1])(T[k] - T[k-1])^T
+ *           + beta0 / beta* (T[0] - mu0)(T[0] - mu0)^T;
+ * then Bartlett's draw with the variates, all as for als_sample_hyper (chi2[i] with
+ * nu* - i degrees of freedom). The steps are differenced in fp64. ALS_ERR_INVALID_ARG
+ * without time bins or without a chain prior.
+ */
+als_status als_sample_time_hyper(als_ctx *ctx, const float *T, const double *chi2,
+                                 const double *offdiag, const double *z_mu, double *mu_out,
+                                 double *Lambda_out, int32_t *status_out);
+
+/*
+ * One mode of the BPTF Gibbs step: every row of the mode's factor (buffers as for
+ * als_tensor_half_sweep) drawn from its Gaussian conditional given the other two modes,
+ * with the fixed vectors of als_tensor_half_sweep and precision
+ * P = P0 + alpha sum f f^T, mean P^{-1} (h0 + alpha sum r f), x = mean + L^{-T} z
+ * (P = L L^T):
+ *   ALS_MODE_USERS / ALS_MODE_ITEMS: P0 = Lambda, h0 = Lambda mu (Lambda, mu: device fp64,
+ *     e.g. from als_sample_hyper); rows without ratings are drawn from that prior.
+ *   ALS_MODE_TIME: Lambda, mu are the chain's (mu_T, Lambda_T); bin k has
+ *     P0 = 2 Lambda_T (Lambda_T for the last bin) and
+ *     h0 = Lambda_T (m_k + T[k+1]) with m_0 = mu_T, m_k = T[k-1], and no T[k+1] term for
+ *     the last bin. The even bins are drawn first, given the odd ones, then the odd bins
+ *     given the new even ones: the bins of one parity are conditionally independent, so
+ *     this is one Gibbs sweep over the chain. Bins without ratings are drawn from their
+ *     conditional in the same kernels.
+ *   alpha   rating precision, finite and > 0.
+ *   z       device fp32 [rows of the mode x D] standard normals.
+ * rmse_out (host, nullable): as for als_tensor_half_sweep. Flagged rows keep their values.
+ */
+als_status als_tensor_gibbs_half_sweep(als_ctx *ctx, als_mode mode, float *U, float *V, float *T,
+                                       float alpha, const double *Lambda, const double *mu,
+                                       const float *z, double *rmse_out);
+
+/*
+ * Draw the rating precision from its posterior given the three factors: with the sum of
+ * squared residuals sse over the stored ratings (computed on the device, fp64 sums),
+ * alpha = chi2 / (1 / w0 + sse), where chi2 (host) is drawn from the chi-square law with
+ * nu0 + nnz degrees of freedom. Synchronises; *alpha_out (host).
+ */
+als_status als_tensor_sample_alpha(als_ctx *ctx, const float *U, const float *V, const float *T,
+                                   double w0, double chi2, double *alpha_out);
+
 void als_destroy(als_ctx *ctx);
 
 const char *als_status_str(als_status s);

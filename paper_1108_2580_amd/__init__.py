@@ -30,6 +30,8 @@ EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_
            "als_set_phase_timing", "als_get_phase_cycles", "als_predict", "als_set_holdout",
            "als_holdout_rmse", "als_set_nw_prior", "als_sample_hyper", "als_gibbs_half_sweep",
            "als_set_time_bins", "als_tensor_half_sweep", "als_tensor_rmse",
+           "als_set_time_nw_prior", "als_sample_time_hyper", "als_tensor_gibbs_half_sweep",
+           "als_tensor_sample_alpha",
            "als_destroy", "als_status_str", "als_last_error")
 
 PHASES = ("stage", "gather", "solve", "residual", "reduce")
@@ -100,6 +102,15 @@ def _load_library(path=LIB_PATH):
     lib.als_tensor_half_sweep.restype = st
     lib.als_tensor_rmse.argtypes = [P, P, P, P, ctypes.POINTER(ctypes.c_double)]
     lib.als_tensor_rmse.restype = st
+    lib.als_set_time_nw_prior.argtypes = [P, P, f64, P, f64]
+    lib.als_set_time_nw_prior.restype = st
+    lib.als_sample_time_hyper.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(ctypes.c_int32)]
+    lib.als_sample_time_hyper.restype = st
+    lib.als_tensor_gibbs_half_sweep.argtypes = [P, st, P, P, P, f32, P, P, P,
+                                                ctypes.POINTER(ctypes.c_double)]
+    lib.als_tensor_gibbs_half_sweep.restype = st
+    lib.als_tensor_sample_alpha.argtypes = [P, P, P, P, f64, f64, ctypes.POINTER(ctypes.c_double)]
+    lib.als_tensor_sample_alpha.restype = st
     lib.als_destroy.argtypes = [P]
     lib.als_destroy.restype = None
     lib.als_status_str.argtypes = [st]
@@ -284,23 +295,22 @@ class ALS:
     # ---- Bayesian (BPMF / BPTF) Gibbs step ----------------------------------------------
 
     def set_nw_prior(self, side, mu0, beta0, W0_inv, nu0):
-        """Normal-Wishart hyperprior of one side (host arrays)."""
+        """Normal-Wishart hyperprior of one side, or of the time chain with side "time"
+        (host arrays)."""
         mu0 = np.ascontiguousarray(mu0, dtype=np.float64)
         W = np.ascontiguousarray(W0_inv, dtype=np.float64)
         if mu0.shape != (self.D,) or W.shape != (self.D, self.D):
             raise ValueError("mu0 must have D entries and W0_inv be D x D")
+        if side == "time":
+            self._check(lib.als_set_time_nw_prior(self._h, _np_ptr(mu0), float(beta0),
+                                                  _np_ptr(W), float(nu0)))
+            return
         self._check(lib.als_set_nw_prior(self._h, _SIDES[side], _np_ptr(mu0), float(beta0),
                                          _np_ptr(W), float(nu0)))
 
-    def sample_hyper(self, side, X, chi2, offdiag, z_mu, mu_out=None, Lambda_out=None,
-                     check=False):
-        """Draw (mu, Lambda) of ``side`` given its rows X; variates are fp64 CUDA tensors.
-        Returns (mu, Lambda) as fp64 CUDA tensors."""
+    def _hyper_args(self, device, chi2, offdiag, z_mu, mu_out, Lambda_out):
         import torch
 
-        sd = _SIDES[side]
-        n = self.M if sd == ALS_ROWS_USERS else self.N
-        xp = _dev_ptr(X, self.D, n, "X")
         D = self.D
         for t, name, size in ((chi2, "chi2", D), (offdiag, "offdiag", D * (D - 1) // 2),
                               (z_mu, "z_mu", D)):
@@ -308,15 +318,32 @@ class ALS:
                     t.dtype != torch.float64 or not t.is_contiguous() or t.numel() != size:
                 raise TypeError(f"{name} must be a contiguous fp64 CUDA tensor of {size} values")
         if mu_out is None:
-            mu_out = torch.empty(D, dtype=torch.float64, device=X.device)
+            mu_out = torch.empty(D, dtype=torch.float64, device=device)
         if Lambda_out is None:
-            Lambda_out = torch.empty((D, D), dtype=torch.float64, device=X.device)
+            Lambda_out = torch.empty((D, D), dtype=torch.float64, device=device)
+        return mu_out, Lambda_out
+
+    def sample_hyper(self, side, X, chi2, offdiag, z_mu, mu_out=None, Lambda_out=None,
+                     check=False):
+        """Draw (mu, Lambda) of ``side`` given its rows X, or with side "time" those of the
+        time chain given T; variates are fp64 CUDA tensors. Returns (mu, Lambda) as fp64
+        CUDA tensors."""
+        if side == "time":
+            tp = _dev_ptr(X, self.D, getattr(self, "n_bins", 0), "T")
+        else:
+            sd = _SIDES[side]
+            n = self.M if sd == ALS_ROWS_USERS else self.N
+            xp = _dev_ptr(X, self.D, n, "X")
+        mu_out, Lambda_out = self._hyper_args(X.device, chi2, offdiag, z_mu, mu_out, Lambda_out)
         status = ctypes.c_int32(0)
-        self._check(lib.als_sample_hyper(
-            self._h, sd, xp, ctypes.c_void_p(chi2.data_ptr()),
-            ctypes.c_void_p(offdiag.data_ptr()) if offdiag.numel() else None,
-            ctypes.c_void_p(z_mu.data_ptr()), ctypes.c_void_p(mu_out.data_ptr()),
-            ctypes.c_void_p(Lambda_out.data_ptr()), ctypes.byref(status) if check else None))
+        args = (ctypes.c_void_p(chi2.data_ptr()),
+                ctypes.c_void_p(offdiag.data_ptr()) if offdiag.numel() else None,
+                ctypes.c_void_p(z_mu.data_ptr()), ctypes.c_void_p(mu_out.data_ptr()),
+                ctypes.c_void_p(Lambda_out.data_ptr()), ctypes.byref(status) if check else None)
+        if side == "time":
+            self._check(lib.als_sample_time_hyper(self._h, tp, *args))
+        else:
+            self._check(lib.als_sample_hyper(self._h, sd, xp, *args))
         return mu_out, Lambda_out
 
     def gibbs_half_sweep(self, side, fixed, alpha, Lambda, mu, z, out, rmse=False,
@@ -375,6 +402,45 @@ class ALS:
         r = ctypes.c_double(0.0)
         self._check(lib.als_tensor_rmse(self._h, up, vp, tp, ctypes.byref(r)))
         return r.value
+
+    # ---- BPTF: the tensor model's Gibbs step -------------------------------------------------
+
+    def tensor_gibbs_half_sweep(self, mode, U, V, T, alpha, Lambda, mu, z, rmse=False,
+                                allow_flagged=False):
+        """Draw the rows of ``mode`` ("users", "items" or "bins") in place from their
+        conditionals given the other two factors; for "bins" (Lambda, mu) are the time
+        chain's and the bins are drawn even, then odd."""
+        import torch
+
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        nb = getattr(self, "n_bins", 0)
+        tp = _dev_ptr(T, self.D, nb, "T")
+        rows = {ALS_MODE_USERS: self.M, ALS_MODE_ITEMS: self.N, ALS_MODE_TIME: nb}[_MODES[mode]]
+        zp = _dev_ptr(z, self.D, rows, "z")
+        for t, name, shape in ((Lambda, "Lambda", (self.D, self.D)), (mu, "mu", (self.D,))):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or \
+                    t.dtype != torch.float64 or not t.is_contiguous() or tuple(t.shape) != shape:
+                raise TypeError(f"{name} must be a contiguous fp64 CUDA tensor of shape {shape}")
+        r = ctypes.c_double(0.0)
+        s = lib.als_tensor_gibbs_half_sweep(self._h, _MODES[mode], up, vp, tp, float(alpha),
+                                            ctypes.c_void_p(Lambda.data_ptr()),
+                                            ctypes.c_void_p(mu.data_ptr()), zp,
+                                            ctypes.byref(r) if rmse else None)
+        if s == ALS_ERR_NOT_SPD and allow_flagged:
+            return r.value
+        self._check(s)
+        return r.value if rmse else None
+
+    def tensor_sample_alpha(self, U, V, T, w0, chi2):
+        """Rating precision drawn from its posterior: chi2 / (1 / w0 + sse)."""
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        tp = _dev_ptr(T, self.D, getattr(self, "n_bins", 0), "T")
+        a = ctypes.c_double(0.0)
+        self._check(lib.als_tensor_sample_alpha(self._h, up, vp, tp, float(w0), float(chi2),
+                                                ctypes.byref(a)))
+        return a.value
 
     def close(self):
         if getattr(self, "_h", None):

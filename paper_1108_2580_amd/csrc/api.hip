@@ -81,7 +81,7 @@ struct als_ctx {
   uint8_t *d_val_t = nullptr;
   float *d_w = nullptr;    // weighted ALS: per-rating weights in CSR order (null: plain ALS)
   float *d_w_t = nullptr;  // the same weights in CSC order
-  SidePlan plan[3];  // users, items, and (tensor ALS) time bins
+  SidePlan plan[5];  // users, items, (tensor ALS) time bins, and the even / odd time bins
   float *d_ws = nullptr;
   size_t ws_bytes = 0;
   float *d_fpad = nullptr;       // staged fixed side [(max(M, N) + 1) x DP], last row zero
@@ -133,10 +133,16 @@ struct als_ctx {
   double *d_hyper_partials = nullptr;
   int32_t *d_hyper_status = nullptr;
   int32_t *h_hyper_status = nullptr;  // pinned
-  double *d_nw_mu0[2] = {nullptr, nullptr};    // Normal-Wishart hyperprior per side
-  double *d_nw_W0inv[2] = {nullptr, nullptr};
-  double nw_beta0[2] = {0, 0}, nw_nu0[2] = {0, 0};
-  bool nw_set[2] = {false, false};
+  // Normal-Wishart hyperprior per side: users, items, and (BPTF) the time chain
+  double *d_nw_mu0[3] = {nullptr, nullptr, nullptr};
+  double *d_nw_W0inv[3] = {nullptr, nullptr, nullptr};
+  double nw_beta0[3] = {0, 0, 0}, nw_nu0[3] = {0, 0, 0};
+  bool nw_set[3] = {false, false, false};
+  // BPTF time chain (allocated on first use)
+  float *d_time_h0 = nullptr;      // per-bin prior right-hand side [n_bins x D]
+  int64_t time_h0_bins = 0;
+  double *d_time_extra = nullptr;  // step scatter of the chain, D (D + 1) / 2
+  double *d_zero_mu = nullptr;     // D zeros (the chain's image has no mean term)
 };
 
 namespace {
@@ -198,7 +204,10 @@ void csc_blocking(int64_t n_users, int64_t n_items, int64_t &rows_per_blk, int64
   nblk = (n_users + rows_per_blk - 1) / rows_per_blk;
 }
 
-als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr) {
+// parity >= 0: only the rows s with s % 2 == parity, and those without ratings are
+// scheduled like the others (the time chain's bins, whose prior depends on the row).
+als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr,
+                      int parity = -1) {
   const int64_t n_rows = (int64_t)ptr.size() - 1;
   P = SidePlan();
   P.n_rows = n_rows;
@@ -206,8 +215,14 @@ als_status build_plan(als_ctx *ctx, SidePlan &P, const std::vector<int64_t> &ptr
   order.reserve(n_rows);
   for (int64_t s = 0; s < n_rows; ++s) {
     const int64_t d = ptr[s + 1] - ptr[s];
-    if (d > 0) order.push_back((int32_t)s);
-    else P.zero_rows.push_back((int32_t)s);
+    if (parity >= 0) {
+      if ((s & 1) != parity) continue;
+      order.push_back((int32_t)s);
+    } else if (d > 0) {
+      order.push_back((int32_t)s);
+    } else {
+      P.zero_rows.push_back((int32_t)s);
+    }
     P.max_deg = std::max(P.max_deg, d);
   }
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
@@ -366,10 +381,13 @@ void free_ctx(als_ctx *c) {
   dfree(c->d_hyper_partials);
   dfree(c->d_hyper_status);
   if (c->h_hyper_status) (void)hipHostFree(c->h_hyper_status);
-  for (int sd = 0; sd < 2; ++sd) {
+  for (int sd = 0; sd < 3; ++sd) {
     dfree(c->d_nw_mu0[sd]);
     dfree(c->d_nw_W0inv[sd]);
   }
+  dfree(c->d_time_h0);
+  dfree(c->d_time_extra);
+  dfree(c->d_zero_mu);
   if (c->h_cyc_sum) (void)hipHostFree(c->h_cyc_sum);
   for (auto &pe : c->prof_pending) {
     (void)hipEventDestroy(pe.a);
@@ -640,6 +658,7 @@ struct SweepSpec {
   const float *wts = nullptr;
   int64_t n_fixed = 0;
   als::Hadamard hd;
+  bool keep_flags = false;  // add to the flag count of the previous sweep (time chain)
 };
 
 als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out_factors,
@@ -687,7 +706,7 @@ als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out
   const int64_t n_fixed = sp.n_fixed;
   const als::Hadamard &hd = sp.hd;
   const int side = sp.plan;
-  HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
+  if (!sp.keep_flags) HIP_OR_FAIL(ctx, als::launch_fill_i32(ctx->d_flag, 1, 0, ctx->stream));
   for (const Batch &b : P.batches) {
     double *sse = ctx->d_sse_items + b.gitem_off;
     if (ctx->lane_solve) {
@@ -796,6 +815,34 @@ als_status ensure_bayes(als_ctx *ctx) {
   return st;
 }
 
+// The Normal-Wishart hyperprior of users (0), items (1) or the time chain (2).
+als_status set_nw_prior_at(als_ctx *ctx, int at, const double *mu0, double beta0,
+                           const double *W0_inv, double nu0) {
+  const int D = ctx->D;
+  if (!mu0 || !W0_inv) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (!(beta0 >= 0.0) || !std::isfinite(beta0) || !std::isfinite(nu0) || !(nu0 > D - 1))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "need beta0 >= 0 and nu0 > D - 1");
+  for (int a = 0; a < D; ++a) {
+    if (!std::isfinite(mu0[a])) return fail(ctx, ALS_ERR_INVALID_ARG, "mu0 is not finite");
+    for (int e = 0; e < D; ++e) {
+      if (!std::isfinite(W0_inv[a * D + e]) || W0_inv[a * D + e] != W0_inv[e * D + a])
+        return fail(ctx, ALS_ERR_INVALID_ARG, "W0_inv must be finite and symmetric");
+    }
+  }
+  DeviceGuard g(ctx->device);
+  als_status st = ensure(ctx, &ctx->d_nw_mu0[at], (size_t)D, "prior mean");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_nw_W0inv[at], (size_t)D * D, "prior scale");
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_mu0[at], mu0, sizeof(double) * D, hipMemcpyHostToDevice));
+  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_W0inv[at], W0_inv, sizeof(double) * D * D,
+                             hipMemcpyHostToDevice));
+  ctx->nw_beta0[at] = beta0;
+  ctx->nw_nu0[at] = nu0;
+  ctx->nw_set[at] = true;
+  return ALS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -843,29 +890,14 @@ als_status als_set_nw_prior(als_ctx *ctx, als_side side, const double *mu0, doub
   ctx->err.clear();
   if (side != ALS_ROWS_USERS && side != ALS_ROWS_ITEMS)
     return fail(ctx, ALS_ERR_INVALID_ARG, "side must be ALS_ROWS_USERS or ALS_ROWS_ITEMS");
-  const int D = ctx->D;
-  if (!mu0 || !W0_inv) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
-  if (!(beta0 >= 0.0) || !std::isfinite(beta0) || !std::isfinite(nu0) || !(nu0 > D - 1))
-    return fail(ctx, ALS_ERR_INVALID_ARG, "need beta0 >= 0 and nu0 > D - 1");
-  for (int a = 0; a < D; ++a) {
-    if (!std::isfinite(mu0[a])) return fail(ctx, ALS_ERR_INVALID_ARG, "mu0 is not finite");
-    for (int e = 0; e < D; ++e) {
-      if (!std::isfinite(W0_inv[a * D + e]) || W0_inv[a * D + e] != W0_inv[e * D + a])
-        return fail(ctx, ALS_ERR_INVALID_ARG, "W0_inv must be finite and symmetric");
-    }
-  }
-  DeviceGuard g(ctx->device);
-  als_status st = ensure(ctx, &ctx->d_nw_mu0[side], (size_t)D, "prior mean");
-  if (st == ALS_OK) st = ensure(ctx, &ctx->d_nw_W0inv[side], (size_t)D * D, "prior scale");
-  if (st != ALS_OK) return st;
-  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
-  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_mu0[side], mu0, sizeof(double) * D, hipMemcpyHostToDevice));
-  HIP_OR_FAIL(ctx, hipMemcpy(ctx->d_nw_W0inv[side], W0_inv, sizeof(double) * D * D,
-                             hipMemcpyHostToDevice));
-  ctx->nw_beta0[side] = beta0;
-  ctx->nw_nu0[side] = nu0;
-  ctx->nw_set[side] = true;
-  return ALS_OK;
+  return set_nw_prior_at(ctx, (int)side, mu0, beta0, W0_inv, nu0);
+}
+
+als_status als_set_time_nw_prior(als_ctx *ctx, const double *mu0, double beta0,
+                                 const double *W0_inv, double nu0) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  return set_nw_prior_at(ctx, 2, mu0, beta0, W0_inv, nu0);
 }
 
 als_status als_sample_hyper(als_ctx *ctx, als_side side, const float *X, const double *chi2,
@@ -1081,11 +1113,16 @@ als_status als_set_time_bins(als_ctx *ctx, int32_t n_bins, const int32_t *bins) 
   dfree(ctx->d_tb_item);
   dfree(ctx->d_tb_val);
   dfree(ctx->d_fpad2);
+  for (int q = 2; q < 5; ++q) {
+    SidePlan &P = ctx->plan[q];
+    dfree(P.d_gitems);
+    dfree(P.d_rows);
+    dfree(P.d_zero_rows);
+    P = SidePlan();
+  }
   SidePlan &TP = ctx->plan[2];
-  dfree(TP.d_gitems);
-  dfree(TP.d_rows);
-  dfree(TP.d_zero_rows);
-  TP = SidePlan();
+  dfree(ctx->d_time_h0);
+  ctx->time_h0_bins = 0;
   ctx->n_bins = 0;
   const int64_t nnz = ctx->nnz, M = ctx->M;
   HIP_OR_FAIL(ctx, dalloc(&ctx->d_tbin, nnz));
@@ -1153,8 +1190,10 @@ als_status als_set_time_bins(als_ctx *ctx, int32_t n_bins, const int32_t *bins) 
     HIP_OR_FAIL(ctx, e2);
   }
   als_status st = build_plan(ctx, TP, ptr);
+  if (st == ALS_OK) st = build_plan(ctx, ctx->plan[3], ptr, 0);
+  if (st == ALS_OK) st = build_plan(ctx, ctx->plan[4], ptr, 1);
   if (st != ALS_OK) return st;
-  // shared buffers sized for the third plan too
+  // shared buffers sized for the time-bin plans too
   int64_t max_slots = 0, max_sse = 0, max_rows = 0;
   for (auto &P : ctx->plan) {
     max_slots = std::max(max_slots, P.max_slots);
@@ -1255,6 +1294,152 @@ als_status als_tensor_rmse(als_ctx *ctx, const float *U, const float *V, const f
                                   hipMemcpyDeviceToHost, ctx->stream));
   HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
   *rmse_out = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse / (double)ctx->nnz) : 0.0;
+  return ALS_OK;
+}
+
+// ---- BPTF: the tensor model's Gibbs step -------------------------------------------
+
+als_status als_tensor_gibbs_half_sweep(als_ctx *ctx, als_mode mode, float *U, float *V, float *T,
+                                       float alpha, const double *Lambda, const double *mu,
+                                       const float *z, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (ctx->n_bins <= 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no time bins set");
+  if (mode != ALS_MODE_USERS && mode != ALS_MODE_ITEMS && mode != ALS_MODE_TIME)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "mode %d is not a tensor mode", (int)mode);
+  if (!U || !V || !T || !Lambda || !mu || !z)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (!(alpha > 0.f) || !std::isfinite(alpha))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "alpha must be finite and > 0");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15) || ((uintptr_t)T & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  if (ctx->d_w) return fail(ctx, ALS_ERR_INVALID_ARG, "BPTF takes no rating weights; detach them");
+  const int D = ctx->D;
+  const int64_t K = ctx->n_bins;
+  const size_t bu = sizeof(float) * ctx->M * D, bv = sizeof(float) * ctx->N * D;
+  const size_t bt = sizeof(float) * (size_t)K * D;
+  if (overlap(U, bu, V, bv) || overlap(U, bu, T, bt) || overlap(V, bv, T, bt))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "U, V and T must not overlap");
+  const size_t bo = mode == ALS_MODE_USERS ? bu : (mode == ALS_MODE_ITEMS ? bv : bt);
+  float *out = mode == ALS_MODE_USERS ? U : (mode == ALS_MODE_ITEMS ? V : T);
+  if (overlap(z, bo, out, bo)) return fail(ctx, ALS_ERR_INVALID_ARG, "z overlaps the drawn factors");
+  DeviceGuard g(ctx->device);
+  als_status st = ensure_bayes(ctx);
+  if (st != ALS_OK) return st;
+  const float *F1, *F2;
+  int64_t n1, n2;
+  SweepSpec sp;
+  sp.plan = (int)mode;
+  if (mode == ALS_MODE_USERS) {
+    F1 = V; n1 = ctx->N; F2 = T; n2 = K;
+    sp.idx = ctx->d_col; sp.val = ctx->d_val; sp.hd.idx2 = ctx->d_tbin;
+  } else if (mode == ALS_MODE_ITEMS) {
+    F1 = U; n1 = ctx->M; F2 = T; n2 = K;
+    sp.idx = ctx->d_row_idx; sp.val = ctx->d_val_t; sp.hd.idx2 = ctx->d_tbin_t;
+  } else {
+    F1 = U; n1 = ctx->M; F2 = V; n2 = ctx->N;
+    sp.idx = ctx->d_tb_user; sp.val = ctx->d_tb_val; sp.hd.idx2 = ctx->d_tb_item;
+  }
+  sp.n_fixed = n1;
+  sp.hd.Tp = ctx->d_fpad2;
+  {
+    PhaseTimer t(ctx, 0);
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(F1, n1, D, ctx->DP, ctx->d_fpad, ctx->stream));
+    HIP_OR_FAIL(ctx, als::launch_stage_fixed(F2, n2, D, ctx->DP, ctx->d_fpad2, ctx->stream));
+  }
+  als::RowPrior pr;
+  pr.init = ctx->d_prior_init;
+  pr.z = z;
+  pr.zscale = (float)(1.0 / std::sqrt((double)alpha));
+  if (mode != ALS_MODE_TIME) {
+    HIP_OR_FAIL(ctx, als::launch_prior_prepare(Lambda, mu, D, ctx->DP, (double)alpha,
+                                               !ctx->plan[mode].zero_rows.empty(),
+                                               ctx->d_prior_init, ctx->d_prior_K,
+                                               ctx->d_prior_mu32, ctx->d_prior_ok, ctx->stream));
+    return run_sweep(ctx, sp, 0.f, out, rmse_out, pr);
+  }
+  // the time chain: the image is Lambda_T / alpha without a mean term; bin k takes twice
+  // the image (once for its own step, once as the condition of bin k + 1), the last bin
+  // once, and its neighbours' right-hand side from k_time_rhs; even bins, then odd bins
+  if (!ctx->d_zero_mu) {
+    st = ensure(ctx, &ctx->d_zero_mu, (size_t)D, "zero mean");
+    if (st != ALS_OK) return st;
+    HIP_OR_FAIL(ctx, als::launch_fill_i32(reinterpret_cast<int32_t *>(ctx->d_zero_mu), 2 * D, 0,
+                                          ctx->stream));
+  }
+  if (ctx->time_h0_bins != K) {
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    dfree(ctx->d_time_h0);
+    HIP_OR_FAIL(ctx, dalloc(&ctx->d_time_h0, K * D));
+    ctx->time_h0_bins = K;
+  }
+  HIP_OR_FAIL(ctx, als::launch_prior_prepare(Lambda, ctx->d_zero_mu, D, ctx->DP, (double)alpha,
+                                             false, ctx->d_prior_init, ctx->d_prior_K,
+                                             ctx->d_prior_mu32, ctx->d_prior_ok, ctx->stream));
+  pr.scale = 2.f;
+  pr.scale_last = 1.f;
+  pr.last_row = K - 1;
+  pr.h0 = ctx->d_time_h0;
+  for (int parity = 0; parity < 2; ++parity) {
+    HIP_OR_FAIL(ctx, als::launch_time_rhs(T, K, D, Lambda, mu, (double)alpha, parity,
+                                          ctx->d_time_h0, ctx->stream));
+    SweepSpec sq = sp;
+    sq.plan = 3 + parity;
+    sq.keep_flags = parity == 1;
+    st = run_sweep(ctx, sq, 0.f, T, nullptr, pr);
+    if (st != ALS_OK) return st;
+  }
+  if (rmse_out) {
+    st = als_tensor_rmse(ctx, U, V, T, rmse_out);
+    if (st != ALS_OK) return st;
+    if (*ctx->h_flag > 0)
+      return fail(ctx, ALS_ERR_NOT_SPD, "%d time bins were flagged and left unchanged",
+                  (int)*ctx->h_flag);
+  }
+  return ALS_OK;
+}
+
+als_status als_sample_time_hyper(als_ctx *ctx, const float *T, const double *chi2,
+                                 const double *offdiag, const double *z_mu, double *mu_out,
+                                 double *Lambda_out, int32_t *status_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (ctx->n_bins <= 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no time bins set");
+  if (!ctx->nw_set[2]) return fail(ctx, ALS_ERR_INVALID_ARG, "no Normal-Wishart prior set for the time chain");
+  if (!T || !chi2 || (!offdiag && ctx->D > 1) || !z_mu || !mu_out || !Lambda_out)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(ctx->device);
+  als_status st = ensure_bayes(ctx);
+  if (st == ALS_OK)
+    st = ensure(ctx, &ctx->d_time_extra, (size_t)ctx->D * (ctx->D + 1) / 2, "chain scatter");
+  if (st != ALS_OK) return st;
+  HIP_OR_FAIL(ctx, als::launch_time_hyper(T, ctx->n_bins, ctx->D, ctx->d_nw_mu0[2],
+                                          ctx->nw_beta0[2], ctx->d_nw_W0inv[2], ctx->nw_nu0[2],
+                                          chi2, offdiag, z_mu, ctx->d_bayes_scratch,
+                                          ctx->d_time_extra, mu_out, Lambda_out,
+                                          ctx->d_hyper_status, ctx->stream));
+  if (status_out) {
+    HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_hyper_status, ctx->d_hyper_status, sizeof(int32_t),
+                                    hipMemcpyDeviceToHost, ctx->stream));
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    *status_out = *ctx->h_hyper_status;
+    if (*status_out != 0)
+      return fail(ctx, ALS_ERR_NOT_SPD, "a factorisation of the Normal-Wishart draw failed");
+  }
+  return ALS_OK;
+}
+
+als_status als_tensor_sample_alpha(als_ctx *ctx, const float *U, const float *V, const float *T,
+                                   double w0, double chi2, double *alpha_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!alpha_out) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (!(w0 > 0.0) || !std::isfinite(w0) || !(chi2 > 0.0) || !std::isfinite(chi2))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "w0 and chi2 must be finite and > 0");
+  double rmse = 0.0;
+  als_status st = als_tensor_rmse(ctx, U, V, T, &rmse);
+  if (st != ALS_OK) return st;
+  *alpha_out = chi2 / (1.0 / w0 + *ctx->h_sse);
   return ALS_OK;
 }
 

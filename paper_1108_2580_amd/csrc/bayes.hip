@@ -21,6 +21,16 @@
 //                     about the mean), then Bartlett's draw: W* = F F^T, B lower
 //                     triangular with B_ii = sqrt(chi2_i) and normal B_ij, Lambda =
 //                     (F B)(F B)^T, and mu = mu0* + R^{-T} zmu with beta* Lambda = R R^T.
+// The time chain of BPTF (T_0 ~ N(mu_T, Lambda_T^{-1}), T_k ~ N(T_{k-1}, Lambda_T^{-1})):
+//   k_time_rhs        a bin's prior right-hand side Lambda_T (m_k + [k < K - 1] T_{k+1}) /
+//                     alpha (m_k = mu_T for the first bin, else T_{k-1}) for the bins of
+//                     one parity, in fp64; the bins of a parity are drawn together given
+//                     the other parity.
+//   k_time_moments    the chain's posterior inputs: the moments of T_0 alone (n = 1) in
+//                     the segment layout k_hyper_sample reads, and the step scatter
+//                     sum_{k>=1} (T_k - T_{k-1})(T_k - T_{k-1})^T with the differences
+//                     formed in fp64 (exact for fp32 inputs), which k_hyper_sample adds
+//                     to W*^{-1}.
 // The variates (chi-square, normals) are inputs. Matrices live as fp64
 // packed triangles in LDS (two of them, 132 KB at D = 128); the factorisations are
 // right-looking Cholesky steps with a barrier between steps.
@@ -306,12 +316,13 @@ __global__ __launch_bounds__(64) void k_hyper_reduce(const double *__restrict__ 
 //   P1 = W*^{-1} -> R (Cholesky);  P2 = R^{-1};  P1 = W* = R^{-T} R^{-1} -> F (Cholesky);
 //   P2 = F B (lower times lower is lower);  P1 = Lambda = (F B)(F B)^T, written out;
 //   P1 = beta* Lambda -> its Cholesky factor;  mu = mu0* + R^{-T} zmu.
+// extra (nullable): a packed upper triangle added to W*^{-1} (the time chain's steps).
 __global__ __launch_bounds__(kBayesBlock) void k_hyper_sample(
     const double *__restrict__ seg_sums, int64_t n, int D,
     const double *__restrict__ mu0, double beta0, const double *__restrict__ W0inv, double nu0,
     const double *__restrict__ chi2, const double *__restrict__ offd,
-    const double *__restrict__ zmu, double *__restrict__ H, double *__restrict__ mu_out,
-    double *__restrict__ Lam_out, int32_t *__restrict__ status) {
+    const double *__restrict__ zmu, const double *__restrict__ extra, double *__restrict__ H,
+    double *__restrict__ mu_out, double *__restrict__ Lam_out, int32_t *__restrict__ status) {
   __shared__ double P1[kPacked], P2[kPacked];
   __shared__ double xbar[kMaxD], dv[kMaxD], tmp[kMaxD];
   __shared__ int bad;
@@ -336,8 +347,10 @@ __global__ __launch_bounds__(kBayesBlock) void k_hyper_sample(
   // W*^{-1} = W0^{-1} + (sum x x^T - n xbar xbar^T) + shrink dv dv^T (lower triangle)
   for (int i = (int)(threadIdx.x >> 4); i < D; i += 16) {
     for (int j = (int)(threadIdx.x & 15); j <= i; j += 16) {
-      const double sxx = H[D + j * D - j * (j - 1) / 2 + (i - j)];
-      P1[pl(i, j)] = W0inv[i * D + j] + (sxx - nn * xbar[i] * xbar[j]) + shrink * dv[i] * dv[j];
+      const int q = j * D - j * (j - 1) / 2 + (i - j);
+      const double sxx = H[D + q];
+      P1[pl(i, j)] = W0inv[i * D + j] + (sxx - nn * xbar[i] * xbar[j]) + shrink * dv[i] * dv[j] +
+                     (extra ? extra[q] : 0.0);
     }
   }
   __syncthreads();
@@ -401,6 +414,65 @@ __global__ __launch_bounds__(kBayesBlock) void k_hyper_sample(
   if (threadIdx.x == 0) *status = bad ? 1 : 0;
 }
 
+// Row a and column b (a <= b) of packed upper-triangle entry t (rows in order).
+__device__ inline void upper_entry(int t, int D, int &a, int &b) {
+  a = 0;
+  while (t >= D - a) {
+    t -= D - a;
+    ++a;
+  }
+  b = a + t;
+}
+
+__global__ __launch_bounds__(256) void k_time_rhs(const float *__restrict__ T, int64_t K, int D,
+                                                  const double *__restrict__ Lam,
+                                                  const double *__restrict__ mu, double inv_alpha,
+                                                  int parity, float *__restrict__ h0) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nk = (K - parity + 1) / 2;  // bins of this parity
+  if (t >= nk * D) return;
+  const int64_t k = parity + 2 * (t / D);
+  const int a = (int)(t % D);
+  double acc = 0.0;
+  for (int e = 0; e < D; ++e) {
+    const double prev = k == 0 ? mu[e] : (double)T[(k - 1) * D + e];
+    const double next = k < K - 1 ? (double)T[(k + 1) * D + e] : 0.0;
+    acc += Lam[a * D + e] * (prev + next);
+  }
+  h0[k * D + a] = (float)(acc * inv_alpha);
+}
+
+__global__ __launch_bounds__(256) void k_time_moments(const float *__restrict__ T, int64_t K,
+                                                      int D, double *__restrict__ seg_sums,
+                                                      double *__restrict__ extra) {
+  const int ne = D + D * (D + 1) / 2, ntri = D * (D + 1) / 2;
+  const int total = kReduceSegs * ne + ntri;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < total; q += gridDim.x * 256) {
+    if (q < kReduceSegs * ne) {
+      const int g = q / ne, e = q % ne;
+      double v = 0.0;
+      if (g == 0) {
+        if (e < D) {
+          v = (double)T[e];
+        } else {
+          int a, b;
+          upper_entry(e - D, D, a, b);
+          v = (double)T[a] * (double)T[b];
+        }
+      }
+      seg_sums[q] = v;
+    } else {
+      int a, b;
+      upper_entry(q - kReduceSegs * ne, D, a, b);
+      double acc = 0.0;
+      for (int64_t k = 1; k < K; ++k)
+        acc += ((double)T[k * D + a] - (double)T[(k - 1) * D + a]) *
+               ((double)T[k * D + b] - (double)T[(k - 1) * D + b]);
+      extra[q - kReduceSegs * ne] = acc;
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_prior_prepare(const double *Lam, const double *mu, int D, int DP, double alpha,
@@ -447,7 +519,38 @@ hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_hyper_sample, dim3(1), dim3(kBayesBlock), 0, s, seg_sums, n, D, mu0,
-                     beta0, W0inv, nu0, chi2, offd, zmu, scratch, mu_out, Lam_out, status);
+                     beta0, W0inv, nu0, chi2, offd, zmu, (const double *)nullptr, scratch, mu_out,
+                     Lam_out, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_time_rhs(const float *T, int64_t K, int D, const double *Lam, const double *mu,
+                           double alpha, int parity, float *h0, hipStream_t s) {
+  if (D < 1 || D > 128 || K < 1 || (parity != 0 && parity != 1) || !(alpha > 0.0))
+    return hipErrorInvalidValue;
+  const int64_t threads = (K - parity + 1) / 2 * D;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_time_rhs, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, T, K,
+                     D, Lam, mu, 1.0 / alpha, parity, h0);
+  return hipGetLastError();
+}
+
+hipError_t launch_time_hyper(const float *T, int64_t K, int D, const double *mu0, double beta0,
+                             const double *W0inv, double nu0, const double *chi2,
+                             const double *offd, const double *zmu, double *scratch,
+                             double *extra, double *mu_out, double *Lam_out, int32_t *status,
+                             hipStream_t s) {
+  if (D < 1 || D > 128 || K < 1) return hipErrorInvalidValue;
+  const int ne = hyper_entries(D);
+  double *seg_sums = scratch + ne + 8;
+  const int total = kReduceSegs * ne + D * (D + 1) / 2;
+  hipLaunchKernelGGL(k_time_moments, dim3((unsigned)std::min(1024, (total + 255) / 256)),
+                     dim3(256), 0, s, T, K, D, seg_sums, extra);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_hyper_sample, dim3(1), dim3(kBayesBlock), 0, s, seg_sums, (int64_t)1, D,
+                     mu0, beta0, W0inv, nu0, chi2, offd, zmu, (const double *)extra, scratch,
+                     mu_out, Lam_out, status);
   return hipGetLastError();
 }
 

@@ -158,6 +158,18 @@ __device__ __forceinline__ GroupLanes group_lanes(const int32_t *__restrict__ ip
   return g;
 }
 
+// The first group of an item (group_lanes(.., 0, ..)); an item without ratings gets the
+// empty group (the all-zero row, rating 0, weight 0) and reads no rating.
+template <bool WT, bool TS = false>
+__device__ __forceinline__ GroupLanes first_group(const int32_t *__restrict__ ip,
+                                                  const uint8_t *__restrict__ vp,
+                                                  const float *__restrict__ wp,
+                                                  const int32_t *__restrict__ tp, int n,
+                                                  int zrow) {
+  if (n <= 0) return GroupLanes{zrow, 0.f, 0.f, 0};
+  return group_lanes<WT, TS>(ip, vp, wp, tp, n, 0, zrow);
+}
+
 // Gather the staged fixed rows of steps s0 .. s0 + STEPS - 1 of a 64-rating group:
 // lane (kq, c) receives feature 16 X + c of rating 4 s + kq. The group's column
 // indices and ratings come from its staging buffer.
@@ -423,12 +435,13 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
 }
 
 // Whether the last tile of width DP uses only its first four features (D in
-// 16 (T - 1) + 1 .. 16 (T - 1) + 4, three or more tiles): then the strip form of
+// 16 (T - 1) + 1 .. 16 (T - 1) + 4, three to seven tiles): then the strip form of
 // mma_block serves the last tile column, and the augmented column is feature
-// 16 (T - 1) + 4.
+// 16 (T - 1) + 4. At eight tiles the strip form spills several times more registers
+// than the tile form, so those widths keep the tile form.
 template <int DP>
 __host__ __device__ constexpr bool strip_width(int D) {
-  return DP / 16 >= 3 && D > DP - 16 && D <= DP - 12;
+  return DP / 16 >= 3 && DP / 16 <= 7 && D > DP - 16 && D <= DP - 12;
 }
 
 // Finish a strip-form Gram (mma_block with STRIP): sum each strip of the last tile

@@ -51,6 +51,17 @@ struct RowPrior {
                                 // packed record (upper triangle, then the right-hand side)
   const float *z = nullptr;     // standard normal variates, [rows of the side x D]
   float zscale = 0.f;           // 1 / sqrt(alpha)
+  // The time chain of BPTF: row r's prior is scale * init (scale_last * init for row
+  // last_row), plus the per-row right-hand side h0 [rows x D] (already divided by alpha)
+  // when h0 is set. The matrix and tensor Gibbs draws keep scale = 1, no h0.
+  float scale = 1.f;
+  float scale_last = 1.f;
+  int64_t last_row = -1;
+  const float *h0 = nullptr;
+
+  __host__ __device__ float scale_of(int64_t row) const {
+    return row == last_row ? scale_last : scale;
+  }
 };
 
 // Tensor ALS: the second index of every rating (aligned with idx / val) and the second
@@ -177,6 +188,17 @@ hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int 
                                const double *chi2, const double *offd, const double *zmu,
                                double *scratch, double *mu_out, double *Lam_out, int32_t *status,
                                hipStream_t s);
+// The time chain of BPTF: h0 (K x D, fp32) of the bins k = parity, parity + 2, ...:
+// Lambda_T (m_k + [k < K - 1] T_{k+1}) / alpha with m_0 = mu_T and m_k = T_{k-1}.
+hipError_t launch_time_rhs(const float *T, int64_t K, int D, const double *Lam, const double *mu,
+                           double alpha, int parity, float *h0, hipStream_t s);
+// The chain's Normal-Wishart posterior (the moments of T_0 as one row, plus the step
+// scatter in extra, D (D + 1) / 2 doubles) and the Bartlett draw of (mu_T, Lambda_T).
+hipError_t launch_time_hyper(const float *T, int64_t K, int D, const double *mu0, double beta0,
+                             const double *W0inv, double nu0, const double *chi2,
+                             const double *offd, const double *zmu, double *scratch,
+                             double *extra, double *mu_out, double *Lam_out, int32_t *status,
+                             hipStream_t s);
 
 // Predictions u_{users[p]} . v_{items[p]} of n pairs (predict.hip). pred (nullable)
 // receives them, NaN for a pair with an index outside [0, M) x [0, N). With

@@ -17,7 +17,8 @@
 //                half-sweep (BAYES) the record gets the prior image added instead
 //                (Lambda / alpha and Lambda mu / alpha), and y gets z / sqrt(alpha)
 //                before the back substitution, which turns the solve into the
-//                conditional draw mu* + L*^{-T} z.
+//                conditional draw mu* + L*^{-T} z. The time chain of BPTF scales the
+//                image per row and adds a per-row right-hand side (RowPrior).
 // Records hold LD(LD+1)/2 + LD floats (LD = 16 or 20, the width the solve is
 // compiled for; padded features solve to zero), rounded up to a multiple of 4.
 #include "gram.h"
@@ -66,7 +67,7 @@ __global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ ite
   const float *__restrict__ wp = WT ? wts + it.start : nullptr;
   const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
   const GroupLanes g0 =
-      group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
+      first_group<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, zrow);
   // CORNER: lane c < 15 of a row group owns the product (cp, cq), cp <= cq < 5, of the
   // features 16 + cp and 16 + cq (16 + 4 = LD is the augmented column)
   int cp = 0, cq = 0;
@@ -169,11 +170,19 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
     }
   }
   if constexpr (BAYES) {
-    // the prior image carries the identity on the padding
+    // the prior image carries the identity on the padding; the time chain scales it per
+    // row and adds the row's own right-hand side
+    const float cs = pr.scale_of(rt.row);
 #pragma unroll
-    for (int e = 0; e < NTRI; ++e) A[e] += pr.init[e];
+    for (int e = 0; e < NTRI; ++e) A[e] = fmaf(cs, pr.init[e], A[e]);
 #pragma unroll
-    for (int d = 0; d < LD; ++d) b[d] += pr.init[NTRI + d];
+    for (int d = 0; d < LD; ++d) b[d] = fmaf(cs, pr.init[NTRI + d], b[d]);
+    if (pr.h0 != nullptr) {
+      const float *__restrict__ hr = pr.h0 + (int64_t)rt.row * D;
+#pragma unroll
+      for (int d = 0; d < LD; ++d)
+        if (d < D) b[d] += hr[d];
+    }
   } else {
     const float lam_n = (float)((double)lam * (double)rt.deg);
 #pragma unroll

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   const float *__restrict__ wp = WT ? wts + it.start : nullptr;
   const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
   const GroupLanes g0 =
-      group_lanes<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, 0, zrow);
+      first_group<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, zrow);
   float no_corner = 0.f;
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
   gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
@@ -143,7 +143,8 @@ constexpr int kRowWaves = 1;  // rows per workgroup (one per wavefront)
 // BAYES (a Gibbs half-sweep): the accumulators start from the prior image (Lambda /
 // alpha, identity on the padding, and Lambda mu / alpha in the right-hand side) and the
 // forward-substitution result y gets z / sqrt(alpha) before the back substitution, so
-// that the row receives the conditional draw mu* + L*^{-T} z.
+// that the row receives the conditional draw mu* + L*^{-T} z. For the time chain of BPTF
+// the image is scaled per row and a per-row right-hand side h0 is added (RowPrior).
 template <int DP, bool AUG, bool WT, bool BAYES, bool TS, bool STRIP = false>
 __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const RowTask *__restrict__ rows, int64_t n_rows, const int32_t *__restrict__ idx,
@@ -175,9 +176,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   // is accumulated on top. With STRIP the last tile column starts from zero (it holds
   // strips during the Gram) and receives its initial value afterwards.
   const float lam_n = (float)((double)lam * (double)rt.deg);
+  const float pscale = BAYES ? pr.scale_of(rt.row) : 1.f;
   auto tile_init = [&](int I, int J) -> floatx4 {
     if constexpr (BAYES) {
-      return *reinterpret_cast<const floatx4 *>(pr.init + tidx<T>(I, J) * 256 + lane * 4);
+      return pscale *
+             *reinterpret_cast<const floatx4 *>(pr.init + tidx<T>(I, J) * 256 + lane * 4);
     } else {
       floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
       if (I == J) {
@@ -213,7 +216,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const float *__restrict__ wp = WT ? wts + rt.start : nullptr;
     const int32_t *__restrict__ tp = TS ? hd.idx2 + rt.start : nullptr;
     const GroupLanes g0 =
-        group_lanes<WT, TS>(idx + rt.start, val + rt.start, wp, tp, rt.deg, 0, zrow);
+        first_group<WT, TS>(idx + rt.start, val + rt.start, wp, tp, rt.deg, zrow);
     float no_corner = 0.f;
     gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
         acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp, rt.deg, Fp, hd.Tp, zrow,
@@ -248,7 +251,30 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   if constexpr (BAYES && !AUG) {
     // the prior's right-hand side (with the augmented column it sits in the tiles)
 #pragma unroll
-    for (int X = 0; X < T; ++X) rhs[X] += pr.init[NT * 256 + 16 * X + c];
+    for (int X = 0; X < T; ++X) rhs[X] = fmaf(pscale, pr.init[NT * 256 + 16 * X + c], rhs[X]);
+  }
+  if constexpr (BAYES) {
+    // the time chain's per-row right-hand side: into the augmented column (every row group
+    // holds its own rows there) or into rhs (every lane holds the full sums)
+    if (pr.h0 != nullptr) {
+      const float *__restrict__ hr = pr.h0 + (int64_t)rt.row * D;
+      if constexpr (AUG) {
+        if (c == aug_c) {
+#pragma unroll
+          for (int I = 0; I < T; ++I) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int d = 16 * I + 4 * kq + r;
+              if (d < D) acc[tidx<T>(I, T - 1)][r] += hr[d];
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int X = 0; X < T; ++X)
+          if (16 * X + c < D) rhs[X] += hr[16 * X + c];
+      }
+    }
   }
 
   const uint64_t t_gram = __builtin_readcyclecounter();
@@ -475,7 +501,7 @@ static void launch_rows_k(int64_t blocks, const RowTask *rows, int64_t n_rows,
 // The augmented variants, in strip form where the last tile uses four features.
 template <int DP, bool WT, bool BAYES, bool TS, class... A>
 static void launch_rows_aug(bool strip, A &&...args) {
-  if constexpr (DP >= 48) {
+  if constexpr (DP >= 48 && DP <= 112) {
     if (strip) return launch_rows_k<DP, true, WT, BAYES, TS, true>(args...);
   }
   launch_rows_k<DP, true, WT, BAYES, TS, false>(args...);
@@ -493,10 +519,15 @@ static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32
 #define ROW_ARGS blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag, \
                  cyc_gram, cyc_solve, pr, hd, s
   if (hd.idx2) {
-    // tensor ALS: no weights, no Bayesian prior; the tile form throughout (the strip
+    // tensor ALS (and its Gibbs draws): no weights; the tile form throughout (the strip
     // form of its Gram runs out of registers)
-    if (wt || pr.init) return hipErrorInvalidValue;
-    if (aug)
+    if (wt) return hipErrorInvalidValue;
+    if (pr.init) {
+      if (aug)
+        launch_rows_k<DP, true, false, true, true>(ROW_ARGS);
+      else
+        launch_rows_k<DP, false, false, true, true>(ROW_ARGS);
+    } else if (aug)
       launch_rows_k<DP, true, false, false, true>(ROW_ARGS);
     else
       launch_rows_k<DP, false, false, false, true>(ROW_ARGS);
@@ -530,7 +561,7 @@ static void launch_chunks_k(int64_t n, const WorkItem *items, const int32_t *idx
 
 template <int DP, bool WT, bool TS, class... A>
 static void launch_chunks_aug(bool strip, A &&...args) {
-  if constexpr (DP >= 48) {
+  if constexpr (DP >= 48 && DP <= 112) {
     if (strip) return launch_chunks_k<DP, true, WT, TS, true>(args...);
   }
   launch_chunks_k<DP, true, WT, TS, false>(args...);
