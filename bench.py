@@ -54,9 +54,13 @@ def parse():
     ap.add_argument("--tensor", action="store_true",
                     help="tensor ALS over 6649 seeded time bins: one step updates the items, "
                          "the users and the time bins")
+    ap.add_argument("--bptf", action="store_true",
+                    help="BPTF: one step is a Gibbs iteration of the tensor model over 6649 "
+                         "seeded time bins (alpha, the three hyperparameter draws, then the "
+                         "items, users and time bins)")
     args = ap.parse_args()
-    if args.gibbs + args.weighted + args.tensor > 1:
-        ap.error("--gibbs, --weighted and --tensor are exclusive")
+    if args.gibbs + args.weighted + args.tensor + args.bptf > 1:
+        ap.error("--gibbs, --weighted, --tensor and --bptf are exclusive")
     return args
 
 
@@ -154,8 +158,13 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False, tensor=None
             sub_ptr = np.concatenate([[0], np.cumsum(deg[sel])]).astype(np.int64)
             take = np.repeat(r.row_ptr[sel] - sub_ptr[:-1], deg[sel]) + np.arange(sub_ptr[-1])
             t_a = time.perf_counter()
-            oracle.tensor_rows(sub_ptr, r.col[take], bins[take], val[take], fixed, Tf, r.lam,
-                               np.zeros((k, r.D)), threads=threads)
+            if gibbs:
+                oracle.tensor_gibbs_rows(sub_ptr, r.col[take], bins[take], val[take], fixed, Tf,
+                                         BPTF_ALPHA_TYPICAL, np.eye(r.D), np.zeros(r.D),
+                                         np.zeros((k, r.D)), np.zeros((k, r.D)), threads=threads)
+            else:
+                oracle.tensor_rows(sub_ptr, r.col[take], bins[take], val[take], fixed, Tf,
+                                   r.lam, np.zeros((k, r.D)), threads=threads)
             return int(deg[sel].sum()), k, time.perf_counter() - t_a
         if gibbs:
             sub_ptr = np.concatenate([[0], np.cumsum(deg[sel])]).astype(np.int64)
@@ -186,7 +195,8 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False, tensor=None
                 cpu_model=cpu_model,
                 sample=(f"user half-sweep of {r.name}"
                         f"{' (weighted)' if w is not None else ' (Gibbs draws)' if gibbs else ''}"
-                        f"{' (tensor user mode)' if tensor is not None else ''}: "
+                        f"{' (tensor user mode)' if tensor is not None else ''}"
+                        f"{' (BPTF user draws)' if tensor is not None and gibbs else ''}: "
                         f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
@@ -289,6 +299,55 @@ class GibbsSteps:
                              self.z[side][k], out)
 
 
+# BPTF: the rating precision's prior W(w0, nu0) (one-dimensional Wishart), the chain's
+# hyperprior (mean 1, as the time factors start around 1), and a typical alpha for the
+# oracle baseline (noise of standard deviation 30 on the 0..100 scale)
+BPTF_ALPHA_W0 = 1.0
+BPTF_ALPHA_NU0 = 2.0
+BPTF_ALPHA_TYPICAL = 1.0 / 900.0
+
+
+class BPTFSteps:
+    """Seeded variates of every BPTF iteration of the run (device tensors, and the host
+    chi-square of each alpha draw), generated before the timed region; the hyperparameter
+    buffers of the three modes."""
+
+    def __init__(self, r, als, n_bins, n_steps, seed):
+        import numpy as np
+        import torch
+
+        D = r.D
+        dev = torch.device("cuda:0")
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        rng = np.random.default_rng(seed)
+        self.z, self.var = {}, {}
+        for mode, n, prior_side in (("items", r.N, "items"), ("users", r.M, "users"),
+                                    ("bins", n_bins, "time")):
+            als.set_nw_prior(prior_side, np.ones(D) if mode == "bins" else np.zeros(D),
+                             GIBBS_BETA0, np.eye(D), float(D))
+            self.z[mode] = torch.randn((n_steps, n, D), generator=g, device=dev)
+            nu_s = D + n
+            self.var[mode] = [tuple(torch.from_numpy(a).to(dev) for a in (
+                rng.chisquare(nu_s - np.arange(D)), rng.normal(size=D * (D - 1) // 2),
+                rng.normal(size=D))) for _ in range(n_steps)]
+        self.chi2_alpha = rng.chisquare(BPTF_ALPHA_NU0 + r.nnz, size=n_steps)
+        self.mu = {m: torch.empty(D, dtype=torch.float64, device=dev) for m in self.z}
+        self.Lam = {m: torch.empty((D, D), dtype=torch.float64, device=dev) for m in self.z}
+        self.alpha = None
+
+    def mode(self, als, mode, k, U, V, T):
+        if mode == "items":
+            # the iteration starts with alpha and the three hyperparameter draws
+            self.alpha = als.tensor_sample_alpha(U, V, T, BPTF_ALPHA_W0, self.chi2_alpha[k])
+            for m, X in (("items", V), ("users", U), ("bins", T)):
+                chi2, offd, zmu = self.var[m][k]
+                als.sample_hyper("time" if m == "bins" else m, X, chi2, offd, zmu, self.mu[m],
+                                 self.Lam[m])
+        als.tensor_gibbs_half_sweep(mode, U, V, T, self.alpha, self.Lam[mode], self.mu[mode],
+                                    self.z[mode][k])
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -324,7 +383,8 @@ def main():
     gibbs = GibbsSteps(r, als, args.warmup + args.steps, r.init_seed + 77) if args.gibbs else None
     sides = ("items", "users")
     T = bins = None
-    if args.tensor:
+    bptf = None
+    if args.tensor or args.bptf:
         t_b = time.perf_counter()
         nb = workload.N_TIME_BINS
         bins = workload.time_bins(r.row_ptr, nb, workload.time_seed(args.config))
@@ -333,8 +393,13 @@ def main():
         T = torch.from_numpy((1.0 + 0.1 * rng.standard_normal((nb, r.D))).astype(np.float32)).to(dev)
         sides = ("items", "users", "bins")
         log(f"time bins ({nb}) and their layout: {time.perf_counter() - t_b:.1f} s")
+        if args.bptf:
+            bptf = BPTFSteps(r, als, nb, args.warmup + args.steps, r.init_seed + 88)
 
     def half(side, k):
+        if bptf is not None:
+            bptf.mode(als, side, k, U, V, T)
+            return
         if args.tensor:
             als.tensor_half_sweep(side, U, V, T, r.lam)
             return
@@ -370,10 +435,12 @@ def main():
     prof = als.profile()
     als.set_profiling(False)
     elapsed = t1 - t0
-    rmse_in = als.rmse_in()
-    rmse = als.tensor_rmse(U, V, T) if args.tensor else als.rmse(U, V)
+    # (the time chain's draw runs as two passes of half the bins each, so the entering-state
+    # figure of its last pass covers the odd bins only)
+    rmse_in = None if args.bptf else als.rmse_in()
+    rmse = als.tensor_rmse(U, V, T) if (args.tensor or args.bptf) else als.rmse(U, V)
     gram_share = None
-    if r.D > 20 and not args.tensor:
+    if r.D > 20 and not (args.tensor or args.bptf):
         # one extra, untimed half-sweep per side with the row kernel's phase clocks on
         als.set_phase_timing(True)
         half("items", args.warmup + args.steps - 1)
@@ -383,7 +450,7 @@ def main():
         als.set_phase_timing(False)
         gram_share = (gi + gu) / max(gi + si + gu + su, 1.0)
     log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
-        f"rmse entering last half-sweep {rmse_in:.6f}, final {rmse:.6f}")
+        f"rmse entering last half-sweep {rmse_in}, final {rmse:.6f}")
 
     value = len(sides) * r.nnz * args.steps / elapsed
     halves = len(sides) * args.steps
@@ -391,20 +458,24 @@ def main():
         als.plan_stats("items")["rows_with_ratings"]
     if args.tensor:
         rows_with += int(np.unique(bins).size)
+    if args.bptf:
+        # every user, item and bin is drawn (rows without ratings from their priors)
+        rows_with = r.M + r.N + workload.N_TIME_BINS
     D = r.D
     workload_name = r.name + ("_wals" if args.weighted else "_bpmf" if args.gibbs else
-                              "_tensor" if args.tensor else "")
+                              "_tensor" if args.tensor else "_bptf" if args.bptf else "")
+    tensor_like = args.tensor or args.bptf
     dominant = max(prof, key=lambda k: prof[k][0])
     # per rating: a weight (weighted ALS); the second index and second gathered row, and
     # the product of the two rows (tensor ALS)
-    wbytes = 4 if args.weighted else (4 + 4 * D) if args.tensor else 0
-    wflops = D if (args.weighted or args.tensor) else 0
+    wbytes = 4 if args.weighted else (4 + 4 * D) if tensor_like else 0
+    wflops = D if (args.weighted or tensor_like) else 0
     if D <= 20:
         # gather kernel: per rating the index, the rating (and weight) and the gathered fixed
         # row; per solved row the row pointer and the entering value
         k_ms, k_n = prof["gather"]
         alg = halves * r.nnz * (5 + wbytes + 4 * D) + args.steps * rows_with * (8 + 4 * D)
-        if args.tensor:
+        if tensor_like:
             # per step: every rating twice with one large gathered row (the user and item
             # modes) and once with two (the time-bin mode), plus both indices and the rating
             # each time; the time-bin table (6649 rows) once per user and item mode
@@ -439,18 +510,23 @@ def main():
                           method="chunk-kernel time plus the row kernel's time scaled by the "
                                  "share of wavefront clock cycles before the factorisation")
 
-    heldout = heldout_leg(args, r, als, U, V, workload_name) if args.heldout_share > 0 else None
+    # (the held-out leg scores u . v pairs: the matrix model's prediction, so not for the
+    # three-way models)
+    heldout = (heldout_leg(args, r, als, U, V, workload_name)
+               if args.heldout_share > 0 and not tensor_like else None)
 
     cpu = None
     if args.cpu_seconds > 0:
         log("cpu baseline: fp64 oracle on a sample of the user half-sweep ...")
-        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights, gibbs=args.gibbs,
-                           tensor=(bins, T.cpu().numpy()) if args.tensor else None)
+        cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights,
+                           gibbs=args.gibbs or args.bptf,
+                           tensor=(bins, T.cpu().numpy()) if tensor_like else None)
         log(f"cpu baseline: {cpu}")
 
     out = {
         "metric": ("wALS" if args.weighted else "BPMF Gibbs" if args.gibbs else
-                   "tensor ALS" if args.tensor else "ALS") + " ratings/sec per half-sweep",
+                   "tensor ALS" if args.tensor else "BPTF Gibbs" if args.bptf else "ALS")
+        + " ratings/sec per half-sweep",
         "value": value,
         "unit": "ratings/s",
         "n_gpus": 1,
@@ -465,14 +541,21 @@ def main():
         "config": {"workload": workload_name, "n_users": r.M, "n_items": r.N, "nnz": r.nnz, "D": r.D,
                    "weights": ("per rating, log-uniform on [0.25, 4), seeded" if args.weighted
                                else None),
-                   "lambda": None if args.gibbs else r.lam,
+                   "lambda": None if (args.gibbs or args.bptf) else r.lam,
                    "gibbs": (dict(alpha=GIBBS_ALPHA, mu0=0.0, beta0=GIBBS_BETA0, W0="I",
                                   nu0=r.D, variates="seeded, on the device before timing")
-                             if args.gibbs else None),
-                   "time_bins": workload.N_TIME_BINS if args.tensor else None,
+                             if args.gibbs else
+                             dict(alpha_prior=dict(w0=BPTF_ALPHA_W0, nu0=BPTF_ALPHA_NU0),
+                                  mu0="0 (users, items), 1 (time chain)", beta0=GIBBS_BETA0,
+                                  W0="I", nu0=r.D, variates="seeded, on the device before timing")
+                             if args.bptf else None),
+                   "time_bins": workload.N_TIME_BINS if tensor_like else None,
                    "step": ("item side (hyperparameter draw, row draws) + user side"
                             if args.gibbs else "item, user and time-bin mode updates"
-                            if args.tensor else "item half-sweep + user half-sweep"),
+                            if args.tensor else
+                            "alpha and three hyperparameter draws, then item, user and "
+                            "time-bin (even, then odd) draws" if args.bptf else
+                            "item half-sweep + user half-sweep"),
                    "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,

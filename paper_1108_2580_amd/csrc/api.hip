@@ -449,13 +449,15 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 // New-state residual pass over a side's pieces + fixed-order reduction into
 // d_sse_total; the fixed side must already be staged in d_fpad.
+// n_fixed: the rows of the staged fixed side (d_fpad), whose next row is the zero row.
 als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, const uint8_t *val,
-                         const float *X, const als::Hadamard &hd = als::Hadamard{}) {
+                         int64_t n_fixed, const float *X,
+                         const als::Hadamard &hd = als::Hadamard{}) {
   const int64_t n = (int64_t)P.gitems.size();
   {
     PhaseTimer t(c, 3);
-    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_gitems, n, idx, val, c->d_fpad, X, c->D,
-                                     c->d_sse_items, hd, c->stream));
+    HIP_OR_FAIL(c, als::launch_resid(c->DP, P.d_gitems, n, idx, val, c->d_fpad, n_fixed, X,
+                                     c->D, c->d_sse_items, hd, c->stream));
   }
   {
     PhaseTimer t(c, 4);
@@ -771,7 +773,7 @@ als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out
     ctx->cyc[side][1] += ctx->h_cyc_sum[1];
   }
   if (rmse_out) {
-    als_status st = residual_pass(ctx, P, idx, val, out_factors, hd);
+    als_status st = residual_pass(ctx, P, idx, val, n_fixed, out_factors, hd);
     if (st != ALS_OK) return st;
     HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                     hipMemcpyDeviceToHost, ctx->stream));
@@ -957,7 +959,7 @@ als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_o
     HIP_OR_FAIL(ctx, als::launch_stage_fixed(V, ctx->N, ctx->D, ctx->DP, ctx->d_fpad,
                                              ctx->stream));
   }
-  als_status st = residual_pass(ctx, P, ctx->d_col, ctx->d_val, U);
+  als_status st = residual_pass(ctx, P, ctx->d_col, ctx->d_val, ctx->N, U);
   if (st != ALS_OK) return st;
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
@@ -1288,7 +1290,8 @@ als_status als_tensor_rmse(als_ctx *ctx, const float *U, const float *V, const f
   als::Hadamard hd;
   hd.idx2 = ctx->d_tbin;
   hd.Tp = ctx->d_fpad2;
-  als_status st = residual_pass(ctx, ctx->plan[ALS_ROWS_USERS], ctx->d_col, ctx->d_val, U, hd);
+  als_status st = residual_pass(ctx, ctx->plan[ALS_ROWS_USERS], ctx->d_col, ctx->d_val, ctx->N,
+                                U, hd);
   if (st != ALS_OK) return st;
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, ctx->d_sse_total, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));

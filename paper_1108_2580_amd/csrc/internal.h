@@ -117,10 +117,10 @@ hipError_t launch_rows(int dp, const RowTask *rows, int64_t n_rows, const int32_
                        const Hadamard &hd, hipStream_t s);
 
 // Per-item sums of squared residuals with the rows of X against the staged
-// fixed side Fp (row stride DP) (residual.hip).
+// fixed side Fp (row stride DP, n_fixed rows and the zero row) (residual.hip).
 hipError_t launch_resid(int dp, const WorkItem *items, int64_t n_items, const int32_t *idx,
-                        const uint8_t *val, const float *Fp, const float *X, int D,
-                        double *sse_items, const Hadamard &hd, hipStream_t s);
+                        const uint8_t *val, const float *Fp, int64_t n_fixed, const float *X,
+                        int D, double *sse_items, const Hadamard &hd, hipStream_t s);
 
 // Widths solved one row per lane (registers hold the packed normal equations).
 inline int lane_width(int D) { return D <= 16 ? 16 : (D <= 20 ? 20 : 0); }
