@@ -304,3 +304,95 @@ def test_bptf_argument_errors():
             als.tensor_gibbs_half_sweep("users", Ud, Vd, Td, 1.0, Lam, mu, dev(np.zeros((M, D))))
         als.set_weights(None)
         als.tensor_gibbs_half_sweep("users", Ud, Vd, Td, 1.0, Lam, mu, dev(np.zeros((M, D))))
+
+
+def sub_chain(p, i1, i2, v, T, k):
+    """The bins around bin k (k - 1, k, k + 1 where they exist) with bin k's ratings only,
+    and the position of k in it: its conditional is the same as in the whole chain (first
+    bin: the mean mu_T; last bin: one neighbour)."""
+    K = T.shape[0]
+    lo, hi = max(k - 1, 0), min(k + 1, K - 1)
+    n = int(p[k + 1] - p[k])
+    pos = k - lo
+    counts = np.zeros(hi - lo + 1, dtype=np.int64)
+    counts[pos] = n
+    ptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    sl = slice(p[k], p[k + 1])
+    return ptr, i1[sl], i2[sl], v[sl], T[lo:hi + 1], pos
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("k", [3, 4])
+def test_full_size_bptf_sampled(k):
+    """Full-size workload with 6649 time bins: one draw of each mode from the seeded state
+    (the bins even, then odd), checked on sampled users and items (largest, smallest and
+    random) and on sampled bins through their neighbourhood sub-chains."""
+    from paper_1108_2580_amd import ALS
+    from tests.test_gpu_full import sample_rows
+
+    r = workload.make_config(k)
+    D = r.D
+    K = workload.N_TIME_BINS
+    bins = workload.time_bins(r.row_ptr, K, workload.time_seed(3))
+    U0, V0 = workload.init_factors(r.M, r.N, D, r.init_seed)
+    rng = np.random.default_rng(61 + k)
+    T0 = (1.0 + 0.1 * rng.standard_normal((K, D))).astype(np.float32)
+    val = r.val.astype(np.float64)
+    by_user = (r.row_ptr, r.col, bins, val)
+    cp, cu, cv = oracle.transpose(r.row_ptr, r.col, val, r.N)
+    _, _, cb = oracle.transpose(r.row_ptr, r.col, bins.astype(np.float64), r.N)
+    by_item = (cp, cu, cb.astype(np.int32), cv)
+    bp, bu, bv = oracle.transpose(r.row_ptr, bins, val, K)
+    _, _, bi = oracle.transpose(r.row_ptr, bins, r.col.astype(np.float64), K)
+    by_bin = (bp, bu, bi.astype(np.int32), bv)
+    alpha = 1.0 / 900.0
+    log(f"full-size bptf {r.name}: {K} bins")
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, D) as als:
+        als.set_time_bins(K, bins)
+        for mode, groups, nsamp in (("items", by_item, 256), ("users", by_user, 256)):
+            Lam, mu = spd(rng, D, 2.0), rng.normal(0, 0.05, size=D)
+            n = r.N if mode == "items" else r.M
+            z = rng.standard_normal((n, D), dtype=np.float32)
+            U, V, T = dev(U0), dev(V0), dev(T0)
+            als.tensor_gibbs_half_sweep(mode, U, V, T, alpha, dev(Lam, np.float64),
+                                        dev(mu, np.float64), dev(z))
+            assert als.flagged_rows() == 0
+            F1, F2, X = (U0, T0, V0) if mode == "items" else (V0, T0, U0)
+            xg = (V if mode == "items" else U).cpu().numpy()
+            p, i1, i2, v = groups
+            rows = sample_rows(p, 9 + k)
+            rows = np.unique(np.concatenate([rows[:8], rows[-8:], rows[8:8 + nsamp]]))
+            sub_ptr = np.concatenate([[0], np.cumsum(p[rows + 1] - p[rows])]).astype(np.int64)
+            take = np.concatenate([np.arange(p[s], p[s + 1]) for s in rows])
+            xo, fl = oracle.tensor_gibbs_rows(sub_ptr, i1[take], i2[take], v[take], F1, F2, alpha,
+                                              Lam, mu, z[rows], X[rows])
+            assert not fl.any()
+            rr = rel_rows(xg[rows], xo)
+            log(f"  mode={mode}: {rows.size} sampled rows, max rel {rr.max():.2e}")
+            assert rr.max() <= ROW_TOL
+            assert np.isfinite(xg).all()
+        # the chain
+        Lam, mu = spd(rng, D, 20.0), 1.0 + rng.normal(0, 0.01, size=D)
+        z = rng.standard_normal((K, D), dtype=np.float32)
+        U, V, T = dev(U0), dev(V0), dev(T0)
+        als.tensor_gibbs_half_sweep("bins", U, V, T, alpha, dev(Lam, np.float64),
+                                    dev(mu, np.float64), dev(z))
+        assert als.flagged_rows() == 0
+        tg = T.cpu().numpy()
+    p, i1, i2, v = by_bin
+    picks = np.unique(np.concatenate([[0, 1, K - 2, K - 1],
+                                      np.random.default_rng(5 + k).choice(K, 40, replace=False)]))
+    te = T0.astype(np.float64).copy()
+    te[0::2] = tg[0::2]  # the odd bins are drawn given the GPU's even bins
+    worst = 0.0
+    for b in picks:
+        state = T0.astype(np.float64) if b % 2 == 0 else te
+        sp, s1, s2, sv, sT, pos = sub_chain(p, i1, i2, v, state, int(b))
+        sz = np.zeros((sT.shape[0], D))
+        sz[pos] = z[b]
+        parity = pos % 2
+        to, fl = oracle.time_rows(sp, s1, s2, sv, U0, V0, alpha, Lam, mu, sz, parity, sT)
+        assert not fl.any()
+        worst = max(worst, float(rel_rows(tg[b:b + 1], to[pos:pos + 1])[0]))
+    log(f"  chain: {picks.size} sampled bins, max rel {worst:.2e}")
+    assert worst <= ROW_TOL
