@@ -142,6 +142,8 @@ struct als_ctx {
   float *d_time_h0 = nullptr;      // per-bin prior right-hand side [n_bins x D]
   int64_t time_h0_bins = 0;
   double *d_time_extra = nullptr;  // step scatter of the chain, D (D + 1) / 2
+  double *d_time_partials = nullptr;  // its per-slice partial sums
+  int64_t time_partials_cap = 0;
   double *d_zero_mu = nullptr;     // D zeros (the chain's image has no mean term)
 };
 
@@ -387,6 +389,7 @@ void free_ctx(als_ctx *c) {
   }
   dfree(c->d_time_h0);
   dfree(c->d_time_extra);
+  dfree(c->d_time_partials);
   dfree(c->d_zero_mu);
   if (c->h_cyc_sum) (void)hipHostFree(c->h_cyc_sum);
   for (auto &pe : c->prof_pending) {
@@ -1412,15 +1415,23 @@ als_status als_sample_time_hyper(als_ctx *ctx, const float *T, const double *chi
   if (!T || !chi2 || (!offdiag && ctx->D > 1) || !z_mu || !mu_out || !Lambda_out)
     return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
   DeviceGuard g(ctx->device);
+  const int64_t ntri = (int64_t)ctx->D * (ctx->D + 1) / 2;
   als_status st = ensure_bayes(ctx);
-  if (st == ALS_OK)
-    st = ensure(ctx, &ctx->d_time_extra, (size_t)ctx->D * (ctx->D + 1) / 2, "chain scatter");
+  if (st == ALS_OK) st = ensure(ctx, &ctx->d_time_extra, (size_t)ntri, "chain scatter");
   if (st != ALS_OK) return st;
+  int64_t per = 0, nblk = 0;
+  als::time_step_blocks(ctx->n_bins, ctx->D, per, nblk);
+  if (nblk * ntri > ctx->time_partials_cap) {
+    HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+    dfree(ctx->d_time_partials);
+    HIP_OR_FAIL(ctx, dalloc(&ctx->d_time_partials, nblk * ntri));
+    ctx->time_partials_cap = nblk * ntri;
+  }
   HIP_OR_FAIL(ctx, als::launch_time_hyper(T, ctx->n_bins, ctx->D, ctx->d_nw_mu0[2],
                                           ctx->nw_beta0[2], ctx->d_nw_W0inv[2], ctx->nw_nu0[2],
                                           chi2, offdiag, z_mu, ctx->d_bayes_scratch,
-                                          ctx->d_time_extra, mu_out, Lambda_out,
-                                          ctx->d_hyper_status, ctx->stream));
+                                          ctx->d_time_partials, ctx->d_time_extra, mu_out,
+                                          Lambda_out, ctx->d_hyper_status, ctx->stream));
   if (status_out) {
     HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_hyper_status, ctx->d_hyper_status, sizeof(int32_t),
                                     hipMemcpyDeviceToHost, ctx->stream));

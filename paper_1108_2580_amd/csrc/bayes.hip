@@ -26,11 +26,13 @@
 //                     alpha (m_k = mu_T for the first bin, else T_{k-1}) for the bins of
 //                     one parity, in fp64; the bins of a parity are drawn together given
 //                     the other parity.
-//   k_time_moments    the chain's posterior inputs: the moments of T_0 alone (n = 1) in
-//                     the segment layout k_hyper_sample reads, and the step scatter
-//                     sum_{k>=1} (T_k - T_{k-1})(T_k - T_{k-1})^T with the differences
-//                     formed in fp64 (exact for fp32 inputs), which k_hyper_sample adds
-//                     to W*^{-1}.
+//   k_time_moments    the moments of T_0 alone (n = 1), in the segment layout
+//                     k_hyper_sample reads;
+//   k_time_steps      the chain's step scatter sum_{k>=1} (T_k - T_{k-1})(T_k - T_{k-1})^T
+//                     over a slice of the chain per block (the slice's bins staged in
+//                     LDS, differences formed in fp64, exact for fp32 inputs), and
+//   k_time_steps_sum  the slices added in order; k_hyper_sample adds the result to
+//                     W*^{-1}.
 // The variates (chi-square, normals) are inputs. Matrices live as fp64
 // packed triangles in LDS (two of them, 132 KB at D = 128); the factorisations are
 // right-looking Cholesky steps with a barrier between steps.
@@ -45,6 +47,8 @@ constexpr int kStageFloats = 16384;  // LDS stage of the moment kernel (64 KB of
 constexpr int kHyperBlocks = 1024;
 constexpr int kReduceSegs = 16;      // the moment partials are summed in 16 segments
 constexpr int kMaxD = 128;
+constexpr int kStepBlocks = 64;          // slices of the time chain's step scatter
+constexpr int kStepStageFloats = 15360;  // LDS stage of a slice (60 KB)
 constexpr int kPacked = kMaxD * (kMaxD + 1) / 2;
 // 4 x 4 tiles of the upper block triangle of x x^T, per thread at most this many
 constexpr int kTilesPerThread = ((kMaxD / 4) * (kMaxD / 4 + 1) / 2 + kBayesBlock - 1) / kBayesBlock;
@@ -442,35 +446,56 @@ __global__ __launch_bounds__(256) void k_time_rhs(const float *__restrict__ T, i
   h0[k * D + a] = (float)(acc * inv_alpha);
 }
 
-__global__ __launch_bounds__(256) void k_time_moments(const float *__restrict__ T, int64_t K,
-                                                      int D, double *__restrict__ seg_sums,
-                                                      double *__restrict__ extra) {
-  const int ne = D + D * (D + 1) / 2, ntri = D * (D + 1) / 2;
-  const int total = kReduceSegs * ne + ntri;
-  for (int q = blockIdx.x * 256 + threadIdx.x; q < total; q += gridDim.x * 256) {
-    if (q < kReduceSegs * ne) {
-      const int g = q / ne, e = q % ne;
-      double v = 0.0;
-      if (g == 0) {
-        if (e < D) {
-          v = (double)T[e];
-        } else {
-          int a, b;
-          upper_entry(e - D, D, a, b);
-          v = (double)T[a] * (double)T[b];
-        }
+__global__ __launch_bounds__(256) void k_time_moments(const float *__restrict__ T, int D,
+                                                      double *__restrict__ seg_sums) {
+  const int ne = D + D * (D + 1) / 2;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < kReduceSegs * ne; q += gridDim.x * 256) {
+    const int g = q / ne, e = q % ne;
+    double v = 0.0;
+    if (g == 0) {
+      if (e < D) {
+        v = (double)T[e];
+      } else {
+        int a, b;
+        upper_entry(e - D, D, a, b);
+        v = (double)T[a] * (double)T[b];
       }
-      seg_sums[q] = v;
-    } else {
-      int a, b;
-      upper_entry(q - kReduceSegs * ne, D, a, b);
-      double acc = 0.0;
-      for (int64_t k = 1; k < K; ++k)
-        acc += ((double)T[k * D + a] - (double)T[(k - 1) * D + a]) *
-               ((double)T[k * D + b] - (double)T[(k - 1) * D + b]);
-      extra[q - kReduceSegs * ne] = acc;
     }
+    seg_sums[q] = v;
   }
+}
+
+// Block b takes the steps k = 1 + b per .. min(K, 1 + (b + 1) per) - 1, with the bins
+// k - 1 .. of its slice staged in LDS (dynamic, (per + 1) D floats).
+__global__ __launch_bounds__(256) void k_time_steps(const float *__restrict__ T, int64_t K, int D,
+                                                    int64_t per, double *__restrict__ partials) {
+  extern __shared__ float rows[];
+  const int ntri = D * (D + 1) / 2;
+  const int64_t k0 = 1 + (int64_t)blockIdx.x * per;
+  const int64_t k1 = min(K, k0 + per);
+  double *__restrict__ out = partials + (int64_t)blockIdx.x * ntri;
+  const int nr = k0 < K ? (int)(k1 - k0 + 1) : 0;  // bins k0 - 1 .. k1 - 1
+  for (int q = threadIdx.x; q < nr * D; q += 256) rows[q] = T[(k0 - 1) * D + q];
+  __syncthreads();
+  for (int q = threadIdx.x; q < ntri; q += 256) {
+    int a, b;
+    upper_entry(q, D, a, b);
+    double acc = 0.0;
+    for (int r = 1; r < nr; ++r)
+      acc += ((double)rows[r * D + a] - (double)rows[(r - 1) * D + a]) *
+             ((double)rows[r * D + b] - (double)rows[(r - 1) * D + b]);
+    out[q] = acc;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_time_steps_sum(const double *__restrict__ partials,
+                                                        int nblk, int ntri,
+                                                        double *__restrict__ extra) {
+  const int q = blockIdx.x * 256 + threadIdx.x;
+  if (q >= ntri) return;
+  double t = 0.0;
+  for (int b = 0; b < nblk; ++b) t += partials[(int64_t)b * ntri + q];
+  extra[q] = t;
 }
 
 }  // namespace
@@ -535,18 +560,35 @@ hipError_t launch_time_rhs(const float *T, int64_t K, int D, const double *Lam, 
   return hipGetLastError();
 }
 
+void time_step_blocks(int64_t K, int D, int64_t &per, int64_t &nblk) {
+  const int64_t steps = std::max<int64_t>(K - 1, 0);
+  const int64_t max_rows = kStepStageFloats / D;  // staged bins per block
+  per = std::max<int64_t>(1, std::min<int64_t>((steps + kStepBlocks - 1) / kStepBlocks,
+                                               max_rows - 1));
+  nblk = std::max<int64_t>(1, (steps + per - 1) / per);
+}
+
 hipError_t launch_time_hyper(const float *T, int64_t K, int D, const double *mu0, double beta0,
                              const double *W0inv, double nu0, const double *chi2,
                              const double *offd, const double *zmu, double *scratch,
-                             double *extra, double *mu_out, double *Lam_out, int32_t *status,
-                             hipStream_t s) {
+                             double *step_partials, double *extra, double *mu_out,
+                             double *Lam_out, int32_t *status, hipStream_t s) {
   if (D < 1 || D > 128 || K < 1) return hipErrorInvalidValue;
-  const int ne = hyper_entries(D);
+  const int ne = hyper_entries(D), ntri = D * (D + 1) / 2;
   double *seg_sums = scratch + ne + 8;
-  const int total = kReduceSegs * ne + D * (D + 1) / 2;
-  hipLaunchKernelGGL(k_time_moments, dim3((unsigned)std::min(1024, (total + 255) / 256)),
-                     dim3(256), 0, s, T, K, D, seg_sums, extra);
+  hipLaunchKernelGGL(k_time_moments, dim3((unsigned)((kReduceSegs * ne + 255) / 256)), dim3(256),
+                     0, s, T, D, seg_sums);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int64_t per = 0, nblk = 0;
+  time_step_blocks(K, D, per, nblk);
+  hipLaunchKernelGGL(k_time_steps, dim3((unsigned)nblk), dim3(256),
+                     (size_t)(per + 1) * D * sizeof(float), s, T, K, D, per, step_partials);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_time_steps_sum, dim3((unsigned)((ntri + 255) / 256)), dim3(256), 0, s,
+                     step_partials, (int)nblk, ntri, extra);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_hyper_sample, dim3(1), dim3(kBayesBlock), 0, s, seg_sums, (int64_t)1, D,
                      mu0, beta0, W0inv, nu0, chi2, offd, zmu, (const double *)extra, scratch,

@@ -193,12 +193,15 @@ hipError_t launch_hyper_sample(const double *partials, int nblk, int64_t n, int 
 hipError_t launch_time_rhs(const float *T, int64_t K, int D, const double *Lam, const double *mu,
                            double alpha, int parity, float *h0, hipStream_t s);
 // The chain's Normal-Wishart posterior (the moments of T_0 as one row, plus the step
-// scatter in extra, D (D + 1) / 2 doubles) and the Bartlett draw of (mu_T, Lambda_T).
+// scatter in extra, D (D + 1) / 2 doubles, summed over nblk slices of per steps each from
+// step_partials, nblk x D (D + 1) / 2 doubles; time_step_blocks gives the split) and the
+// Bartlett draw of (mu_T, Lambda_T).
+void time_step_blocks(int64_t K, int D, int64_t &per, int64_t &nblk);
 hipError_t launch_time_hyper(const float *T, int64_t K, int D, const double *mu0, double beta0,
                              const double *W0inv, double nu0, const double *chi2,
                              const double *offd, const double *zmu, double *scratch,
-                             double *extra, double *mu_out, double *Lam_out, int32_t *status,
-                             hipStream_t s);
+                             double *step_partials, double *extra, double *mu_out,
+                             double *Lam_out, int32_t *status, hipStream_t s);
 
 // Predictions u_{users[p]} . v_{items[p]} of n pairs (predict.hip). pred (nullable)
 // receives them, NaN for a pair with an index outside [0, M) x [0, N). With
