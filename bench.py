@@ -512,6 +512,15 @@ def main():
 
     # (the held-out leg scores u . v pairs: the matrix model's prediction, so not for the
     # three-way models)
+    # the factorisation and triangular solves on their own: the one-lane solve kernel at
+    # D <= 20; at D > 20 the fused row kernel's time scaled by the share of its wavefront
+    # cycles from the factorisation on (phase clocks; plain ALS and BPMF)
+    if D <= 20:
+        chol_ms = prof["solve"][0] / args.steps
+    elif gram_share is not None:
+        chol_ms = (1.0 - gram_share) * prof["solve"][0] / args.steps
+    else:
+        chol_ms = None
     heldout = (heldout_leg(args, r, als, U, V, workload_name)
                if args.heldout_share > 0 and not tensor_like else None)
 
@@ -561,6 +570,7 @@ def main():
         "cpu_baseline": cpu,
         "per_side": per_side,
         "gram_phase": gram_phase,
+        "chol_ms_per_step": chol_ms,
         "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
         "rmse": rmse,
         "rmse_entering_last_half_sweep": rmse_in,
