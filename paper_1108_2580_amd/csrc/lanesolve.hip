@@ -153,22 +153,51 @@ __global__ __launch_bounds__(64) void k_solve_lane(const RowTask *__restrict__ r
                                                    RowPrior pr) {
   constexpr int NTRI = LD * (LD + 1) / 2;
   constexpr int NES = ne_floats(LD);
-  const int64_t i = (int64_t)blockIdx.x * 64 + threadIdx.x;
+  constexpr int NQ = NES / 4;               // float4 of a record
+  constexpr int ROUNDS = 4;                 // the records are read in four slices
+  constexpr int QS = (NQ + ROUNDS - 1) / ROUNDS;
+  constexpr int STRIDE = QS | 1;            // odd LDS row stride (in float4)
+  __shared__ float4 s_rec[64 * STRIDE];
+  const int lane = threadIdx.x;
+  const int64_t first = (int64_t)blockIdx.x * 64;
+  const int64_t i = first + lane;
+  const int64_t nrec = n_rows - first < 64 ? n_rows - first : 64;  // >= 1
+  const float4 *__restrict__ recs = reinterpret_cast<const float4 *>(ne) + (base + first) * NQ;
+  float A[NTRI], b[LD];
+  // The block's 64 records are contiguous: each slice is read with consecutive lanes on
+  // consecutive float4 (record rr, float4 q0 + pc), staged in LDS, and every lane takes its
+  // own record's part; lanes past the last row read the last record again.
+#pragma unroll
+  for (int h = 0; h < ROUNDS; ++h) {
+    const int q0 = h * QS;
+    const int nq = NQ - q0 < QS ? NQ - q0 : QS;
+#pragma unroll
+    for (int k = 0; k < QS; ++k) {
+      if (k < nq) {
+        const int f = k * 64 + lane;
+        const int rr = f / nq, pc = f - rr * nq;
+        const int64_t rec = rr < nrec ? rr : nrec - 1;
+        s_rec[rr * STRIDE + pc] = recs[rec * NQ + q0 + pc];
+      }
+    }
+    wave_sync();
+#pragma unroll
+    for (int pc = 0; pc < QS; ++pc) {
+      if (pc < nq) {
+        const float4 v = s_rec[lane * STRIDE + pc];
+        const float w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = 4 * (q0 + pc) + j;
+          if (e < NTRI) A[e] = w[j];
+          else if (e < NTRI + LD) b[e - NTRI] = w[j];
+        }
+      }
+    }
+    wave_sync();  // the stage is refilled by the next slice
+  }
   if (i >= n_rows) return;
   const RowTask rt = rows[i];
-  float A[NTRI], b[LD];
-  const float4 *__restrict__ p = reinterpret_cast<const float4 *>(ne + (base + i) * NES);
-#pragma unroll
-  for (int q = 0; q < NES / 4; ++q) {
-    const float4 v = p[q];
-    const float w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = 4 * q + j;
-      if (e < NTRI) A[e] = w[j];
-      else if (e < NTRI + LD) b[e - NTRI] = w[j];
-    }
-  }
   if constexpr (BAYES) {
     // the prior image carries the identity on the padding; the time chain scales it per
     // row and adds the row's own right-hand side
