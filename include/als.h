@@ -378,6 +378,8 @@ als_status als_tensor_gibbs_half_sweep(als_ctx *ctx, als_mode mode, float *U, fl
 als_status als_tensor_sample_alpha(als_ctx *ctx, const float *U, const float *V, const float *T,
                                    double w0, double chi2, double *alpha_out);
 
+/* Release the context and every device buffer it owns (after synchronising its stream);
+ * NULL is ignored. Caller-owned factor buffers are untouched. */
 void als_destroy(als_ctx *ctx);
 
 const char *als_status_str(als_status s);
