@@ -7,7 +7,6 @@ seeded random rows. Bars as in the small tests: relative row error <= 1e-4 after
 half-sweep from the seeded initial factors; the RMSE returned with the half-sweep equals
 the fp64 residual of the GPU state within 1e-5; no row flagged; every factor finite.
 """
-import os
 import sys
 
 import numpy as np
@@ -74,8 +73,7 @@ def test_full_first_half_sweep_sampled(k):
             assert abs(rm - ro) <= RMSE_TOL
 
 
-@pytest.mark.skipif(os.environ.get("ALS_FULL_TRAJECTORY") != "1",
-                    reason="several minutes of host fp64 work; set ALS_FULL_TRAJECTORY=1")
+@pytest.mark.slow
 @pytest.mark.timeout(1500)
 def test_full_d20_free_running_rmse():
     """Five free-running sweeps at full size, D = 20: GPU fp32 vs oracle fp64 trajectory."""
