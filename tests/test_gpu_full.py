@@ -7,6 +7,7 @@ seeded random rows. Bars as in the small tests: relative row error <= 1e-4 after
 half-sweep from the seeded initial factors; the RMSE returned with the half-sweep equals
 the fp64 residual of the GPU state within 1e-5; no row flagged; every factor finite.
 """
+import os
 import sys
 
 import numpy as np
@@ -91,6 +92,36 @@ def test_full_d20_free_running_rmse():
             ro = t.rmse()
             log(f"  sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
         assert abs(rm - ro) <= RMSE_TOL
+
+
+@pytest.mark.slow
+@pytest.mark.skipif(os.environ.get("ALS_FULL_TRAJECTORY_WIDE") != "1",
+                    reason="5 to 7 minutes of host fp64 work per workload; "
+                           "set ALS_FULL_TRAJECTORY_WIDE=1")
+@pytest.mark.timeout(1100)
+@pytest.mark.parametrize("k", [4, 5])
+def test_full_wide_free_running_rmse(k):
+    """Three free-running sweeps at full size, D = 100 and D = 128 (the hub workload): the
+    GPU fp32 trajectory against the oracle's fp64 one, the RMSE after every sweep within
+    1e-5."""
+    from paper_1108_2580_amd import ALS
+
+    r = workload.make_config(k)
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    t = oracle.Trajectory(r.M, r.N, r.row_ptr, r.col, r.val, U0, V0, r.lam)
+    log(f"wide free running {r.name}, {r.sweeps} sweeps")
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        U, V = dev(U0), dev(V0)
+        for sweep in range(1, r.sweeps + 1):
+            als.half_sweep("items", U, r.lam, V)
+            rm = als.half_sweep("users", V, r.lam, U, rmse=True)
+            log(f"  sweep {sweep}: gpu {rm:.9f}; oracle running ...")
+            t.step("items")
+            log(f"    oracle items done")
+            t.step("users")
+            ro = t.rmse()
+            log(f"  sweep {sweep}: gpu {rm:.9f} oracle {ro:.9f} diff {rm - ro:.2e}")
+            assert abs(rm - ro) <= RMSE_TOL
 
 
 @pytest.mark.parametrize("k", [3, 4])
