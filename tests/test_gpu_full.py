@@ -74,6 +74,48 @@ def test_full_first_half_sweep_sampled(k):
             assert abs(rm - ro) <= RMSE_TOL
 
 
+def every_row_check(k):
+    """One half-sweep per side from the seeded factors at full size, every row against the
+    oracle's solve of the same row (p50, p99 and max of the relative row error)."""
+    from paper_1108_2580_amd import ALS
+
+    r = workload.make_config(k)
+    U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
+    val = r.val.astype(np.float64)
+    csc = oracle.transpose(r.row_ptr, r.col, val, r.N)
+    log(f"every row of {r.name}")
+    with ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D) as als:
+        for side, fixed, prev, (p, i, v) in (("items", U0, V0, csc),
+                                             ("users", V0, U0, (r.row_ptr, r.col, val))):
+            out = dev(prev)
+            als.half_sweep(side, dev(fixed), r.lam, out)
+            assert als.flagged_rows() == 0
+            xg = out.cpu().numpy()
+            log(f"  {side}: oracle half-sweep of {p.size - 1} rows ...")
+            xo, fl = oracle.half_sweep(p, i, v, fixed, r.lam, prev)
+            assert not (fl == 1).any()
+            has = np.diff(p) > 0
+            rel = (np.linalg.norm(xg[has] - xo[has], axis=1)
+                   / np.maximum(np.linalg.norm(xo[has], axis=1), 1e-30))
+            log(f"  {side}: {has.sum()} rows, rel p50={np.median(rel):.2e} "
+                f"p99={np.percentile(rel, 99):.2e} max={rel.max():.2e}")
+            assert rel.max() <= ROW_TOL
+            assert np.array_equal(xg[~has], prev[~has])
+
+
+@pytest.mark.slow
+def test_full_d20_every_row():
+    every_row_check(3)
+
+
+@pytest.mark.slow
+@pytest.mark.skipif(os.environ.get("ALS_FULL_TRAJECTORY_WIDE") != "1",
+                    reason="about two minutes of host fp64 work; set ALS_FULL_TRAJECTORY_WIDE=1")
+@pytest.mark.timeout(900)
+def test_full_d100_every_row():
+    every_row_check(4)
+
+
 @pytest.mark.slow
 @pytest.mark.timeout(1500)
 def test_full_d20_free_running_rmse():
