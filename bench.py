@@ -201,6 +201,27 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False, tensor=None
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
 
 
+def one_thread_scale():
+    """For scale beside the all-threads figure: the fp64 oracle on one host thread over the
+    whole user half-sweep of the mid workload (100,000 x 50,000, 10M ratings, D = 20), from
+    its seeded initial factors."""
+    import numpy as np
+
+    import oracle
+    import workload
+
+    m = workload.make_config(2)
+    _, V0 = workload.init_factors(m.M, m.N, m.D, m.init_seed)
+    rows = np.arange(m.M)
+    val = m.val.astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.solve_rows(rows, m.row_ptr, m.col, val, V0.astype(np.float64), m.lam, threads=1)
+    dt = time.perf_counter() - t0
+    return dict(value=m.nnz / dt, unit="ratings/s", cores=1,
+                sample=(f"whole user half-sweep of {m.name} ({m.M} x {m.N}, {m.nnz} ratings, "
+                        f"D={m.D}), fp64, one thread, {dt:.1f} s"))
+
+
 def heldout_leg(args, r, als, U, V, workload_name, reps=20):
     """Held-out predictions r_hat = u . v on a seeded sample of the stored positions (the
     degree distributions of both sides), timed over back-to-back launches of the predict
@@ -530,6 +551,8 @@ def main():
         cpu = cpu_baseline(r, V.cpu().numpy(), args.cpu_seconds, weights,
                            gibbs=args.gibbs or args.bptf,
                            tensor=(bins, T.cpu().numpy()) if tensor_like else None)
+        if not (args.weighted or args.gibbs or tensor_like):
+            cpu["one_thread"] = one_thread_scale()
         log(f"cpu baseline: {cpu}")
 
     out = {
