@@ -106,7 +106,12 @@ struct GroupStage {
   float r[2][64];
   float w[2][64];   // per-rating weights (weighted ALS only)
   int32_t t[2][64]; // second index of each rating (tensor ALS only)
+  // the 16 step partials of every lane, transposed for the end-of-group sums: row group kq,
+  // feature lane c, step s at [kq * kRedGroup + c * kRedRow + s]; the odd row stride keeps
+  // both the row-wise stores and the column-wise loads free of bank conflicts
+  float red[4 * 16 * 17];
 };
+constexpr int kRedRow = 17, kRedGroup = 16 * kRedRow;
 
 // One rating per lane of a 64-rating group: column index, rating, weight and (tensor
 // ALS) the index into the second fixed table.
@@ -288,44 +293,26 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
   }
 }
 
-// The partner of lane c at reduce-scatter level O (within 16-lane rows): c ^ 8, the
-// half-row mirror c ^ 7, then c ^ 2 and c ^ 1. Each pair differs in bit O of the lane
-// and agrees on the bits of the earlier levels, and {8, 7, 2, 1} span all 16 lanes.
-template <int O>
-__device__ __forceinline__ float rs_partner(float v) {
-  if constexpr (O == 8) return row_ror<8>(v);
-  else if constexpr (O == 4) return dpp_move<kDppHalfMirror>(v);
-  else if constexpr (O == 2) return dpp_move<kDppQuadXor2>(v);
-  else return dpp_move<kDppQuadXor1>(v);
-}
-
-template <int O>
-__device__ __forceinline__ void rs_level(float (&pi)[16], int c) {
-  const bool hi = (c & O) != 0;
-#pragma unroll
-  for (int i = 0; i < O; ++i) {
-    const float keep = hi ? pi[O + i] : pi[i];
-    const float give = hi ? pi[i] : pi[O + i];
-    pi[i] = keep + rs_partner<O>(give);
-  }
-}
-
-// End of a 64-rating group: reduce-scatter the 16 step partials over the 16 feature
-// lanes, after which lane c holds the full prediction of step c for its rating group
-// (at each level a lane keeps the half selected by one bit of c and adds the partner's
-// copy of it), and add the squared residuals of the group's ratings.
-__device__ __forceinline__ void group_residuals(float (&pi)[16], const GroupStage &st, int buf,
+// End of a 64-rating group: every lane stores its 16 step partials (feature lane c's
+// share of the predictions of steps 0..15 of its rating group) to LDS, then lane (kq, c)
+// sums the 16 feature lanes' shares of step c in lane order, which gives the full
+// prediction of rating g + 4 c + kq; its squared residual is added to sse.
+__device__ __forceinline__ void group_residuals(const float (&pi)[16], GroupStage &st, int buf,
                                                 int g, int n, double &sse) {
   const int lane = threadIdx.x & 63;
   const int kq = lane >> 4, c = lane & 15;
-  rs_level<8>(pi, c);
-  rs_level<4>(pi, c);
-  rs_level<2>(pi, c);
-  rs_level<1>(pi, c);
-  // lane (kq, c) now holds the prediction of rating g + 4c + kq (step c of row group kq)
+  float *row = &st.red[kq * kRedGroup + c * kRedRow];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) row[u] = pi[u];
+  wave_sync();
+  const float *col = &st.red[kq * kRedGroup + c];
+  float p = col[0];
+#pragma unroll
+  for (int q = 1; q < 16; ++q) p += col[q * kRedRow];
   const float rq = st.r[buf][kq * 16 + c];
+  wave_sync();  // the area is rewritten by the next group
   if (g + 4 * c + kq < n) {
-    const double e = (double)rq - (double)pi[0];
+    const double e = (double)rq - (double)p;
     sse = fma(e, e, sse);
   }
 }

@@ -30,16 +30,15 @@ namespace als {
 // tile) and the per-rating right-hand-side FMAs disappear. WT: weighted ALS, with the
 // per-rating weights wts aligned with idx / val. TS: tensor ALS, whose fixed vectors are
 // the elementwise products Fp[idx] * hd.Tp[hd.idx2].
+// Waves per SIMD: six for plain ALS (79 registers), five for weighted and four for tensor
+// ALS, which gather more per rating; the bound keeps the allocator within each budget.
 template <int DP, int LD, bool AUG, bool WT, bool TS>
-__global__ __launch_bounds__(64) void k_gram_ne(const WorkItem *__restrict__ items,
-                                                int64_t n_chunk_items,
-                                                const int32_t *__restrict__ idx,
-                                                const uint8_t *__restrict__ val,
-                                                const float *__restrict__ wts,
-                                                const float *__restrict__ Fp, int zrow,
-                                                const float *__restrict__ Xold, int D,
-                                                float *__restrict__ ws, float *__restrict__ ne,
-                                                double *__restrict__ sse_out, Hadamard hd) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(TS ? 4 : WT ? 5 : 6)))
+void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
+               const int32_t *__restrict__ idx, const uint8_t *__restrict__ val,
+               const float *__restrict__ wts, const float *__restrict__ Fp, int zrow,
+               const float *__restrict__ Xold, int D, float *__restrict__ ws,
+               float *__restrict__ ne, double *__restrict__ sse_out, Hadamard hd) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
   constexpr int NTRI = LD * (LD + 1) / 2;
