@@ -7,8 +7,9 @@
 // feature 16 X + c of the staged fixed row of rating 4 s + kq for all 16 steps s of the
 // group at once, so that every load instruction reads four rows in contiguous 64-byte
 // segments. Lane (kq, c) forms the per-step partial dot products with its features of
-// x_s; the group's 16 x 16 partials are reduce-scattered over the feature lanes (DPP),
-// after which each lane holds one rating's prediction and adds (r - r_hat)^2 in fp64.
+// x_s; the group's 16 x 16 partials are summed over the feature lanes through an LDS
+// transpose (group_residuals), after which each lane holds one rating's prediction and
+// adds (r - r_hat)^2 in fp64.
 // The wavefront total goes to sse_items[item]; a fixed-order reduction over the items
 // follows. TS (tensor ALS): f is the elementwise product of the staged rows Fp[j] and
 // hd.Tp[t], t the rating's second index.

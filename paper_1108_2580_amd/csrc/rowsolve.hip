@@ -519,8 +519,8 @@ static hipError_t launch_rows_t(const RowTask *rows, int64_t n_rows, const int32
 #define ROW_ARGS blocks, rows, n_rows, idx, val, wts, Fp, zrow, ws, D, lam, X, sse, flag, \
                  cyc_gram, cyc_solve, pr, hd, s
   if (hd.idx2) {
-    // tensor ALS (and its Gibbs draws): no weights; the tile form throughout (the strip
-    // form of its Gram runs out of registers)
+    // tensor ALS (and its Gibbs draws): no weights; the tile form throughout (with the
+    // second gathered row the strip form needs more registers and is no faster)
     if (wt) return hipErrorInvalidValue;
     if (pr.init) {
       if (aug)
