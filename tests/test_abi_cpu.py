@@ -77,3 +77,42 @@ def test_create_validation(case, status):
     assert st == status, msg
     assert h.value is None
     assert msg
+
+
+@pytest.mark.parametrize("case", ["users_2_31", "nnz_2_31", "staged_4GiB", "staged_max_ok_shape",
+                                  "negative_tuning"])
+def test_create_size_limits(case):
+    """The shape limits of als_create are checked on the host before any device call: row
+    counts below 2^31, nnz below 2^31, and the staged fixed side (max(M, N) + 1) rows of
+    16 * ceil(D / 16) floats below 4 GiB (32-bit gather offsets)."""
+    from paper_1108_2580_amd import Tuning, lib
+
+    ptr = np.array([0, 2, 3], dtype=np.int64)
+    col = np.array([0, 2, 1], dtype=np.int32)
+    val = np.array([5, 0, 7], dtype=np.uint8)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    h = ctypes.c_void_p(123)
+    M, N, nnz, D, tun = 2, 3, 3, 4, None
+    if case == "users_2_31":
+        M = 1 << 31
+    elif case == "nnz_2_31":
+        nnz = 1 << 31
+    elif case == "staged_4GiB":
+        # D = 128: 512 bytes per staged row; 2^23 - 1 rows plus the zero row reach 4 GiB
+        M, D = (1 << 23) - 1, 128
+    elif case == "staged_max_ok_shape":
+        # 2^23 - 2 rows (plus the zero row) fit; the call then reaches the CSR checks, and a
+        # row_ptr that does not start at 0 stops it there, before any device call
+        M, D = (1 << 23) - 2, 128
+        ptr = np.ones(M + 1, dtype=np.int64)
+    elif case == "negative_tuning":
+        tun = Tuning(-1, 0, 0)
+    st = lib.als_create(ctypes.byref(h), M, N, nnz, p(ptr), p(col), p(val), D, None,
+                        None if tun is None else ctypes.byref(tun))
+    msg = lib.als_last_error(None).decode()
+    assert h.value is None
+    if case == "staged_max_ok_shape":
+        assert st == 2 and "row_ptr[0]" in msg, msg
+    else:
+        assert st == 1, msg
+        assert msg
