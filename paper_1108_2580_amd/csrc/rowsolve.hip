@@ -159,7 +159,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   constexpr int T = C::T, NT = C::NT;
   constexpr int NPAN = DP / 4;
   __shared__ floatx4 s_panel[kRowWaves][T][16];  // one panel's rows, per tile column and lane column
-  __shared__ float s_ud[kRowWaves][NPAN][16];    // per panel: M (10 entries) and y_p (4)
+  // per panel: M as a full 4 x 4 row-major block (zeros above the diagonal), then y_p
+  __shared__ __attribute__((aligned(16))) float s_ud[kRowWaves][NPAN][20];
   __shared__ GroupStage s_stage[kRowWaves];        // gather staging of the row's rating groups
 
   const int wv = threadIdx.x >> 6;
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   const RowTask rt = rows[task];
   const int lane = threadIdx.x & 63, kq = lane >> 4, c = lane & 15;
   floatx4(&panel)[T][16] = s_panel[wv];
-  float(&ud)[NPAN][16] = s_ud[wv];
+  float(&ud)[NPAN][20] = s_ud[wv];
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
 
   // A starts as lambda n_s I on the first D diagonal entries and I on the padding (only
@@ -326,11 +327,6 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       const float m20 = -(u02 * m00 + u12 * m10) * i22, m21 = -(u12 * m11) * i22, m22 = i22;
       const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
       const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
-      // this lane's row of M
-      const float w0 = kq == 0 ? m00 : (kq == 1 ? m10 : (kq == 2 ? m20 : m30));
-      const float w1 = kq == 0 ? 0.f : (kq == 1 ? m11 : (kq == 2 ? m21 : m31));
-      const float w2 = kq <= 1 ? 0.f : (kq == 2 ? m22 : m32);
-      const float w3 = kq == 3 ? m33 : 0.f;
       const int pan = p0 >> 2;
       float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
       if constexpr (!AUG) {
@@ -346,17 +342,22 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
         v2 = m22 * y2 + m32 * y3;
         v3 = m33 * y3;
         if (lane == 0) {
-          ud[pan][10] = y0; ud[pan][11] = y1; ud[pan][12] = y2; ud[pan][13] = y3;
+          ud[pan][16] = y0; ud[pan][17] = y1; ud[pan][18] = y2; ud[pan][19] = y3;
         }
       }
       if (lane == 0) {
-        ud[pan][0] = m00; ud[pan][1] = m10; ud[pan][2] = m11; ud[pan][3] = m20;
-        ud[pan][4] = m21; ud[pan][5] = m22; ud[pan][6] = m30; ud[pan][7] = m31;
-        ud[pan][8] = m32; ud[pan][9] = m33;
+        float4 *mr = reinterpret_cast<float4 *>(ud[pan]);
+        mr[0] = make_float4(m00, 0.f, 0.f, 0.f);
+        mr[1] = make_float4(m10, m11, 0.f, 0.f);
+        mr[2] = make_float4(m20, m21, m22, 0.f);
+        mr[3] = make_float4(m30, m31, m32, m33);
       }
       // (3) panel rows U[p0 + kq][j] = (M A_p)[kq][j] for the later columns j (zero for
       // j <= p0 + 3, which keeps the finished rows and columns out of the update)
       wave_sync();
+      // this lane's row of M (row group kq holds panel row p0 + kq)
+      const float4 wr = reinterpret_cast<const float4 *>(ud[pan])[kq];
+      const float w0 = wr.x, w1 = wr.y, w2 = wr.z, w3 = wr.w;
       float u[T];
 #pragma unroll
       for (int X = 0; X < T; ++X) {
@@ -377,7 +378,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       }
       if constexpr (AUG) {
         // the augmented column's panel entries are y_p = U_gg^{-T} b_p
-        if (c == aug_c) ud[pan][10 + kq] = u[T - 1];
+        if (c == aug_c) ud[pan][16 + kq] = u[T - 1];
       }
       // (4) trailing update on MFMA: A_IJ -= U_p(:, I)^T U_p(:, J). The tile row that the
       // next panel publishes is issued first, so that the next panel's factorisation runs
@@ -402,12 +403,12 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   }
 
   if constexpr (BAYES) {
-    // y += z / sqrt(alpha): the panels keep y_p in ud[p][10 .. 13]
+    // y += z / sqrt(alpha): the panels keep y_p in ud[p][16 .. 19]
     const float *__restrict__ zr = pr.z + (int64_t)rt.row * D;
 #pragma unroll
     for (int d0 = 0; d0 < DP; d0 += 64) {
       const int d = d0 + lane;
-      if (d < D) ud[d >> 2][10 + (d & 3)] += pr.zscale * zr[d];
+      if (d < D) ud[d >> 2][16 + (d & 3)] += pr.zscale * zr[d];
     }
     wave_sync();
   }
@@ -445,13 +446,13 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       const float a0 = lane_value(sr, 16 * g + 0), a1 = lane_value(sr, 16 * g + 4);
       const float a2 = lane_value(sr, 16 * g + 8), a3 = lane_value(sr, 16 * g + 12);
       const int pan = p0 >> 2;
-      const float m00 = ud[pan][0], m10 = ud[pan][1], m11 = ud[pan][2], m20 = ud[pan][3];
-      const float m21 = ud[pan][4], m22 = ud[pan][5], m30 = ud[pan][6], m31 = ud[pan][7];
-      const float m32 = ud[pan][8], m33 = ud[pan][9];
-      const float z0 = ud[pan][10] - m00 * a0;
-      const float z1 = ud[pan][11] - (m10 * a0 + m11 * a1);
-      const float z2 = ud[pan][12] - (m20 * a0 + m21 * a1 + m22 * a2);
-      const float z3 = ud[pan][13] - (m30 * a0 + m31 * a1 + m32 * a2 + m33 * a3);
+      const float m00 = ud[pan][0], m10 = ud[pan][4], m11 = ud[pan][5], m20 = ud[pan][8];
+      const float m21 = ud[pan][9], m22 = ud[pan][10], m30 = ud[pan][12], m31 = ud[pan][13];
+      const float m32 = ud[pan][14], m33 = ud[pan][15];
+      const float z0 = ud[pan][16] - m00 * a0;
+      const float z1 = ud[pan][17] - (m10 * a0 + m11 * a1);
+      const float z2 = ud[pan][18] - (m20 * a0 + m21 * a1 + m22 * a2);
+      const float z3 = ud[pan][19] - (m30 * a0 + m31 * a1 + m32 * a2 + m33 * a3);
       const float x0 = m00 * z0 + m10 * z1 + m20 * z2 + m30 * z3;
       const float x1 = m11 * z1 + m21 * z2 + m31 * z3;
       const float x2 = m22 * z2 + m32 * z3;
