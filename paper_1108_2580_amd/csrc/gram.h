@@ -253,8 +253,13 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float &corner, int cx, int cy) {
   constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
   static_assert(!CORNER || T == 2, "the corner path is for two tiles");
-  static_assert(!STRIP || (T >= 3 && !AUG && !CORNER),
-                "the strip path is for three or more tiles, with the right-hand side in rhs");
+  static_assert(!STRIP || (T >= 3 && !AUG && !CORNER) || (T == 2 && AUG && CORNER),
+                "the strip path is for three or more tiles with the right-hand side in rhs, or "
+                "for the two-tile corner widths");
+  // two-tile strip (with CORNER): the strip operand is feature 16 + (c & 3) of the lane's
+  // rating, which lane c & 3 of the same row group holds in its second block; ds_swizzle in
+  // bit mode (and-mask 0x13: keep lane bits 0, 1 and 4) fetches it without a second load
+  constexpr bool STRIP2 = STRIP && T == 2;
 #pragma unroll
   for (int u0 = 0; u0 < STEPS; u0 += SUB) {
     if (s0 + u0 < steps) {
@@ -268,6 +273,12 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
           if constexpr (!AUG) rhs[X] = fmaf(rw, a[u][X], rhs[X]);
           pi[s0 + u] = fmaf(a[u][X], xo[X], pi[s0 + u]);
         }
+        // the two-tile strip leaves the augmented column out: features 0..15 take their
+        // right-hand side on VALU (16..19 take it in the corner products)
+        if constexpr (STRIP2) rhs[0] = fmaf(rw, a[u][0], rhs[0]);
+        const float sbu = STRIP2 ? __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(
+                                                                   __builtin_bit_cast(int, a[u][T - 1]), 0x13))
+                                 : sb[u];
 #pragma unroll
         for (int I = 0; I < T; ++I) {
 #pragma unroll
@@ -275,7 +286,7 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
             if (CORNER && I == T - 1) continue;
             if (STRIP && J == T - 1)
               acc[tidx<T>(I, J)] =
-                  __builtin_amdgcn_mfma_f32_4x4x1f32(wa[I], sb[u], acc[tidx<T>(I, J)], 0, 0, 0);
+                  __builtin_amdgcn_mfma_f32_4x4x1f32(wa[I], sbu, acc[tidx<T>(I, J)], 0, 0, 0);
             else
               acc[tidx<T>(I, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[I], a[u][J],
                                                                         acc[tidx<T>(I, J)], 0, 0, 0);
@@ -367,8 +378,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
           float a[STEPS][T];
           float sb[STEPS], r[STEPS], w[STEPS];
           gather_block<DP, STEPS, AUG, WT, TS>(a, sb, r, w, st, 0, s0, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT, CORNER>(acc, rhs, xo, pi, a, sb, r, w, s0, steps, corner,
-                                                cx, cy);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a, sb, r, w, s0, steps,
+                                                       corner, cx, cy);
         }
       }
       group_residuals(pi, st, 0, g, n, sse);

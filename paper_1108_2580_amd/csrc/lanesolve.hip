@@ -45,8 +45,10 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   constexpr int NES = ne_floats(LD);
   static_assert(!AUG || (LD < DP && LD > 16 * (T - 1) && LD % 4 == 0),
                 "the augmented column is feature LD of the last tile");
-  // the last diagonal tile holds features 16 .. LD only: its 15 products go to VALU
+  // the last diagonal tile holds features 16 .. LD only: its 15 products go to VALU, and
+  // the tile above it, which holds four used features, goes to 4 x 4 strips (STRIP)
   constexpr bool CORNER = AUG && T == 2 && LD == 20;
+  constexpr bool STRIP = CORNER;
   __shared__ GroupStage s_stage;
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
@@ -81,11 +83,11 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   }
   const int cx = (kq * 16 + cp) * 4, cy = (kq * 16 + cq) * 4;
   float corner = 0.f;
-  gram_accumulate<DP, AUG, WT, TS, CORNER>(acc, rhs, xo, sse, idx + it.start, val + it.start, wp,
-                                           tp, it.len, Fp, hd.Tp, zrow,
-                                           AUG ? LD - 16 * (T - 1) : -1, s_stage, g0, corner, cx,
-                                           cy);
-  if constexpr (!AUG) {
+  gram_accumulate<DP, AUG, WT, TS, CORNER, STRIP>(acc, rhs, xo, sse, idx + it.start,
+                                                  val + it.start, wp, tp, it.len, Fp, hd.Tp, zrow,
+                                                  AUG ? LD - 16 * (T - 1) : -1, s_stage, g0,
+                                                  corner, cx, cy);
+  if constexpr (!AUG || STRIP) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
       rhs[X] += __shfl_xor(rhs[X], 16);
@@ -104,11 +106,25 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
       else if (a < LD) out[NTRI + a] = corner;  // (a, LD): the right-hand side of feature a
     }
   }
+  if constexpr (STRIP) {
+    // the strip of tile (0, 1), summed over the four rating groups: lane c holds
+    // G[4 (c >> 2) + r][16 + (c & 3)] in element r; the right-hand side of features 0..15
+    // is rhs[0], summed above
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = acc[tidx<T>(0, 1)][r];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (kq == 0) out[tri<LD>(4 * (c >> 2) + r, 16 + (c & 3))] = v;
+    }
+    if (kq == 0) out[NTRI + c] = rhs[0];
+  }
 #pragma unroll
   for (int I = 0; I < T; ++I) {
 #pragma unroll
     for (int J = I; J < T; ++J) {
       if (CORNER && I == T - 1) continue;
+      if (STRIP && J == T - 1) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int a = 16 * I + 4 * kq + r, b = 16 * J + c;
