@@ -58,6 +58,12 @@ __device__ __forceinline__ float sum16x4(float s0, float s1, float s2, float s3)
   return u;
 }
 
+// Value of lane (kq, c & 3), i.e. lane 16 kq + (c & 3): ds_swizzle in bit mode with and-mask
+// 0x13 keeps lane bits 0, 1 and 4 within each 32-lane half.
+__device__ __forceinline__ float from_row_lane03(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x13));
+}
+
 // Value of lane l (wave-uniform) broadcast to the wave through a scalar register.
 __device__ __forceinline__ float lane_value(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
@@ -257,8 +263,8 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                 "the strip path is for three or more tiles with the right-hand side in rhs, or "
                 "for the two-tile corner widths");
   // two-tile strip (with CORNER): the strip operand is feature 16 + (c & 3) of the lane's
-  // rating, which lane c & 3 of the same row group holds in its second block; ds_swizzle in
-  // bit mode (and-mask 0x13: keep lane bits 0, 1 and 4) fetches it without a second load
+  // rating, which lane c & 3 of the same row group holds in its second block; a swizzle
+  // fetches it without a second load
   constexpr bool STRIP2 = STRIP && T == 2;
 #pragma unroll
   for (int u0 = 0; u0 < STEPS; u0 += SUB) {
@@ -276,9 +282,7 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
         // the two-tile strip leaves the augmented column out: features 0..15 take their
         // right-hand side on VALU (16..19 take it in the corner products)
         if constexpr (STRIP2) rhs[0] = fmaf(rw, a[u][0], rhs[0]);
-        const float sbu = STRIP2 ? __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(
-                                                                   __builtin_bit_cast(int, a[u][T - 1]), 0x13))
-                                 : sb[u];
+        const float sbu = STRIP2 ? from_row_lane03(a[u][T - 1]) : sb[u];
 #pragma unroll
         for (int I = 0; I < T; ++I) {
 #pragma unroll
