@@ -240,25 +240,30 @@ __device__ __forceinline__ void gather_block(float (&a)[STEPS][DP / 16], float (
 // operand carries c f, so the tiles accumulate sum c f f^T (and, in the augmented
 // column, sum c r f); predictions use the unweighted rows.
 // CORNER (two tiles, features 16..20 used in the second: the one-lane widths D = 17..20,
-// always with STRIP): the last diagonal tile would spend a 16x16 MFMA on its 4 x 4 block
-// of used features, so that block takes one v_mfma_f32_4x4x1f32 of the strip operand with
-// itself into the tile's accumulator (each rating's four blocks agree; the caller keeps
-// the first), and the right-hand side of features 16..19 accumulates in corner on VALU.
+// always with STRIP): the last diagonal tile would spend a 16x16 MFMA on 15 useful
+// products, so it is skipped. With CMFMA its 4 x 4 block of used features takes one
+// v_mfma_f32_4x4x1f32 of the strip operand with itself into the tile's (otherwise unused)
+// accumulator (each rating's four blocks agree; the caller keeps the first), and the
+// right-hand side of features 16..19 accumulates in corner on VALU. Without CMFMA (tensor
+// ALS, whose steps this extra MFMA slows) each lane c < 15 of a row group accumulates one
+// product f[16 + p] f[16 + q] of the group's rating, fetching the two values across the
+// group's lanes with ds_bpermute (byte addresses cx, cy) and adding them with one FMA.
 // STRIP (only features 16 (T - 1) .. 16 (T - 1) + 3 used in the last tile): the tiles
 // (I, T - 1) of the last column would spend a 16x16 MFMA each on four useful columns, so
 // each takes one v_mfma_f32_4x4x1f32 instead. Its 16 blocks are b = 4 kq + cb: block b
 // multiplies rows 16 I + 4 cb .. + 3 (the lane's own operand) by the four used features
 // of the last tile (sb), for rating kq alone; acc[tidx(I, T - 1)] then holds these
 // per-rating strips until strip_finish sums and rearranges them.
-template <int DP, int STEPS, bool AUG, bool WT, bool CORNER = false, bool STRIP = false>
+template <int DP, int STEPS, bool AUG, bool WT, bool CORNER = false, bool STRIP = false,
+          bool CMFMA = false>
 __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                           float (&rhs)[DP / 16], const float (&xo)[DP / 16],
                                           float (&pi)[16], const float (&a)[STEPS][DP / 16],
                                           const float (&sb)[STEPS], const float (&r)[STEPS],
                                           const float (&wt)[STEPS], int s0, int steps,
-                                          float &corner) {
+                                          float &corner, int cx, int cy) {
   constexpr int T = DP / 16, SUB = STEPS < 4 ? STEPS : 4;
-  static_assert(!CORNER || (T == 2 && STRIP), "the corner path is for two tiles, with the strip");
+  static_assert(!CORNER || T == 2, "the corner path is for two tiles");
   static_assert(!STRIP || (T >= 3 && !AUG && !CORNER) || (T == 2 && AUG && CORNER),
                 "the strip path is for three or more tiles with the right-hand side in rhs, or "
                 "for the two-tile corner widths");
@@ -296,14 +301,17 @@ __device__ __forceinline__ void mma_block(floatx4 (&acc)[RowCfg<DP>::NT],
                                                                         acc[tidx<T>(I, J)], 0, 0, 0);
           }
         }
-        if constexpr (CORNER) {
-          // the corner's four used features times themselves, in the otherwise unused
-          // accumulator of the last diagonal tile: block 4 kq + cb holds f[16 + i] f[16 + j]
-          // of rating kq (the four blocks of a rating agree); their right-hand side on VALU
+        if constexpr (CORNER && CMFMA) {
           const float ws = WT ? wt[u] * sbu : sbu;
           acc[tidx<T>(T - 1, T - 1)] =
               __builtin_amdgcn_mfma_f32_4x4x1f32(ws, sbu, acc[tidx<T>(T - 1, T - 1)], 0, 0, 0);
           corner = fmaf(rw, sbu, corner);
+        } else if constexpr (CORNER) {
+          const float xv = __builtin_bit_cast(
+              float, __builtin_amdgcn_ds_bpermute(cx, __builtin_bit_cast(int, wa[T - 1])));
+          const float yv = __builtin_bit_cast(
+              float, __builtin_amdgcn_ds_bpermute(cy, __builtin_bit_cast(int, a[u][T - 1])));
+          corner = fmaf(xv, yv, corner);
         }
       }
     }
@@ -349,7 +357,8 @@ __device__ __forceinline__ void group_residuals(const float (&pi)[16], GroupStag
 //    one, so that its latency hides behind them. The blocks of the last group that
 //    lie past the item's end are still gathered (from the zero row) but not multiplied.
 // tp, Tp (tensor ALS, TS): the item's second indices and the second staged table.
-// corner: the right-hand side of features 16..19 (CORNER), else unused.
+// corner, cx, cy: the corner products of mma_block (CORNER; with CMFMA, for all but TS,
+// only the right-hand side of features 16..19), else unused.
 // STRIP: the last tile column in strip form (mma_block); the caller finishes it with
 // strip_finish.
 template <int DP, bool AUG, bool WT, bool TS = false, bool CORNER = false, bool STRIP = false>
@@ -363,7 +372,7 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
                                                 const float *__restrict__ Fp,
                                                 const float *__restrict__ Tp, int zrow,
                                                 int aug_c, GroupStage &st, GroupLanes gv,
-                                                float &corner) {
+                                                float &corner, int cx, int cy) {
   using C = RowCfg<DP>;
   constexpr int T = C::T, STEPS = C::STEPS, NB = 16 / STEPS;
   const int lane = threadIdx.x & 63;
@@ -384,8 +393,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
           float a[STEPS][T];
           float sb[STEPS], r[STEPS], w[STEPS];
           gather_block<DP, STEPS, AUG, WT, TS>(a, sb, r, w, st, 0, s0, Fp, Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a, sb, r, w, s0, steps,
-                                                       corner);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP, CORNER && !TS>(acc, rhs, xo, pi, a, sb, r, w, s0, steps,
+                                                       corner, cx, cy);
         }
       }
       group_residuals(pi, st, 0, g, n, sse);
@@ -414,8 +423,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
           if constexpr (b + 1 < NB)
             gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a1, b1, r1, w1, st, buf, s0 + STEPS, Fp,
                                                         Tp, aug_lane);
-          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a0, b0, r0, w0, s0,
-                                                       steps, corner);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP, CORNER && !TS>(acc, rhs, xo, pi, a0, b0, r0, w0, s0,
+                                                       steps, corner, cx, cy);
         } else {
           if constexpr (b + 1 < NB) {
             gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a0, b0, r0, w0, st, buf, s0 + STEPS, Fp,
@@ -427,8 +436,8 @@ __device__ __forceinline__ void gram_accumulate(floatx4 (&acc)[RowCfg<DP>::NT],
             gather_block<DP, STEPS, AUG, WT, TS, STRIP>(a0, b0, r0, w0, st, buf ^ 1, 0, Fp, Tp,
                                                         aug_lane);
           }
-          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP>(acc, rhs, xo, pi, a1, b1, r1, w1, s0,
-                                                       steps, corner);
+          mma_block<DP, STEPS, AUG, WT, CORNER, STRIP, CORNER && !TS>(acc, rhs, xo, pi, a1, b1, r1, w1, s0,
+                                                       steps, corner, cx, cy);
         }
       };
       unroll_blocks<0, NB>(block);

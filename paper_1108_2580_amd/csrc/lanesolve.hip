@@ -69,11 +69,25 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   const int32_t *__restrict__ tp = TS ? hd.idx2 + it.start : nullptr;
   const GroupLanes g0 =
       first_group<WT, TS>(idx + it.start, val + it.start, wp, tp, it.len, zrow);
-  float corner = 0.f;  // CORNER: the right-hand side of features 16..19
+  // CORNER without the corner MFMA (TS): lane c < 15 of a row group owns the product
+  // (cp, cq), cp <= cq < 5, of the features 16 + cp and 16 + cq (16 + 4 = LD is the
+  // augmented column)
+  int cp = 0, cq = 0;
+  if constexpr (CORNER) {
+    int rem = c;
+    while (cp < 4 && rem >= 5 - cp) {
+      rem -= 5 - cp;
+      ++cp;
+    }
+    cq = c < 15 ? cp + rem : 0;
+    if (c >= 15) cp = 0;
+  }
+  const int cx = (kq * 16 + cp) * 4, cy = (kq * 16 + cq) * 4;
+  float corner = 0.f;
   gram_accumulate<DP, AUG, WT, TS, CORNER, STRIP>(acc, rhs, xo, sse, idx + it.start,
                                                   val + it.start, wp, tp, it.len, Fp, hd.Tp, zrow,
                                                   AUG ? LD - 16 * (T - 1) : -1, s_stage, g0,
-                                                  corner);
+                                                  corner, cx, cy);
   if constexpr (!AUG || STRIP) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
@@ -84,7 +98,7 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
   float *__restrict__ out = ((int64_t)blockIdx.x < n_chunk_items ? ws : ne) + it.slot * NES;
-  if constexpr (CORNER) {
+  if constexpr (CORNER && !TS) {
     // the corner block (tile (1, 1) accumulator) and the right-hand side of features
     // 16..19, summed over the four rating groups: lane c < 4 holds G[16 + r][16 + c] in
     // element r and b[16 + c]
@@ -98,6 +112,14 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
       if (kq == 0 && c < 4 && r <= c) out[tri<LD>(16 + r, 16 + c)] = v;
     }
     if (kq == 0 && c < 4) out[NTRI + 16 + c] = corner;
+  } else if constexpr (CORNER) {
+    corner += __shfl_xor(corner, 16);
+    corner += __shfl_xor(corner, 32);
+    if (kq == 0 && c < 15) {
+      const int a = 16 + cp, b = 16 + cq;
+      if (b < LD) out[tri<LD>(a, b)] = corner;
+      else if (a < LD) out[NTRI + a] = corner;  // (a, LD): the right-hand side of feature a
+    }
   }
   if constexpr (STRIP) {
     // the strip of tile (0, 1), summed over the four rating groups: lane c holds

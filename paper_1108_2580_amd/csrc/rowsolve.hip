@@ -105,7 +105,7 @@ __global__ __launch_bounds__(64) void k_gram_chunks(const WorkItem *__restrict__
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
   gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
       acc, rhs, xo, sse, idx + it.start, val + it.start, wp, tp, it.len, Fp, hd.Tp, zrow,
-      STRIP ? -1 : aug_c, s_stage, g0, no_corner);
+      STRIP ? -1 : aug_c, s_stage, g0, no_corner, 0, 0);
   if constexpr (STRIP) strip_finish<DP>(acc, rhs, aug_c);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     float no_corner = 0.f;
     gram_accumulate<DP, AUG && !STRIP, WT, TS, false, STRIP>(
         acc, rhs, xo, sse, idx + rt.start, val + rt.start, wp, tp, rt.deg, Fp, hd.Tp, zrow,
-        STRIP ? -1 : aug_c, s_stage[wv], g0, no_corner);
+        STRIP ? -1 : aug_c, s_stage[wv], g0, no_corner, 0, 0);
     if constexpr (STRIP) strip_finish<DP>(acc, rhs, aug_c);
     if constexpr (!AUG) {
 #pragma unroll
