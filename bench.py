@@ -40,7 +40,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=None, choices=[1, 2, 3, 4, 5],
+                    help="one workload only (default: the D = 20 headline on the full-scale "
+                         "matrix, then the same matrix at D = 100 as the d100 leg)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -179,26 +181,40 @@ def cpu_baseline(r, side_fixed, target_s, weights=None, gibbs=False, tensor=None
         dt = time.perf_counter() - t0
         return int(deg[sel].sum()), k, dt
 
-    cpu_model = "unknown"
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu_model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
     n0, k0, t0 = run(max(1, r.nnz // 500))
     rate0 = n0 / max(t0, 1e-9)
     target = min(r.nnz, int(rate0 * target_s))
     n1, k1, t1 = run(target)
     return dict(value=n1 / t1, unit="ratings/s", cores=threads, kind="oracle",
-                cpu_model=cpu_model,
+                cpu_model=host_cpu(), build=" ".join(["gcc", *oracle.CFLAGS]),
+                schedule="rows in descending degree order, dynamic",
                 sample=(f"user half-sweep of {r.name}"
                         f"{' (weighted)' if w is not None else ' (Gibbs draws)' if gibbs else ''}"
                         f"{' (tensor user mode)' if tensor is not None else ''}"
                         f"{' (BPTF user draws)' if tensor is not None and gibbs else ''}: "
                         f"{k1} of {rows.size} rows (seeded random), "
                         f"{n1} ratings, D={r.D}, fp64, {t1:.1f} s"))
+
+
+def host_cpu():
+    """The host CPU as lscpu names it (model name, with family / model / stepping when the
+    name alone is generic)."""
+    import subprocess
+
+    fields = {}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            if ":" in line:
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    name = fields.get("Model name", "unknown")
+    ident = ", ".join(f"{k.lower()} {fields[k]}" for k in ("CPU family", "Model", "Stepping")
+                      if k in fields)
+    sockets = fields.get("Socket(s)")
+    return f"{name} ({ident}{', ' + sockets + ' socket(s)' if sockets else ''})"
 
 
 def one_thread_scale():
@@ -222,7 +238,7 @@ def one_thread_scale():
                         f"D={m.D}), fp64, one thread, {dt:.1f} s"))
 
 
-def heldout_leg(args, r, als, U, V, workload_name, reps=20):
+def heldout_leg(args, k, r, als, U, V, workload_name, reps=20):
     """Held-out predictions r_hat = u . v on a seeded sample of the stored positions (the
     degree distributions of both sides), timed over back-to-back launches of the predict
     kernel; plus the validation RMSE of the same pairs through the registered-set path."""
@@ -232,7 +248,7 @@ def heldout_leg(args, r, als, U, V, workload_name, reps=20):
 
     n = r.nnz // args.heldout_share
     hu, hi, hr = workload.stored_pairs(r.row_ptr, r.col, r.val, n,
-                                       workload.holdout_seed(args.config))
+                                       workload.holdout_seed(k))
     dev = U.device
     du = torch.from_numpy(hu).to(dev)
     di = torch.from_numpy(hi).to(dev)
@@ -369,24 +385,16 @@ class BPTFSteps:
                                     self.z[mode][k])
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              f"(the half-sweep would shard by rows with an all-gather of the solved side).",
-              file=sys.stderr)
-        sys.exit(2)
+def run_workload(args, k):
+    """Warm-up and timed steps of workload k; returns the result record."""
     import numpy as np
     import torch
 
-    if args.copy_calibration:
-        copy_calibration()
-        return
     import workload
     from paper_1108_2580_amd import ALS
 
     t_gen = time.perf_counter()
-    r = workload.make_config(args.config)
+    r = workload.make_config(k)
     U0, V0 = workload.init_factors(r.M, r.N, r.D, r.init_seed)
     log(f"generated {r.name}: nnz={r.nnz} in {time.perf_counter() - t_gen:.1f} s")
     dev = torch.device("cuda:0")
@@ -394,7 +402,7 @@ def main():
     als = ALS(r.M, r.N, r.row_ptr, r.col, r.val, r.D)
     weights = None
     if args.weighted:
-        weights = workload.rating_weights(r.nnz, workload.weight_seed(args.config))
+        weights = workload.rating_weights(r.nnz, workload.weight_seed(k))
         als.set_weights(weights)
     log(f"als_create (validation, upload, device CSC, schedules): "
         f"{time.perf_counter() - t_c:.1f} s; users {als.plan_stats('users')} "
@@ -408,7 +416,7 @@ def main():
     if args.tensor or args.bptf:
         t_b = time.perf_counter()
         nb = workload.N_TIME_BINS
-        bins = workload.time_bins(r.row_ptr, nb, workload.time_seed(args.config))
+        bins = workload.time_bins(r.row_ptr, nb, workload.time_seed(k))
         als.set_time_bins(nb, bins)
         rng = np.random.default_rng(r.init_seed + 99)
         T = torch.from_numpy((1.0 + 0.1 * rng.standard_normal((nb, r.D))).astype(np.float32)).to(dev)
@@ -456,9 +464,7 @@ def main():
     prof = als.profile()
     als.set_profiling(False)
     elapsed = t1 - t0
-    # (the time chain's draw runs as two passes of half the bins each, so the entering-state
-    # figure of its last pass covers the odd bins only)
-    rmse_in = None if args.bptf else als.rmse_in()
+    rmse_in = als.rmse_in()
     rmse = als.tensor_rmse(U, V, T) if (args.tensor or args.bptf) else als.rmse(U, V)
     gram_share = None
     if r.D > 20 and not (args.tensor or args.bptf):
@@ -504,17 +510,23 @@ def main():
                                 + rows_with * (8 + 4 * D))
         achieved = alg / (k_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS, kernel="k_gram_ne")
+                    frac=achieved / HBM_PEAK_GBS, kernel="k_gram_ne",
+                    whole_step_frac=alg / elapsed / 1e9 / HBM_PEAK_GBS)
     else:
-        # fused row kernel + chunk kernel of split rows: SYRK-convention Gram flops, the
-        # right-hand side and residual dot per rating, Cholesky and two solves per row
+        # fused row kernel + chunk kernel of split rows, priced on the Gram build alone: the
+        # SYRK-convention Gram flops D (D + 1) and the right-hand side 2 D per rating (plus
+        # the weight or the second factor's product). The residual dot and the Cholesky
+        # with its two solves run in the same kernels but are not counted here; the
+        # factorisation's own flops are reported beside it.
         k_ms = prof["solve"][0] + prof["gather"][0]
         k_n = prof["solve"][1]
-        alg = halves * r.nnz * (D * (D + 1) + 4 * D + wflops) + \
-            args.steps * rows_with * (D ** 3 / 3.0 + 2.0 * D * D)
+        alg = halves * r.nnz * (D * (D + 1) + 2 * D + wflops)
         achieved = alg / (k_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=achieved, peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s",
-                    frac=achieved / MFMA_F32_PEAK_TFS, kernel="k_rows+k_gram_chunks")
+                    frac=achieved / MFMA_F32_PEAK_TFS, kernel="k_rows+k_gram_chunks",
+                    flops="SYRK Gram + right-hand side per rating",
+                    whole_step_frac=alg / elapsed / 1e12 / MFMA_F32_PEAK_TFS,
+                    chol_flops_per_step=rows_with * (D ** 3 / 3.0 + 2.0 * D * D))
     roof.update(launches=k_n, avg_launch_ms=k_ms / max(k_n, 1), alg_per_launch=alg / max(k_n, 1),
                 traffic=measured_traffic(workload_name, roof["kernel"]), dominant_phase=dominant)
     gram_phase = None
@@ -542,7 +554,7 @@ def main():
         chol_ms = (1.0 - gram_share) * prof["solve"][0] / args.steps
     else:
         chol_ms = None
-    heldout = (heldout_leg(args, r, als, U, V, workload_name)
+    heldout = (heldout_leg(args, k, r, als, U, V, workload_name)
                if args.heldout_share > 0 and not tensor_like else None)
 
     cpu = None
@@ -599,8 +611,31 @@ def main():
         "rmse_entering_last_half_sweep": rmse_in,
         "heldout": heldout,
     }
-    print(json.dumps(out), flush=True)
     als.close()
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the half-sweep would shard by rows with an all-gather of the solved side).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    special = args.weighted or args.gibbs or args.tensor or args.bptf
+    out = run_workload(args, args.config or 3)
+    if args.config is None and not special:
+        # the headline's second width: the same matrix at D = 100, on the fp32 matrix cores
+        log("d100 leg: the same matrix at D = 100")
+        leg = run_workload(args, 4)
+        out["d100"] = {key: leg[key] for key in (
+            "value", "unit", "ms_per_step", "config", "roofline", "gram_phase",
+            "chol_ms_per_step", "per_side", "phases_ms_per_step", "cpu_baseline", "rmse",
+            "rmse_entering_last_half_sweep", "heldout")}
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

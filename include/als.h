@@ -1,12 +1,12 @@
 /*
  * als.h -- C ABI of the MI355X (gfx950) alternating-least-squares half-sweep.
  *
- * The method (paper Sec. 2.2, "ALS and BPTF"): the observed ratings form a
- * sparse M x N matrix A (users x items); A ~= U V with U (M x D) and V
- * (D x N). Starting from an initial guess, each iteration fixes U and solves
- * V by least squares, then fixes V and solves U the same way. A prediction is
- * the dot product of the user and item vectors. One such least-squares pass
- * over one side is a "half-sweep":
+ * The method (paper Sec. 2.2, "ALS and BPTF"): a sparse M x N matrix A of
+ * observed ratings (users x items) is modelled as U V, with U (M x D) and V
+ * (D x N). ALS alternates: with U held, every item column of V is a
+ * least-squares fit; with V held, every user row of U is. A rating is
+ * predicted by the inner product of its user's and its item's vectors. One
+ * least-squares pass over one side is a "half-sweep":
  *
  *   for every row s of the solved side with n_s = |Omega_s| > 0 ratings,
  *     x_s = (sum_{j in Omega_s} f_j f_j^T + lambda * n_s * I)^{-1}
@@ -73,7 +73,9 @@ typedef struct {
 } als_tuning;
 
 /*
- * Create a context for one rating matrix and one factor width D.
+ * Create a context for one rating matrix and one factor width D: the observed ratings
+ * of paper Sec. 2.2 (matrix A, users x items; every stored position is observed, Sec. 3
+ * rates on 0..100 with 0 a valid rating) and the width D of the factors U and V.
  *   n_users, n_items  matrix shape (M, N); each >= 1, and (max(M, N) + 1) * DP * 4
  *                     < 2^32 bytes with DP = 16 * ceil(D / 16) (the staged fixed side
  *                     is addressed with 32-bit offsets): up to 8.4M rows per side at
@@ -126,15 +128,18 @@ als_status als_half_sweep(als_ctx *ctx, als_side side, const float *fixed_factor
 als_status als_last_rmse_in(als_ctx *ctx, double *rmse_in);
 
 /*
- * Training RMSE of (U, V): sqrt(sum over stored ratings of (r - u_u . v_i)^2 / nnz).
+ * Training RMSE of (U, V), the quality measure of paper Sec. 4.1 over the stored ratings,
+ * with the inner-product prediction of Sec. 2.2:
+ * sqrt(sum over stored ratings of (r - u_u . v_i)^2 / nnz).
  * U, V: device fp32 [n_users x D], [n_items x D]. Synchronises the stream.
  * An empty matrix gives 0.
  */
 als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
 
-/* Rows flagged (not SPD / non-finite) by the last half-sweep; synchronises the
- * stream. Returns -1 for a NULL context. */
-int64_t als_flagged_rows(als_ctx *ctx);
+/* Rows flagged (not SPD / non-finite, so the Cholesky of the per-update inversion of
+ * Sec. 4.1 failed) by the last half-sweep; synchronises the stream. Returns -1 for a NULL
+ * context or a failed synchronisation. */
+int64_t als_flagged_rows(const als_ctx *ctx);
 
 /*
  * Copy the device-built CSC (rows ascending within each column) to host
@@ -226,8 +231,8 @@ als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
 als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
 
 /*
- * Bayesian factorisation (BPTF, paper Sec. 2.2: the least-squares step plus sampling from
- * the hyperpriors of U and V), as the published BPMF / BPTF Gibbs sampler: ratings are
+ * Bayesian factorisation (BPTF, paper Sec. 2.2, which pairs the least-squares update with
+ * draws of the factor priors' parameters), as the published BPMF / BPTF Gibbs sampler: ratings are
  * Gaussian with precision alpha around u . v; each row of a side has the prior
  * N(mu, Lambda^{-1}); (mu, Lambda) has the Normal-Wishart hyperprior NW(mu0, beta0, W0, nu0).
  * One Gibbs step for a side: als_sample_hyper draws (mu, Lambda) given the side's rows,
@@ -378,14 +383,18 @@ als_status als_tensor_gibbs_half_sweep(als_ctx *ctx, als_mode mode, float *U, fl
 als_status als_tensor_sample_alpha(als_ctx *ctx, const float *U, const float *V, const float *T,
                                    double w0, double chi2, double *alpha_out);
 
-/* Release the context and every device buffer it owns (after synchronising its stream);
- * NULL is ignored. Caller-owned factor buffers are untouched. */
+/* Release the context of als_create (the rating matrix of paper Sec. 2.2, its device
+ * layouts, schedules and workspace) after synchronising its stream; NULL is ignored.
+ * Caller-owned factor buffers are untouched. */
 void als_destroy(als_ctx *ctx);
 
+/* Text of a status code. Error reporting of this interface; no passage of the paper
+ * defines it. The string is static. */
 const char *als_status_str(als_status s);
 
 /* Message of the last failing call on ctx (or of the last failed
- * als_create when ctx is NULL); valid until the next call on ctx. */
+ * als_create when ctx is NULL); valid until the next call on ctx. Error reporting of
+ * this interface; no passage of the paper defines it. */
 const char *als_last_error(const als_ctx *ctx);
 
 #ifdef __cplusplus

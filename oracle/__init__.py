@@ -37,9 +37,15 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "als_oracle.c")
 
 
+# Optimised for any x86-64 host with AVX2 and FMA (the library is built once and runs on
+# other hosts), with floating-point contraction off: every product and sum is rounded as
+# written, so the results do not depend on the instruction set or the optimisation level.
+CFLAGS = ["-O3", "-march=x86-64-v3", "-ffp-contract=off", "-fopenmp"]
+
+
 def build(verbose: bool = False) -> str:
-    """Compile als_oracle.c into liboracle.so (gcc -O2, OpenMP, strict IEEE fp64)."""
-    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    """Compile als_oracle.c into liboracle.so (gcc, OpenMP, strict IEEE fp64)."""
+    cmd = ["gcc", *CFLAGS, "-shared", "-fPIC", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.check_call(cmd)
@@ -177,8 +183,10 @@ def half_sweep(ptr, idx, val, F, lam, X_prev, threads=0, w=None):
     D = F.shape[1]
     assert X.shape == (n_rows, D)
     flags = np.empty(n_rows, dtype=np.int8)
-    _load().orc_half_sweep(n_rows, _p(ptr), _p(idx), _p(val), _p(w), D, _p(F), float(lam), _p(X),
-                           _p(flags), int(threads))
+    nflag = _load().orc_half_sweep(n_rows, _p(ptr), _p(idx), _p(val), _p(w), D, _p(F),
+                                   float(lam), _p(X), _p(flags), int(threads))
+    if nflag < 0:
+        raise MemoryError("oracle half-sweep: schedule allocation failed")
     return X, flags
 
 
@@ -494,59 +502,3 @@ def alpha_posterior(sse, n, w0, nu0):
     W(w0, nu0) given the n residuals with sum of squares sse: W(w*, nu*) with
     1 / w* = 1 / w0 + sse and nu* = nu0 + n. A draw is w* times a chi-square(nu*) variate."""
     return 1.0 / (1.0 / float(w0) + float(sse)), float(nu0) + float(n)
-
-
-class BPTFChain:
-    """Free-running fp64 BPTF Gibbs sampler over (user, item, time bin) ratings. One
-    iteration, all variates supplied by the caller:
-      alpha from its posterior given the current U, V, T;
-      (mu, Lambda) of the items from V, of the users from U, and of the time chain from T;
-      the item rows, then the user rows, then the time bins (even, then odd)."""
-
-    def __init__(self, M, N, n_bins, row_ptr, col, bins, val, U0, V0, T0, threads=0):
-        self.t = TensorTrajectory(M, N, n_bins, row_ptr, col, bins, val, U0, V0, T0, 0.0,
-                                  threads)
-        self.threads = threads
-
-    @property
-    def U(self):
-        return self.t.U
-
-    @property
-    def V(self):
-        return self.t.V
-
-    @property
-    def T(self):
-        return self.t.T
-
-    def sse(self):
-        p, i1, i2, v = self.t.by_user
-        return tensor_sse(p, i1, i2, v, self.U, self.V, self.T, self.threads)
-
-    def iterate(self, alpha_prior, priors, variates):
-        """alpha_prior = (w0, nu0); priors = {"items"|"users"|"time": (mu0, beta0, W0inv,
-        nu0)}; variates = {"alpha_chi2": x, "hyper": {side: (chi2, offd, zmu)}, "z": {side:
-        array}}. Returns (alpha, {side: (mu, Lambda)})."""
-        t = self.t
-        w_s, _ = alpha_posterior(self.sse(), t.nnz, *alpha_prior)
-        alpha = w_s * float(variates["alpha_chi2"])
-        hyper = {}
-        for side, X in (("items", t.V), ("users", t.U), ("time", t.T)):
-            mu0, beta0, W0inv, nu0 = priors[side]
-            post = (time_posterior if side == "time" else nw_posterior)(X, mu0, beta0, W0inv, nu0)
-            drawn = nw_sample(post[0], post[1], post[2], *variates["hyper"][side])
-            if drawn is None:
-                raise FloatingPointError(f"Normal-Wishart draw failed for {side}")
-            hyper[side] = drawn
-        p, i1, i2, v = t.by_item
-        t.V, _ = tensor_gibbs_rows(p, i1, i2, v, t.U, t.T, alpha, hyper["items"][1],
-                                   hyper["items"][0], variates["z"]["items"], t.V, self.threads)
-        p, i1, i2, v = t.by_user
-        t.U, _ = tensor_gibbs_rows(p, i1, i2, v, t.V, t.T, alpha, hyper["users"][1],
-                                   hyper["users"][0], variates["z"]["users"], t.U, self.threads)
-        p, i1, i2, v = t.by_bin
-        for parity in (0, 1):
-            t.T, _ = time_rows(p, i1, i2, v, t.U, t.V, alpha, hyper["time"][1], hyper["time"][0],
-                               variates["z"]["time"], parity, t.T, self.threads)
-        return alpha, hyper

@@ -29,8 +29,8 @@
  * pairs, r_hat = u_u . v_i, and the validation RMSE is
  * sqrt(sum over the pairs of (r - r_hat)^2 / number of pairs).
  *
- * Bayesian factorisation (BPTF, named in Sec. 2.2 as least squares plus sampling from the
- * hyperpriors of U and V; the published BPMF/BPTF Gibbs sampler): ratings are Gaussian
+ * Bayesian factorisation (BPTF, Sec. 2.2, which pairs the least-squares update with draws
+ * of the factor priors' parameters; the published BPMF/BPTF Gibbs sampler): ratings are Gaussian
  * with precision alpha around u . v, each row of a side has the prior N(mu, Lambda^{-1}),
  * and (mu, Lambda) have a Normal-Wishart hyperprior. One Gibbs step for a side draws
  *   - the hyperparameters from their Normal-Wishart posterior given the side's rows
@@ -158,10 +158,32 @@ static int solve_one(int32_t D, int64_t n, const int32_t *idx, const double *val
  * (n_fixed x D), X[s,:] <- the regularised least-squares solution. Rows with
  * no ratings and flagged rows keep their previous X. flags[s] (nullable)
  * receives 0 solved, 1 flagged, 2 empty. Returns the number of flagged rows. */
+/* Row order of a half-sweep's schedule: descending degree, ties by row index, so that
+ * the largest rows start first and do not form the tail. Rows are independent, so the
+ * order changes no result. Returns a malloc'ed array of n_rows indices, or NULL. */
+typedef struct { int64_t deg, row; } deg_row;
+static int by_degree_desc(const void *pa, const void *pb) {
+  const deg_row *a = (const deg_row *)pa, *b = (const deg_row *)pb;
+  if (a->deg != b->deg) return a->deg > b->deg ? -1 : 1;
+  return a->row < b->row ? -1 : (a->row > b->row);
+}
+static int64_t *degree_order(int64_t n_rows, const int64_t *ptr) {
+  deg_row *key = (deg_row *)malloc(sizeof(deg_row) * (n_rows > 0 ? n_rows : 1));
+  int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (n_rows > 0 ? n_rows : 1));
+  if (!key || !order) { free(key); free(order); return NULL; }
+  for (int64_t s = 0; s < n_rows; ++s) { key[s].deg = ptr[s + 1] - ptr[s]; key[s].row = s; }
+  qsort(key, (size_t)n_rows, sizeof(deg_row), by_degree_desc);
+  for (int64_t t = 0; t < n_rows; ++t) order[t] = key[t].row;
+  free(key);
+  return order;
+}
+
 int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, const double *val,
                        const double *wt, int32_t D, const double *F, double lambda, double *X,
                        int8_t *flags, int nthreads) {
   set_threads(nthreads);
+  int64_t *order = degree_order(n_rows, ptr);
+  if (!order) return -1;
   int64_t nflag = 0;
 #pragma omp parallel reduction(+ : nflag)
   {
@@ -169,8 +191,9 @@ int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, c
     double *W = (double *)malloc(sizeof(double) * D * D);
     double *b = (double *)malloc(sizeof(double) * D);
     double *xs = (double *)malloc(sizeof(double) * D);
-#pragma omp for schedule(dynamic, 16)
-    for (int64_t s = 0; s < n_rows; ++s) {
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t t = 0; t < n_rows; ++t) {
+      const int64_t s = order[t];
       int st = solve_one(D, ptr[s + 1] - ptr[s], idx + ptr[s], val + ptr[s],
                          wt ? wt + ptr[s] : NULL, F, lambda, A, b, W, xs, X + s * D);
       if (flags) flags[s] = (int8_t)st;
@@ -178,6 +201,7 @@ int64_t orc_half_sweep(int64_t n_rows, const int64_t *ptr, const int32_t *idx, c
     }
     free(A); free(W); free(b); free(xs);
   }
+  free(order);
   return nflag;
 }
 

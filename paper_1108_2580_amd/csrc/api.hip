@@ -93,7 +93,9 @@ struct als_ctx {
   double *d_sse_total = nullptr; // SSE of the last residual pass
   int32_t *d_flag = nullptr;
   double *h_sse = nullptr;    // pinned
-  double *h_sse_in = nullptr; // pinned
+  double *h_sse_in = nullptr; // pinned [2]: the entering-state SSE of the last half-sweep,
+                              // in one part, or two for the time chain's even and odd passes
+  int sse_in_parts = 1;
   int32_t *h_flag = nullptr;  // pinned
   int last_side = -1;
   std::string err;
@@ -635,11 +637,11 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   CK(dalloc(&c->d_sse_total, 1));
   CK(dalloc(&c->d_flag, 1));
   CK(hipHostMalloc((void **)&c->h_sse, sizeof(double), hipHostMallocDefault));
-  CK(hipHostMalloc((void **)&c->h_sse_in, sizeof(double), hipHostMallocDefault));
+  CK(hipHostMalloc((void **)&c->h_sse_in, 2 * sizeof(double), hipHostMallocDefault));
   CK(hipHostMalloc((void **)&c->h_flag, sizeof(int32_t), hipHostMallocDefault));
   *c->h_flag = 0;
   *c->h_sse = 0.0;
-  *c->h_sse_in = 0.0;
+  c->h_sse_in[0] = c->h_sse_in[1] = 0.0;
   CK(als::launch_fill_i32(c->d_flag, 1, 0, c->stream));
   CK(hipStreamSynchronize(c->stream));
 #undef CK
@@ -664,6 +666,7 @@ struct SweepSpec {
   int64_t n_fixed = 0;
   als::Hadamard hd;
   bool keep_flags = false;  // add to the flag count of the previous sweep (time chain)
+  int sse_in_part = 0;      // which part of the entering-state SSE this pass writes
 };
 
 als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out_factors,
@@ -758,11 +761,12 @@ als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out
     HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_sse_items, (int64_t)P.gitems.size(),
                                         ctx->d_partials, ctx->d_sse_in, ctx->stream));
   }
-  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse_in, ctx->d_sse_in, sizeof(double),
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse_in + sp.sse_in_part, ctx->d_sse_in, sizeof(double),
                                   hipMemcpyDeviceToHost, ctx->stream));
   HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, ctx->stream));
   ctx->last_side = side;
+  ctx->sse_in_parts = sp.sse_in_part + 1;
   if (ctx->phase_timing && !ctx->lane_solve && !P.rows.empty() && side < 2) {
     const int64_t nr = (int64_t)P.rows.size();
     HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_cyc, nr, ctx->d_partials, ctx->d_cyc_sum,
@@ -945,7 +949,11 @@ als_status als_last_rmse_in(als_ctx *ctx, double *rmse_in) {
   if (ctx->last_side < 0) return fail(ctx, ALS_ERR_INVALID_ARG, "no half-sweep has run yet");
   DeviceGuard g(ctx->device);
   HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
-  *rmse_in = ctx->nnz > 0 ? std::sqrt(*ctx->h_sse_in / (double)ctx->nnz) : 0.0;
+  // the time chain's passes cover disjoint ratings (a rating's prediction reads only its own
+  // bin's row, which the other parity's pass leaves alone): their parts add up, in order
+  double sse = 0.0;
+  for (int q = 0; q < ctx->sse_in_parts; ++q) sse += ctx->h_sse_in[q];
+  *rmse_in = ctx->nnz > 0 ? std::sqrt(sse / (double)ctx->nnz) : 0.0;
   return ALS_OK;
 }
 
@@ -971,7 +979,7 @@ als_status als_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_o
   return ALS_OK;
 }
 
-int64_t als_flagged_rows(als_ctx *ctx) {
+int64_t als_flagged_rows(const als_ctx *ctx) {
   if (!ctx) return -1;
   DeviceGuard g(ctx->device);
   if (hipStreamSynchronize(ctx->stream) != hipSuccess) return -1;
@@ -1101,7 +1109,7 @@ als_status als_set_time_bins(als_ctx *ctx, int32_t n_bins, const int32_t *bins) 
   if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
   ctx->err.clear();
   if (n_bins < 1) return fail(ctx, ALS_ERR_INVALID_ARG, "n_bins must be >= 1");
-  if ((int64_t)(n_bins + 1) * ctx->DP * 4 > als::kMaxStagedBytes)
+  if (((int64_t)n_bins + 1) * ctx->DP * 4 > als::kMaxStagedBytes)
     return fail(ctx, ALS_ERR_INVALID_ARG, "too many time bins for the staged-table limit");
   if (ctx->nnz > 0 && !bins) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL bins");
   for (int64_t p = 0; p < ctx->nnz; ++p) {
@@ -1392,6 +1400,7 @@ als_status als_tensor_gibbs_half_sweep(als_ctx *ctx, als_mode mode, float *U, fl
     SweepSpec sq = sp;
     sq.plan = 3 + parity;
     sq.keep_flags = parity == 1;
+    sq.sse_in_part = parity;
     st = run_sweep(ctx, sq, 0.f, T, nullptr, pr);
     if (st != ALS_OK) return st;
   }

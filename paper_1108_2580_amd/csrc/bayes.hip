@@ -1,5 +1,5 @@
-// Bayesian factorisation (BPTF, named in Sec. 2.2: least squares plus sampling from the
-// hyperpriors of U and V), in the form of the published BPMF / BPTF Gibbs sampler.
+// Bayesian factorisation (BPTF, Sec. 2.2, which pairs the least-squares update with draws
+// of the factor priors' parameters), in the form of the published BPMF / BPTF Gibbs sampler.
 // Ratings are Gaussian with precision alpha around u . v; each row of a side has the
 // prior N(mu, Lambda^{-1}); (mu, Lambda) has a Normal-Wishart hyperprior. The row draws
 // reuse the half-sweep kernels (their BAYES variants): this file holds the rest.

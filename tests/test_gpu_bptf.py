@@ -119,8 +119,15 @@ def check_chain(M, N, K, D, seed, tuning=None, empty_bins=(3,), deg=(6, 30), emp
         log(f"  {label} chain D={D} K={K}")
         rm = als.tensor_gibbs_half_sweep("bins", Ud, Vd, Td, alpha, dev(Lam, np.float64),
                                          dev(mu, np.float64), dev(z), rmse=True)
+        rm_in = als.rmse_in()
         tg = Td.cpu().numpy()
         assert als.flagged_rows() == 0
+    # the entering state's RMSE covers every rating: the even pass's residuals plus the odd
+    # pass's, both of the bins as they entered the chain
+    by_user = groupings(M, N, K, ptr, col, bins, val)[0]
+    ro_in = np.sqrt(oracle.tensor_sse(*by_user, U, V, T) / col.size)
+    log(f"    entering rmse gpu {rm_in:.9f} oracle {ro_in:.9f}")
+    assert abs(rm_in - ro_in) <= 1e-5
     # the oracle draws the even bins, then the odd bins given the new even ones
     to, fl0 = oracle.time_rows(p, i1, i2, v, U, V, alpha, Lam, mu, z, 0, T)
     # the odd pass reads the GPU's even bins, so each pass is checked from identical inputs

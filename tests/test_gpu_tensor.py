@@ -179,6 +179,13 @@ def test_tensor_argument_errors():
         bad[3] = -1
         with pytest.raises(ALSError):
             als.set_time_bins(n_bins, bad)
+        # the staged time-bin table, (n_bins + 1) rows of 16 * ceil(D / 16) floats, must stay
+        # below 4 GiB; at n_bins = 2^31 - 1 the row count is formed in 64 bits, and the call
+        # is refused before it reads a bin
+        for nb in (2**31 - 1, 2**26 - 1):
+            with pytest.raises(ALSError) as e:
+                als.set_time_bins(nb, bins)
+            assert e.value.status == ALS_ERR_INVALID_ARG and "limit" in str(e.value)
         als.set_time_bins(n_bins, bins)
         Td = dev(T)
         with pytest.raises(ALSError):  # U and V the same buffer

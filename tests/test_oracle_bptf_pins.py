@@ -228,36 +228,3 @@ def test_bt8_alpha_posterior_is_conjugate():
         lik = st.norm.logpdf(resid, scale=1 / np.sqrt(alpha)).sum()
         logs.append(prior + lik - st.gamma.logpdf(alpha, a=nu_s / 2, scale=2 * w_s))
     assert np.ptp(logs) <= 1e-9 * max(1.0, np.abs(logs).max())
-
-
-def test_bt9_chain_iteration_is_deterministic_and_moves_every_mode():
-    """One BPTF iteration from fixed variates: reproducible bit for bit, every mode drawn."""
-    rng = np.random.default_rng(130)
-    M, N, K, D = 12, 10, 5, 3
-    n = 80
-    users = np.sort(rng.integers(0, M, size=n)).astype(np.int32)
-    row_ptr = np.searchsorted(users, np.arange(M + 1)).astype(np.int64)
-    col = rng.integers(0, N, size=n).astype(np.int32)
-    bins = rng.integers(0, K, size=n).astype(np.int32)
-    val = rng.integers(0, 101, size=n).astype(np.float64) / 10
-    U0, V0 = rng.normal(0, 0.5, size=(M, D)), rng.normal(0, 0.5, size=(N, D))
-    T0 = 1 + 0.1 * rng.normal(size=(K, D))
-    priors = {s: (np.zeros(D), 2.0, np.eye(D), float(D)) for s in ("items", "users", "time")}
-    var = {
-        "alpha_chi2": float(rng.chisquare(4 + n)),
-        "hyper": {s: (rng.chisquare(np.arange(D + 2, 2, -1) + (K if s == "time" else 0)),
-                      rng.normal(size=D * (D - 1) // 2), rng.normal(size=D))
-                  for s in ("items", "users", "time")},
-        "z": {"items": rng.normal(size=(N, D)), "users": rng.normal(size=(M, D)),
-              "time": rng.normal(size=(K, D))},
-    }
-    outs = []
-    for _ in range(2):
-        c = oracle.BPTFChain(M, N, K, row_ptr, col, bins, val, U0, V0, T0)
-        alpha, hyper = c.iterate((1.0, 4.0), priors, var)
-        outs.append((alpha, c.U.copy(), c.V.copy(), c.T.copy()))
-    a, b = outs
-    assert a[0] == b[0] and all(np.array_equal(x, y) for x, y in zip(a[1:], b[1:]))
-    assert alpha > 0
-    assert not np.array_equal(a[1], U0) and not np.array_equal(a[2], V0)
-    assert not np.array_equal(a[3], T0)

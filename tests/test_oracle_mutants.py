@@ -148,7 +148,7 @@ def test_pins_catch_mutant(tmp_path, name, orig, mut):
     path = tmp_path / "mutant.c"
     path.write_text(src.replace(orig, mut))
     so = tmp_path / "libmutant.so"
-    subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", str(so), str(path), "-lm"])
+    subprocess.check_call(["gcc", *oracle.CFLAGS, "-shared", "-fPIC", "-o", str(so), str(path), "-lm"])
     saved = oracle._lib
     oracle._lib = oracle._configure(ctypes.CDLL(str(so)))
     caught = []
