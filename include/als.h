@@ -231,6 +231,28 @@ als_status als_set_holdout(als_ctx *ctx, int64_t n_pairs, const int32_t *users,
 als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double *rmse_out);
 
 /*
+ * Validation RMSE of (U, V) on caller-provided device pairs, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and fixed summation order as als_holdout_rmse,
+ * with no registration and no allocation. Its scratch (per-block sums, the reduction's
+ * partials and the total) is a fixed array of 4 MiB in device memory that every GPU the
+ * library runs on holds until the process ends; the call neither allocates nor frees.
+ *   users, items, ratings  device int32[n_pairs], int32[n_pairs], uint8[n_pairs], read only;
+ *                          a pair with an index outside the tables makes the result NaN.
+ *                          Pairs grouped by user (as als_set_holdout stores them) give the
+ *                          registered set's result bit for bit.
+ *   n_pairs                0 .. 16,000,000 (ALS_ERR_INVALID_ARG above: the scratch's limit);
+ *                          0 gives 0.
+ *   U, V, rmse_out         as for als_holdout_rmse. Synchronises the context's stream.
+ * All calls on one GPU share its scratch array, whatever their context: calls that
+ * overlap on one GPU (other host threads, other streams) race and must be serialised by
+ * the caller.
+ */
+als_status als_pair_rmse_noalloc(als_ctx *ctx, const float *U, const float *V, int64_t n_pairs,
+                                 const int32_t *users, const int32_t *items,
+                                 const uint8_t *ratings, double *rmse_out);
+
+/*
  * Bayesian factorisation (BPTF, paper Sec. 2.2, which pairs the least-squares update with
  * draws of the factor priors' parameters), as the published BPMF / BPTF Gibbs sampler: ratings are
  * Gaussian with precision alpha around u . v; each row of a side has the prior

@@ -28,7 +28,7 @@ EXPORTS = ("als_create", "als_half_sweep", "als_last_rmse_in", "als_rmse", "als_
            "als_get_csc",
            "als_plan_stats", "als_set_profiling", "als_get_profile", "als_set_weights",
            "als_set_phase_timing", "als_get_phase_cycles", "als_predict", "als_set_holdout",
-           "als_holdout_rmse", "als_set_nw_prior", "als_sample_hyper", "als_gibbs_half_sweep",
+           "als_holdout_rmse", "als_pair_rmse_noalloc", "als_set_nw_prior", "als_sample_hyper", "als_gibbs_half_sweep",
            "als_set_time_bins", "als_tensor_half_sweep", "als_tensor_rmse",
            "als_set_time_nw_prior", "als_sample_time_hyper", "als_tensor_gibbs_half_sweep",
            "als_tensor_sample_alpha",
@@ -88,6 +88,8 @@ def _load_library(path=LIB_PATH):
     lib.als_set_holdout.restype = st
     lib.als_holdout_rmse.argtypes = [P, P, P, ctypes.POINTER(ctypes.c_double)]
     lib.als_holdout_rmse.restype = st
+    lib.als_pair_rmse_noalloc.argtypes = [P, P, P, i64, P, P, P, ctypes.POINTER(ctypes.c_double)]
+    lib.als_pair_rmse_noalloc.restype = st
     f64 = ctypes.c_double
     lib.als_set_nw_prior.argtypes = [P, st, P, f64, P, f64]
     lib.als_set_nw_prior.restype = st
@@ -290,6 +292,29 @@ class ALS:
         vp = _dev_ptr(V, self.D, self.N, "V")
         r = ctypes.c_double(0.0)
         self._check(lib.als_holdout_rmse(self._h, up, vp, ctypes.byref(r)))
+        return r.value
+
+    def pair_rmse_noalloc(self, U, V, users, items, ratings):
+        """Validation RMSE of (U, V) on device pairs (contiguous 1-D int32 ``users`` and
+        ``items``, uint8 ``ratings`` CUDA tensors) through the allocation-free entry point."""
+        import torch
+
+        up = _dev_ptr(U, self.D, self.M, "U")
+        vp = _dev_ptr(V, self.D, self.N, "V")
+        for t, name, dt in ((users, "users", torch.int32), (items, "items", torch.int32),
+                            (ratings, "ratings", torch.uint8)):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != dt or \
+                    not t.is_contiguous() or t.dim() != 1:
+                raise TypeError(f"{name} must be a contiguous 1-D {dt} CUDA tensor")
+        n = users.numel()
+        if items.numel() != n or ratings.numel() != n:
+            raise ValueError("users, items and ratings differ in length")
+        r = ctypes.c_double(0.0)
+        self._check(lib.als_pair_rmse_noalloc(self._h, up, vp, n,
+                                              ctypes.c_void_p(users.data_ptr()),
+                                              ctypes.c_void_p(items.data_ptr()),
+                                              ctypes.c_void_p(ratings.data_ptr()),
+                                              ctypes.byref(r)))
         return r.value
 
     # ---- Bayesian (BPMF / BPTF) Gibbs step ----------------------------------------------

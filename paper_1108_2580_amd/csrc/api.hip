@@ -15,6 +15,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -147,6 +148,7 @@ struct als_ctx {
   double *d_time_partials = nullptr;  // its per-slice partial sums
   int64_t time_partials_cap = 0;
   double *d_zero_mu = nullptr;     // D zeros (the chain's image has no mean term)
+  double *d_scratch = nullptr;     // this device's copy of the allocation-free scratch array
 };
 
 namespace {
@@ -472,6 +474,35 @@ als_status residual_pass(als_ctx *c, const SidePlan &P, const int32_t *idx, cons
   return ALS_OK;
 }
 
+// ---- scratch of the allocation-free validation RMSE ---------------------------------------
+// als_pair_rmse_noalloc keeps the per-block squared errors of its pairs, the reduction's
+// partial sums and the total in this file-scope array: every GPU the library runs on holds
+// its own copy until the process ends. Host code never names the array itself (its name
+// on the host is only a stand-in); it uses the device address that hipGetSymbolAddress
+// returns for the current device, once per device, at context creation.
+constexpr int64_t kScratchDoubles = 1 << 19;  // 4 MiB per GPU
+constexpr int64_t kNoAllocMaxPairs = 16000000;
+static __device__ __align__(256) double scratch[kScratchDoubles];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double *g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the scratch array on `device`, which must be the current device.
+hipError_t scratch_address(int device, double **out) {
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[device]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_dev[device] = static_cast<double *>(ptr);
+  }
+  *out = g_scratch_dev[device];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -560,6 +591,14 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   if (hipGetDevice(&c->device) != hipSuccess) {
     delete c;
     return fail(nullptr, ALS_ERR_HIP, "no HIP device");
+  }
+  {
+    const hipError_t e = scratch_address(c->device, &c->d_scratch);
+    if (e != hipSuccess) {
+      delete c;
+      return fail(nullptr, ALS_ERR_HIP, "scratch address on device %d: %s", c->device,
+                  hipGetErrorString(e));
+    }
   }
   auto bail = [&](als_status st) {
     g_create_err = c->err;
@@ -1565,6 +1604,42 @@ als_status als_holdout_rmse(als_ctx *ctx, const float *U, const float *V, double
                                   hipMemcpyDeviceToHost, ctx->stream));
   HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
   *rmse_out = std::sqrt(*ctx->h_sse / (double)ctx->n_hold);
+  return ALS_OK;
+}
+
+als_status als_pair_rmse_noalloc(als_ctx *ctx, const float *U, const float *V, int64_t n_pairs,
+                                 const int32_t *users, const int32_t *items,
+                                 const uint8_t *ratings, double *rmse_out) {
+  if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  ctx->err.clear();
+  if (!U || !V || !rmse_out) return fail(ctx, ALS_ERR_INVALID_ARG, "NULL argument");
+  if (n_pairs < 0 || n_pairs > kNoAllocMaxPairs)
+    return fail(ctx, ALS_ERR_INVALID_ARG,
+                "n_pairs = %lld outside [0, %lld], the capacity of the fixed scratch array",
+                (long long)n_pairs, (long long)kNoAllocMaxPairs);
+  if (n_pairs > 0 && (!users || !items || !ratings))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "NULL pair array");
+  if (((uintptr_t)U & 15) || ((uintptr_t)V & 15))
+    return fail(ctx, ALS_ERR_INVALID_ARG, "factor buffers must be 16-byte aligned");
+  if (n_pairs == 0) {
+    *rmse_out = 0.0;
+    return ALS_OK;
+  }
+  // scratch layout: per-block squared errors [nb], the reduction's partials [np], total [1]
+  const int64_t nb = als::pair_blocks(n_pairs, ctx->D);
+  const int64_t np = als::reduce_partials(nb);
+  if (nb + np + 1 > kScratchDoubles)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "%lld pairs need %lld scratch doubles, above %lld",
+                (long long)n_pairs, (long long)(nb + np + 1), (long long)kScratchDoubles);
+  DeviceGuard g(ctx->device);
+  double *blocks = ctx->d_scratch, *partials = blocks + nb, *total = partials + np;
+  HIP_OR_FAIL(ctx, als::launch_predict(U, V, ctx->M, ctx->N, ctx->D, n_pairs, users, items,
+                                       ratings, nullptr, blocks, ctx->stream));
+  HIP_OR_FAIL(ctx, als::launch_reduce(blocks, nb, partials, total, ctx->stream));
+  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse, total, sizeof(double), hipMemcpyDeviceToHost,
+                                  ctx->stream));
+  HIP_OR_FAIL(ctx, hipStreamSynchronize(ctx->stream));
+  *rmse_out = std::sqrt(*ctx->h_sse / (double)n_pairs);
   return ALS_OK;
 }
 
