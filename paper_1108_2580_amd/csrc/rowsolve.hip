@@ -158,7 +158,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   using C = RowCfg<DP>;
   constexpr int T = C::T, NT = C::NT;
   constexpr int NPAN = DP / 4;
-  __shared__ floatx4 s_panel[kRowWaves][T][16];  // one panel's rows, per tile column and lane column
+  // tile row I0 of the panel step, as published by each row group: [row group][tile column][lane column]
+  __shared__ floatx4 s_panel[kRowWaves][4][T][16];
   // per panel: M as a full 4 x 4 row-major block (zeros above the diagonal), then y_p
   __shared__ __attribute__((aligned(16))) float s_ud[kRowWaves][NPAN][20];
   __shared__ GroupStage s_stage[kRowWaves];        // gather staging of the row's rating groups
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   if (task >= n_rows) return;
   const RowTask rt = rows[task];
   const int lane = threadIdx.x & 63, kq = lane >> 4, c = lane & 15;
-  floatx4(&panel)[T][16] = s_panel[wv];
+  floatx4(&panel)[4][T][16] = s_panel[wv];
   float(&ud)[NPAN][20] = s_ud[wv];
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
 
@@ -281,126 +282,156 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   const uint64_t t_gram = __builtin_readcyclecounter();
 
   // ---- factorisation A = U^T U with forward substitution U^T y = b ------------------------
+  // Panel step (I0, g) of rows p0 .. p0 + 3, p0 = 16 I0 + 4 g. Its update of the trailing
+  // tiles is split in two: the tiles that the next panel reads (tile row I0 while g < 3,
+  // else tile row I0 + 1) are updated at once; the tiles below them are updated during
+  // the next panel's step, in the same instruction stream as that step's dependent chain
+  // of scalar-like work (diagonal block, pivots, M), so that the matrix unit runs while
+  // the chain waits on its own latencies. The per-tile order of the updates is unchanged.
   bool bad = false;
+  float up[T];  // the previous panel's rows U_p(:, 16 X + c) (its deferred update)
 #pragma unroll
-  for (int I0 = 0; I0 < T; ++I0) {
-    // panels of one tile row run as a loop (unrolling them all would blow up the
-    // register allocation around the accumulator tiles)
-#pragma clang loop unroll(disable)
-    for (int g = 0; g < 4; ++g) {
-      const int p0 = 16 * I0 + 4 * g;
-      if (p0 >= D) break;
-      // (1) the 4x4 diagonal block A[p0 + r][p0 + r'] sits in element r of lane
-      // (g, 4 g + r') of tile (I0, I0); it goes to scalar registers directly, while the
-      // panel rows p0..p0+3 (held by row group g) are published to LDS for the columns
-      const floatx4 dg = acc[tidx<T>(I0, I0)];
-      const int l0 = 20 * g;
-      const float a00 = lane_value(dg[0], l0), a01 = lane_value(dg[0], l0 + 1);
-      const float a02 = lane_value(dg[0], l0 + 2), a03 = lane_value(dg[0], l0 + 3);
-      const float a11 = lane_value(dg[1], l0 + 1), a12 = lane_value(dg[1], l0 + 2);
-      const float a13 = lane_value(dg[1], l0 + 3), a22 = lane_value(dg[2], l0 + 2);
-      const float a23 = lane_value(dg[2], l0 + 3), a33 = lane_value(dg[3], l0 + 3);
-      if (kq == g) {
-#pragma unroll
-        for (int X = I0; X < T; ++X) panel[X][c] = acc[tidx<T>(I0, X)];
-      }
-      // (2) 4x4 diagonal block, factored redundantly in every lane
-      float p;
-      p = a00;
-      bad |= !(p > 0.f && p < INFINITY);
-      const float i00 = inv_sqrt_pivot(p);
-      const float u01 = a01 * i00, u02 = a02 * i00, u03 = a03 * i00;
-      p = a11 - u01 * u01;
-      bad |= !(p > 0.f && p < INFINITY);
-      const float i11 = inv_sqrt_pivot(p);
-      const float u12 = (a12 - u01 * u02) * i11, u13 = (a13 - u01 * u03) * i11;
-      p = a22 - u02 * u02 - u12 * u12;
-      bad |= !(p > 0.f && p < INFINITY);
-      const float i22 = inv_sqrt_pivot(p);
-      const float u23 = (a23 - u02 * u03 - u12 * u13) * i22;
-      p = a33 - u03 * u03 - u13 * u13 - u23 * u23;
-      bad |= !(p > 0.f && p < INFINITY);
-      const float i33 = inv_sqrt_pivot(p);
-      // M = U_gg^{-T} (lower triangular; diagonal 1 / u_qq)
-      const float m00 = i00;
-      const float m10 = -(u01 * m00) * i11, m11 = i11;
-      const float m20 = -(u02 * m00 + u12 * m10) * i22, m21 = -(u12 * m11) * i22, m22 = i22;
-      const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
-      const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
-      const int pan = p0 >> 2;
-      float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
-      if constexpr (!AUG) {
-        // y_p = M b_p, and the weights v = M^T y_p of the right-hand-side update
-        const float b0 = lane_value(rhs[I0], 4 * g + 0), b1 = lane_value(rhs[I0], 4 * g + 1);
-        const float b2 = lane_value(rhs[I0], 4 * g + 2), b3 = lane_value(rhs[I0], 4 * g + 3);
-        const float y0 = m00 * b0;
-        const float y1 = m10 * b0 + m11 * b1;
-        const float y2 = m20 * b0 + m21 * b1 + m22 * b2;
-        const float y3 = m30 * b0 + m31 * b1 + m32 * b2 + m33 * b3;
-        v0 = m00 * y0 + m10 * y1 + m20 * y2 + m30 * y3;
-        v1 = m11 * y1 + m21 * y2 + m31 * y3;
-        v2 = m22 * y2 + m32 * y3;
-        v3 = m33 * y3;
-        if (lane == 0) {
-          ud[pan][16] = y0; ud[pan][17] = y1; ud[pan][18] = y2; ud[pan][19] = y3;
-        }
-      }
-      if (lane == 0) {
-        float4 *mr = reinterpret_cast<float4 *>(ud[pan]);
-        mr[0] = make_float4(m00, 0.f, 0.f, 0.f);
-        mr[1] = make_float4(m10, m11, 0.f, 0.f);
-        mr[2] = make_float4(m20, m21, m22, 0.f);
-        mr[3] = make_float4(m30, m31, m32, m33);
-      }
-      // (3) panel rows U[p0 + kq][j] = (M A_p)[kq][j] for the later columns j (zero for
-      // j <= p0 + 3, which keeps the finished rows and columns out of the update)
-      wave_sync();
-      // this lane's row of M (row group kq holds panel row p0 + kq)
-      const float4 wr = reinterpret_cast<const float4 *>(ud[pan])[kq];
-      const float w0 = wr.x, w1 = wr.y, w2 = wr.z, w3 = wr.w;
-      float u[T];
-#pragma unroll
-      for (int X = 0; X < T; ++X) {
-        u[X] = 0.f;
-        if (X >= I0) {
-          const floatx4 col = panel[X][c];
-          float Y = w0 * col[0];
-          Y = fmaf(w1, col[1], Y);
-          Y = fmaf(w2, col[2], Y);
-          Y = fmaf(w3, col[3], Y);
-          const int j = 16 * X + c;
-          if (X == I0) Y = j > p0 + 3 ? Y : 0.f;
-          if constexpr (!AUG) {
-            if (j > p0 + 3) rhs[X] -= v0 * col[0] + v1 * col[1] + v2 * col[2] + v3 * col[3];
-          }
-          u[X] = Y;
-        }
-      }
-      if constexpr (AUG) {
-        // the augmented column's panel entries are y_p = U_gg^{-T} b_p
-        if (c == aug_c) ud[pan][16 + kq] = u[T - 1];
-      }
-      // (4) trailing update on MFMA: A_IJ -= U_p(:, I)^T U_p(:, J). The tile row that the
-      // next panel publishes is issued first, so that the next panel's factorisation runs
-      // while the matrix unit works through the rest. After the last panel of a tile row
-      // (g == 3) that row has no unfactored rows left and its update is skipped.
-      if (g < 3) {
-#pragma unroll
-        for (int J = I0; J < T; ++J)
-          acc[tidx<T>(I0, J)] =
-              __builtin_amdgcn_mfma_f32_16x16x4f32(-u[I0], u[J], acc[tidx<T>(I0, J)], 0, 0, 0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+  for (int X = 0; X < T; ++X) up[X] = 0.f;
+  // one-hot row-group selectors: lane (kq, c) takes row kq of M
+  const float e0 = kq == 0 ? 1.f : 0.f, e1 = kq == 1 ? 1.f : 0.f;
+  const float e2 = kq == 2 ? 1.f : 0.f, e3 = kq == 3 ? 1.f : 0.f;
+  // DEFER: the step issues its predecessor's deferred update; LAST: the step is the last
+  // panel of its tile row (g = 3), whose immediate update is of tile row I0 + 1.
+  auto panel_step = [&](auto i0c, auto deferc, auto lastc, int g) {
+    constexpr int I0 = decltype(i0c)::value;
+    constexpr bool DEFER = decltype(deferc)::value != 0;
+    constexpr bool LAST = decltype(lastc)::value != 0;
+    const int p0 = 16 * I0 + 4 * g;
+    const int pan = p0 >> 2;
+    // (0) the previous panel's update of the tiles below tile row I0
+    if constexpr (DEFER) {
 #pragma unroll
       for (int I = I0 + 1; I < T; ++I) {
 #pragma unroll
         for (int J = I; J < T; ++J)
           acc[tidx<T>(I, J)] =
-              __builtin_amdgcn_mfma_f32_16x16x4f32(-u[I], u[J], acc[tidx<T>(I, J)], 0, 0, 0);
+              __builtin_amdgcn_mfma_f32_16x16x4f32(-up[I], up[J], acc[tidx<T>(I, J)], 0, 0, 0);
       }
-      wave_sync();
     }
-  }
+    // (1) the 4x4 diagonal block A[p0 + r][p0 + r'] sits in element r of lane
+    // (g, 4 g + r') of tile (I0, I0) and goes to scalar registers; every row group
+    // publishes its rows of tile row I0 to LDS, and every lane reads row group g's
+    // (the panel rows p0 .. p0 + 3) for its column
+    const floatx4 dg = acc[tidx<T>(I0, I0)];
+    const int l0 = 20 * g;
+    const float a00 = lane_value(dg[0], l0), a01 = lane_value(dg[0], l0 + 1);
+    const float a02 = lane_value(dg[0], l0 + 2), a03 = lane_value(dg[0], l0 + 3);
+    const float a11 = lane_value(dg[1], l0 + 1), a12 = lane_value(dg[1], l0 + 2);
+    const float a13 = lane_value(dg[1], l0 + 3), a22 = lane_value(dg[2], l0 + 2);
+    const float a23 = lane_value(dg[2], l0 + 3), a33 = lane_value(dg[3], l0 + 3);
+#pragma unroll
+    for (int X = I0; X < T; ++X) panel[kq][X][c] = acc[tidx<T>(I0, X)];
+    floatx4 col[T];
+#pragma unroll
+    for (int X = I0; X < T; ++X) col[X] = panel[g][X][c];
+    // (2) 4x4 diagonal block, factored redundantly in every lane
+    float p;
+    p = a00;
+    bad |= !(p > 0.f && p < INFINITY);
+    const float i00 = inv_sqrt_pivot(p);
+    const float u01 = a01 * i00, u02 = a02 * i00, u03 = a03 * i00;
+    p = a11 - u01 * u01;
+    bad |= !(p > 0.f && p < INFINITY);
+    const float i11 = inv_sqrt_pivot(p);
+    const float u12 = (a12 - u01 * u02) * i11, u13 = (a13 - u01 * u03) * i11;
+    p = a22 - u02 * u02 - u12 * u12;
+    bad |= !(p > 0.f && p < INFINITY);
+    const float i22 = inv_sqrt_pivot(p);
+    const float u23 = (a23 - u02 * u03 - u12 * u13) * i22;
+    p = a33 - u03 * u03 - u13 * u13 - u23 * u23;
+    bad |= !(p > 0.f && p < INFINITY);
+    const float i33 = inv_sqrt_pivot(p);
+    // M = U_gg^{-T} (lower triangular; diagonal 1 / u_qq)
+    const float m00 = i00;
+    const float m10 = -(u01 * m00) * i11, m11 = i11;
+    const float m20 = -(u02 * m00 + u12 * m10) * i22, m21 = -(u12 * m11) * i22, m22 = i22;
+    const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
+    const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
+    // this lane's row of M (row group kq holds panel row p0 + kq); the one-hot sums are
+    // exact (every other term is a zero product)
+    const float w0 = e0 * m00 + e1 * m10 + e2 * m20 + e3 * m30;
+    const float w1 = e1 * m11 + e2 * m21 + e3 * m31;
+    const float w2 = e2 * m22 + e3 * m32;
+    const float w3 = e3 * m33;
+    float y0 = 0.f, y1 = 0.f, y2 = 0.f, y3 = 0.f;
+    float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+    if constexpr (!AUG) {
+      // y_p = M b_p, and the weights v = M^T y_p of the right-hand-side update
+      const float b0 = lane_value(rhs[I0], 4 * g + 0), b1 = lane_value(rhs[I0], 4 * g + 1);
+      const float b2 = lane_value(rhs[I0], 4 * g + 2), b3 = lane_value(rhs[I0], 4 * g + 3);
+      y0 = m00 * b0;
+      y1 = m10 * b0 + m11 * b1;
+      y2 = m20 * b0 + m21 * b1 + m22 * b2;
+      y3 = m30 * b0 + m31 * b1 + m32 * b2 + m33 * b3;
+      v0 = m00 * y0 + m10 * y1 + m20 * y2 + m30 * y3;
+      v1 = m11 * y1 + m21 * y2 + m31 * y3;
+      v2 = m22 * y2 + m32 * y3;
+      v3 = m33 * y3;
+    }
+    // (3) panel rows U[p0 + kq][j] = (M A_p)[kq][j] for the later columns j (zero for
+    // j <= p0 + 3, which keeps the finished rows and columns out of the update)
+    float u[T];
+#pragma unroll
+    for (int X = 0; X < T; ++X) {
+      u[X] = 0.f;
+      if (X >= I0) {
+        float Y = w0 * col[X][0];
+        Y = fmaf(w1, col[X][1], Y);
+        Y = fmaf(w2, col[X][2], Y);
+        Y = fmaf(w3, col[X][3], Y);
+        const int j = 16 * X + c;
+        if (X == I0) Y = j > p0 + 3 ? Y : 0.f;
+        if constexpr (!AUG) {
+          if (j > p0 + 3)
+            rhs[X] -= v0 * col[X][0] + v1 * col[X][1] + v2 * col[X][2] + v3 * col[X][3];
+        }
+        u[X] = Y;
+      }
+    }
+    // (4) the update of the tiles that the next panel reads
+    if constexpr (!LAST) {
+#pragma unroll
+      for (int J = I0; J < T; ++J)
+        acc[tidx<T>(I0, J)] =
+            __builtin_amdgcn_mfma_f32_16x16x4f32(-u[I0], u[J], acc[tidx<T>(I0, J)], 0, 0, 0);
+    } else if constexpr (I0 + 1 < T) {
+#pragma unroll
+      for (int J = I0 + 1; J < T; ++J)
+        acc[tidx<T>(I0 + 1, J)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+            -u[I0 + 1], u[J], acc[tidx<T>(I0 + 1, J)], 0, 0, 0);
+    }
+#pragma unroll
+    for (int X = 0; X < T; ++X) up[X] = u[X];
+    // (5) M (row-major 4 x 4, zeros above the diagonal) and y_p for the back substitution
+    if (c == 0) *reinterpret_cast<float4 *>(&ud[pan][4 * kq]) = make_float4(w0, w1, w2, w3);
+    if constexpr (AUG) {
+      // the augmented column's panel entries are y_p = U_gg^{-T} b_p
+      if (c == aug_c) ud[pan][16 + kq] = u[T - 1];
+    } else {
+      if (lane == 0) *reinterpret_cast<float4 *>(&ud[pan][16]) = make_float4(y0, y1, y2, y3);
+    }
+  };
+  // Rows from D on are padding: the steps stop at the first panel past D, and the updates
+  // still deferred then only touch padding rows, which nothing reads.
+  auto tile_row = [&](auto i0c) {
+    constexpr int I0 = decltype(i0c)::value;
+    if (16 * I0 >= D) return;
+    // the first panel has no predecessor
+    panel_step(i0c, IntC<I0 == 0 ? 0 : 1>{}, IntC<0>{}, 0);
+    if (16 * I0 + 4 >= D) return;
+    panel_step(i0c, IntC<1>{}, IntC<0>{}, 1);
+    if (16 * I0 + 8 >= D) return;
+    panel_step(i0c, IntC<1>{}, IntC<0>{}, 2);
+    if (16 * I0 + 12 >= D) return;
+    panel_step(i0c, IntC<1>{}, IntC<1>{}, 3);
+  };
+  unroll_blocks<0, T>(tile_row);
+  wave_sync();
 
   if constexpr (BAYES) {
     // y += z / sqrt(alpha): the panels keep y_p in ud[p][16 .. 19]
