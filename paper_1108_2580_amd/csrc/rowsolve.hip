@@ -447,7 +447,45 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   // ---- back substitution U x = y --------------------------------------------------------
   // Panel p: U_gg x_p = y_p - U_p,rest x_rest with U_p,rest = M A_p,rest, where the
   // accumulators still hold the panel rows A_p as they were when the panel was factored
-  // (later updates leave finished rows alone); so x_p = M^T (y_p - M (A_p,rest x_rest)).
+  // (later updates leave finished rows alone); so x_p = M^T (y_p - M s) = t_p - W_p s with
+  // s = A_p,rest x_rest, t_p = M^T y_p and W_p = M^T M. W_p and t_p do not depend on the
+  // solution, so they are formed for all panels at once, one panel per lane, leaving only
+  // s and one 4-term product per panel on the serial path.
+  {
+    constexpr int kUsed = NPAN < 64 ? NPAN : 64;
+    static_assert(NPAN <= 64, "one lane per panel");
+    const int pl = lane < kUsed ? lane : kUsed - 1;
+    if (4 * pl < D) {
+      const float4 q0 = *reinterpret_cast<const float4 *>(&ud[pl][0]);
+      const float4 q1 = *reinterpret_cast<const float4 *>(&ud[pl][4]);
+      const float4 q2 = *reinterpret_cast<const float4 *>(&ud[pl][8]);
+      const float4 q3 = *reinterpret_cast<const float4 *>(&ud[pl][12]);
+      const float4 yy = *reinterpret_cast<const float4 *>(&ud[pl][16]);
+      // M = [q0.x; q1.x q1.y; q2.x q2.y q2.z; q3.x q3.y q3.z q3.w] (lower triangular)
+      const float w00 = q0.x * q0.x + q1.x * q1.x + q2.x * q2.x + q3.x * q3.x;
+      const float w01 = q1.x * q1.y + q2.x * q2.y + q3.x * q3.y;
+      const float w02 = q2.x * q2.z + q3.x * q3.z;
+      const float w03 = q3.x * q3.w;
+      const float w11 = q1.y * q1.y + q2.y * q2.y + q3.y * q3.y;
+      const float w12 = q2.y * q2.z + q3.y * q3.z;
+      const float w13 = q3.y * q3.w;
+      const float w22 = q2.z * q2.z + q3.z * q3.z;
+      const float w23 = q3.z * q3.w;
+      const float w33 = q3.w * q3.w;
+      const float t0 = q0.x * yy.x + q1.x * yy.y + q2.x * yy.z + q3.x * yy.w;
+      const float t1 = q1.y * yy.y + q2.y * yy.z + q3.y * yy.w;
+      const float t2 = q2.z * yy.z + q3.z * yy.w;
+      const float t3 = q3.w * yy.w;
+      if (lane < kUsed) {
+        *reinterpret_cast<float4 *>(&ud[pl][0]) = make_float4(w00, w01, w02, w03);
+        *reinterpret_cast<float4 *>(&ud[pl][4]) = make_float4(w01, w11, w12, w13);
+        *reinterpret_cast<float4 *>(&ud[pl][8]) = make_float4(w02, w12, w22, w23);
+        *reinterpret_cast<float4 *>(&ud[pl][12]) = make_float4(w03, w13, w23, w33);
+        *reinterpret_cast<float4 *>(&ud[pl][16]) = make_float4(t0, t1, t2, t3);
+      }
+    }
+    wave_sync();
+  }
   float xv[T];
 #pragma unroll
   for (int X = 0; X < T; ++X) xv[X] = 0.f;
@@ -468,6 +506,12 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     for (int g = 3; g >= 0; --g) {
       const int p0 = 16 * I0 + 4 * g;
       if (p0 >= D) continue;
+      const int pan = p0 >> 2;
+      // lane column 4 g + jj receives x[p0 + jj]: its row of W_p and its entry of t_p
+      const int jj = c - 4 * g;
+      const int jc = min(max(jj, 0), 3);
+      const float4 wr = *reinterpret_cast<const float4 *>(&ud[pan][4 * jc]);
+      const float tj = ud[pan][16 + jc];
       // s_r = sum_{j > p0 + 3} A_p[r][j] x_j: the solved tiles plus the later panels
       // of this tile
       const float xj = c > 4 * g + 3 ? xv[I0] : 0.f;
@@ -476,20 +520,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
                                fmaf(aa[3], xj, P3));
       const float a0 = lane_value(sr, 16 * g + 0), a1 = lane_value(sr, 16 * g + 4);
       const float a2 = lane_value(sr, 16 * g + 8), a3 = lane_value(sr, 16 * g + 12);
-      const int pan = p0 >> 2;
-      const float m00 = ud[pan][0], m10 = ud[pan][4], m11 = ud[pan][5], m20 = ud[pan][8];
-      const float m21 = ud[pan][9], m22 = ud[pan][10], m30 = ud[pan][12], m31 = ud[pan][13];
-      const float m32 = ud[pan][14], m33 = ud[pan][15];
-      const float z0 = ud[pan][16] - m00 * a0;
-      const float z1 = ud[pan][17] - (m10 * a0 + m11 * a1);
-      const float z2 = ud[pan][18] - (m20 * a0 + m21 * a1 + m22 * a2);
-      const float z3 = ud[pan][19] - (m30 * a0 + m31 * a1 + m32 * a2 + m33 * a3);
-      const float x0 = m00 * z0 + m10 * z1 + m20 * z2 + m30 * z3;
-      const float x1 = m11 * z1 + m21 * z2 + m31 * z3;
-      const float x2 = m22 * z2 + m32 * z3;
-      const float x3 = m33 * z3;
-      const int jj = c - 4 * g;
-      if (jj >= 0 && jj < 4) xv[I0] = jj == 0 ? x0 : (jj == 1 ? x1 : (jj == 2 ? x2 : x3));
+      const float x = tj - (fmaf(wr.x, a0, wr.y * a1) + fmaf(wr.z, a2, wr.w * a3));
+      xv[I0] = (jj >= 0 && jj < 4) ? x : xv[I0];
     }
   }
 
