@@ -466,7 +466,7 @@ def run_workload(args, k):
     elapsed = t1 - t0
     rmse_in = als.rmse_in()
     rmse = als.tensor_rmse(U, V, T) if (args.tensor or args.bptf) else als.rmse(U, V)
-    gram_share = None
+    gram_share = phase_cycles = None
     if r.D > 20 and not (args.tensor or args.bptf):
         # one extra, untimed half-sweep per side with the row kernel's phase clocks on
         als.set_phase_timing(True)
@@ -476,6 +476,11 @@ def run_workload(args, k):
         gu, su = als.phase_cycles("users")
         als.set_phase_timing(False)
         gram_share = (gi + gu) / max(gi + si + gu + su, 1.0)
+        rows_i = als.plan_stats("items")["rows_with_ratings"]
+        rows_u = als.plan_stats("users")["rows_with_ratings"]
+        # mean wavefront clock cycles per row in each phase (both waves of a SIMD share it)
+        phase_cycles = {"items": {"gram": gi / max(rows_i, 1), "solve": si / max(rows_i, 1)},
+                        "users": {"gram": gu / max(rows_u, 1), "solve": su / max(rows_u, 1)}}
     log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
         f"rmse entering last half-sweep {rmse_in}, final {rmse:.6f}")
 
@@ -540,6 +545,7 @@ def run_workload(args, k):
         gram_phase = dict(ms_per_step=g_ms, flops_per_step=g_flops, achieved=g_tf,
                           peak=MFMA_F32_PEAK_TFS, unit="TFLOP/s", frac=g_tf / MFMA_F32_PEAK_TFS,
                           row_kernel_gram_share=gram_share,
+                          cycles_per_row=phase_cycles,
                           method="chunk-kernel time plus the row kernel's time scaled by the "
                                  "share of wavefront clock cycles before the factorisation")
 

@@ -77,6 +77,11 @@ __device__ __forceinline__ float inv_sqrt_pivot(float p) {
   return __builtin_amdgcn_rsqf(fmaxf(p, 1e-30f));
 }
 
+// 1 / sqrt(p) without the clamp, for a factorisation that discards the whole system when
+// a pivot is not positive and finite (the NaN or infinity it then produces stays in that
+// system); two dependent instructions shorter per pivot.
+__device__ __forceinline__ float inv_sqrt_pivot_raw(float p) { return __builtin_amdgcn_rsqf(p); }
+
 template <int T>
 __host__ __device__ constexpr int tidx(int I, int J) {
   return I * T - I * (I - 1) / 2 + (J - I);

@@ -292,11 +292,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   float up[T];  // the previous panel's rows U_p(:, 16 X + c) (its deferred update)
 #pragma unroll
   for (int X = 0; X < T; ++X) up[X] = 0.f;
+  // DEFER: the step issues its predecessor's deferred update; LAST: the step is the last
+  // panel of its tile row (g = 3), whose immediate update is of tile row I0 + 1.
   // one-hot row-group selectors: lane (kq, c) takes row kq of M
   const float e0 = kq == 0 ? 1.f : 0.f, e1 = kq == 1 ? 1.f : 0.f;
   const float e2 = kq == 2 ? 1.f : 0.f, e3 = kq == 3 ? 1.f : 0.f;
-  // DEFER: the step issues its predecessor's deferred update; LAST: the step is the last
-  // panel of its tile row (g = 3), whose immediate update is of tile row I0 + 1.
   auto panel_step = [&](auto i0c, auto deferc, auto lastc, int g) {
     constexpr int I0 = decltype(i0c)::value;
     constexpr bool DEFER = decltype(deferc)::value != 0;
@@ -333,19 +333,19 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     float p;
     p = a00;
     bad |= !(p > 0.f && p < INFINITY);
-    const float i00 = inv_sqrt_pivot(p);
+    const float i00 = inv_sqrt_pivot_raw(p);
     const float u01 = a01 * i00, u02 = a02 * i00, u03 = a03 * i00;
     p = a11 - u01 * u01;
     bad |= !(p > 0.f && p < INFINITY);
-    const float i11 = inv_sqrt_pivot(p);
+    const float i11 = inv_sqrt_pivot_raw(p);
     const float u12 = (a12 - u01 * u02) * i11, u13 = (a13 - u01 * u03) * i11;
     p = a22 - u02 * u02 - u12 * u12;
     bad |= !(p > 0.f && p < INFINITY);
-    const float i22 = inv_sqrt_pivot(p);
+    const float i22 = inv_sqrt_pivot_raw(p);
     const float u23 = (a23 - u02 * u03 - u12 * u13) * i22;
     p = a33 - u03 * u03 - u13 * u13 - u23 * u23;
     bad |= !(p > 0.f && p < INFINITY);
-    const float i33 = inv_sqrt_pivot(p);
+    const float i33 = inv_sqrt_pivot_raw(p);
     // M = U_gg^{-T} (lower triangular; diagonal 1 / u_qq)
     const float m00 = i00;
     const float m10 = -(u01 * m00) * i11, m11 = i11;
@@ -353,7 +353,8 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
     const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
     // this lane's row of M (row group kq holds panel row p0 + kq); the one-hot sums are
-    // exact (every other term is a zero product)
+    // exact (every other term is a zero product). Per-lane selects of the uniform values
+    // compile to branches that sink the M terms into divergent code.
     const float w0 = e0 * m00 + e1 * m10 + e2 * m20 + e3 * m30;
     const float w1 = e1 * m11 + e2 * m21 + e3 * m31;
     const float w2 = e2 * m22 + e3 * m32;
