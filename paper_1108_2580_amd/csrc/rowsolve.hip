@@ -419,16 +419,21 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   };
   // Rows from D on are padding: the steps stop at the first panel past D, and the updates
   // still deferred then only touch padding rows, which nothing reads.
+  // D > 16 (T - 1), so every panel of the tile rows before the last is inside D and only
+  // the last tile row needs the bound; without it the steps of the other tile rows form
+  // one straight-line block that the scheduler can interleave across steps
   auto tile_row = [&](auto i0c) {
     constexpr int I0 = decltype(i0c)::value;
-    if (16 * I0 >= D) return;
+    // (the variants with an explicit right-hand side keep every bound: their longer
+    // straight-line block spills)
+    constexpr bool LASTROW = I0 == T - 1 || !AUG;
     // the first panel has no predecessor
     panel_step(i0c, IntC<I0 == 0 ? 0 : 1>{}, IntC<0>{}, 0);
-    if (16 * I0 + 4 >= D) return;
+    if (LASTROW && 16 * I0 + 4 >= D) return;
     panel_step(i0c, IntC<1>{}, IntC<0>{}, 1);
-    if (16 * I0 + 8 >= D) return;
+    if (LASTROW && 16 * I0 + 8 >= D) return;
     panel_step(i0c, IntC<1>{}, IntC<0>{}, 2);
-    if (16 * I0 + 12 >= D) return;
+    if (LASTROW && 16 * I0 + 12 >= D) return;
     panel_step(i0c, IntC<1>{}, IntC<1>{}, 3);
   };
   unroll_blocks<0, T>(tile_row);
