@@ -162,6 +162,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   __shared__ floatx4 s_panel[kRowWaves][4][T][16];
   // per panel: M as a full 4 x 4 row-major block (zeros above the diagonal), then y_p
   __shared__ __attribute__((aligned(16))) float s_ud[kRowWaves][NPAN][20];
+  __shared__ float s_dummy[kRowWaves][64];  // sink of the stores of lanes without an entry
   __shared__ GroupStage s_stage[kRowWaves];        // gather staging of the row's rating groups
 
   const int wv = threadIdx.x >> 6;
@@ -171,6 +172,7 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   const int lane = threadIdx.x & 63, kq = lane >> 4, c = lane & 15;
   floatx4(&panel)[4][T][16] = s_panel[wv];
   float(&ud)[NPAN][20] = s_ud[wv];
+  float(&dummy)[64] = s_dummy[wv];
   const int aug_c = AUG ? aug_column<DP>(D) : -1;
 
   // A starts as lambda n_s I on the first D diagonal entries and I on the padding (only
@@ -297,6 +299,9 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
   // one-hot row-group selectors: lane (kq, c) takes row kq of M
   const float e0 = kq == 0 ? 1.f : 0.f, e1 = kq == 1 ? 1.f : 0.f;
   const float e2 = kq == 2 ? 1.f : 0.f, e3 = kq == 3 ? 1.f : 0.f;
+  // and lane column c's entry of a row of M (the stores of step (5); zero past c = 3)
+  const float f0 = c == 0 ? 1.f : 0.f, f1 = c == 1 ? 1.f : 0.f;
+  const float f2 = c == 2 ? 1.f : 0.f, f3 = c == 3 ? 1.f : 0.f;
   auto panel_step = [&](auto i0c, auto deferc, auto lastc, int g) {
     constexpr int I0 = decltype(i0c)::value;
     constexpr bool DEFER = decltype(deferc)::value != 0;
@@ -352,13 +357,25 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     const float m20 = -(u02 * m00 + u12 * m10) * i22, m21 = -(u12 * m11) * i22, m22 = i22;
     const float m30 = -(u03 * m00 + u13 * m10 + u23 * m20) * i33;
     const float m31 = -(u13 * m11 + u23 * m21) * i33, m32 = -(u23 * m22) * i33, m33 = i33;
-    // this lane's row of M (row group kq holds panel row p0 + kq); the one-hot sums are
-    // exact (every other term is a zero product). Per-lane selects of the uniform values
-    // compile to branches that sink the M terms into divergent code.
-    const float w0 = e0 * m00 + e1 * m10 + e2 * m20 + e3 * m30;
-    const float w1 = e1 * m11 + e2 * m21 + e3 * m31;
-    const float w2 = e2 * m22 + e3 * m32;
-    const float w3 = e3 * m33;
+    // this lane's row of M (row group kq holds panel row p0 + kq). With the augmented
+    // column nothing else needs M as uniform values: row kq of U_gg^{-T} is column kq of
+    // U_gg^{-1}, the back substitution of U_gg w = e_kq, ten instructions per lane instead
+    // of M's sixteen and the selection's ten. Otherwise (y and v below need M) the row is
+    // picked by one-hot sums, exact since every other term is a zero product; per-lane
+    // selects of the uniform values compile to branches that sink the M terms into
+    // divergent code.
+    float w0, w1, w2, w3;
+    if constexpr (AUG) {
+      w3 = e3 * i33;
+      w2 = (e2 - u23 * w3) * i22;
+      w1 = (e1 - u12 * w2 - u13 * w3) * i11;
+      w0 = (e0 - u01 * w1 - u02 * w2 - u03 * w3) * i00;
+    } else {
+      w0 = e0 * m00 + e1 * m10 + e2 * m20 + e3 * m30;
+      w1 = e1 * m11 + e2 * m21 + e3 * m31;
+      w2 = e2 * m22 + e3 * m32;
+      w3 = e3 * m33;
+    }
     float y0 = 0.f, y1 = 0.f, y2 = 0.f, y3 = 0.f;
     float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
     if constexpr (!AUG) {
@@ -408,13 +425,20 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
     }
 #pragma unroll
     for (int X = 0; X < T; ++X) up[X] = u[X];
-    // (5) M (row-major 4 x 4, zeros above the diagonal) and y_p for the back substitution
-    if (c == 0) *reinterpret_cast<float4 *>(&ud[pan][4 * kq]) = make_float4(w0, w1, w2, w3);
-    if constexpr (AUG) {
-      // the augmented column's panel entries are y_p = U_gg^{-T} b_p
-      if (c == aug_c) ud[pan][16 + kq] = u[T - 1];
-    } else {
-      if (lane == 0) *reinterpret_cast<float4 *>(&ud[pan][16]) = make_float4(y0, y1, y2, y3);
+    // (5) M (row-major 4 x 4, zeros above the diagonal) and y_p for the back substitution.
+    // Every lane stores, the lanes without an entry to a per-lane dummy slot: with
+    // predicated stores each step would end a basic block, and the scheduler could not
+    // interleave one step with the next.
+    {
+      const float wc = f0 * w0 + f1 * w1 + f2 * w2 + f3 * w3;
+      *(c < 4 ? &ud[pan][4 * kq + c] : &dummy[lane]) = wc;
+      if constexpr (AUG) {
+        // the augmented column's panel entries are y_p = U_gg^{-T} b_p
+        *(c == aug_c ? &ud[pan][16 + kq] : &dummy[lane]) = u[T - 1];
+      } else {
+        const float yc = f0 * y0 + f1 * y1 + f2 * y2 + f3 * y3;
+        *(lane < 4 ? &ud[pan][16 + c] : &dummy[lane]) = yc;
+      }
     }
   };
   // Rows from D on are padding: the steps stop at the first panel past D, and the updates
