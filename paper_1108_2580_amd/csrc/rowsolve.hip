@@ -532,16 +532,25 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
       P2 = fmaf(aa[2], xv[X], P2);
       P3 = fmaf(aa[3], xv[X], P3);
     }
-#pragma clang loop unroll(disable)
+    // every lane's row of W_p and entry of t_p for the tile's four panels, read before the
+    // serial steps (lane column 4 g + jj receives x[p0 + jj])
+    float4 wrs[4];
+    float tjs[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int pan = min(4 * I0 + g, NPAN - 1);
+      const int jc = min(max(c - 4 * g, 0), 3);
+      wrs[g] = *reinterpret_cast<const float4 *>(&ud[pan][4 * jc]);
+      tjs[g] = ud[pan][16 + jc];
+    }
+#pragma unroll
     for (int g = 3; g >= 0; --g) {
       const int p0 = 16 * I0 + 4 * g;
-      if (p0 >= D) continue;
-      const int pan = p0 >> 2;
-      // lane column 4 g + jj receives x[p0 + jj]: its row of W_p and its entry of t_p
+      // panels of the tiles before the last are all inside D
+      if (I0 == T - 1 && p0 >= D) continue;
       const int jj = c - 4 * g;
-      const int jc = min(max(jj, 0), 3);
-      const float4 wr = *reinterpret_cast<const float4 *>(&ud[pan][4 * jc]);
-      const float tj = ud[pan][16 + jc];
+      const float4 wr = wrs[g];
+      const float tj = tjs[g];
       // s_r = sum_{j > p0 + 3} A_p[r][j] x_j: the solved tiles plus the later panels
       // of this tile
       const float xj = c > 4 * g + 3 ? xv[I0] : 0.f;
