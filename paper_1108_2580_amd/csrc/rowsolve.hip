@@ -522,10 +522,11 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
 #pragma unroll
   for (int I0 = T - 1; I0 >= 0; --I0) {
     // this tile row's partial products with the solved tiles X > I0 (row group g
-    // holds panel g's rows; the 16-lane sums follow per panel)
+    // holds panel g's rows; the 16-lane sums follow per panel), the newest tile last so
+    // that one product per row waits for it
     float P0 = 0.f, P1 = 0.f, P2 = 0.f, P3 = 0.f;
 #pragma unroll
-    for (int X = I0 + 1; X < T; ++X) {
+    for (int X = T - 1; X > I0; --X) {
       const floatx4 aa = acc[tidx<T>(I0, X)];
       P0 = fmaf(aa[0], xv[X], P0);
       P1 = fmaf(aa[1], xv[X], P1);
@@ -559,7 +560,10 @@ __global__ __launch_bounds__(64 * kRowWaves, 2) void k_rows(
                                fmaf(aa[3], xj, P3));
       const float a0 = lane_value(sr, 16 * g + 0), a1 = lane_value(sr, 16 * g + 4);
       const float a2 = lane_value(sr, 16 * g + 8), a3 = lane_value(sr, 16 * g + 12);
-      const float x = tj - (fmaf(wr.x, a0, wr.y * a1) + fmaf(wr.z, a2, wr.w * a3));
+      // computed in every lane and then selected: as a predicated update the compiler
+      // moves the LDS reads of W_p and t_p into the serial step
+      float x = tj - (fmaf(wr.x, a0, wr.y * a1) + fmaf(wr.z, a2, wr.w * a3));
+      asm volatile("" : "+v"(x));
       xv[I0] = (jj >= 0 && jj < 4) ? x : xv[I0];
     }
   }
