@@ -20,6 +20,20 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Sum over the four row groups (lanes l, l ^ 16, l ^ 32, l ^ 48), in every lane: the
+// 16-lane swap of a value with itself gives row groups {0, 0, 2, 2} and {1, 1, 3, 3},
+// whose sum the 32-lane swap then pairs across the halves. The additions associate as
+// (r0 + r1) + (r2 + r3), as the two butterfly steps xor 16 then xor 32 do, without the
+// round trips through the LDS unit that those shuffles take.
+__device__ __forceinline__ float sum_row_groups(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto h = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float s = __uint_as_float(h[0]) + __uint_as_float(h[1]);
+  const unsigned t = __float_as_uint(s);
+  const auto g = __builtin_amdgcn_permlane32_swap(t, t, false, false);
+  return __uint_as_float(g[0]) + __uint_as_float(g[1]);
+}
+
 // Rotate a value right by K lanes within each 16-lane row (DPP row_ror).
 template <int K>
 __device__ __forceinline__ float row_ror(float v) {
@@ -27,6 +41,36 @@ __device__ __forceinline__ float row_ror(float v) {
 }
 
 // Sum over the 16 lanes of a row; every lane of the row receives the same value.
+// Sum of a double over the 64 lanes, in every lane: rotations within each 16-lane row
+// (both 32-bit halves moved by DPP), then the two swaps across the row groups. A fixed
+// order, so the result is the same on every run.
+template <int K>
+__device__ __forceinline__ double row_ror_f64(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)b, 0x120 + K, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), 0x120 + K, 0xF, 0xF, false);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+__device__ __forceinline__ double sum_wave_f64(double v) {
+  v += row_ror_f64<8>(v);
+  v += row_ror_f64<4>(v);
+  v += row_ror_f64<2>(v);
+  v += row_ror_f64<1>(v);
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const unsigned lo = (unsigned)b, hi = (unsigned)(b >> 32);
+  auto join = [](unsigned l, unsigned h) {
+    return __longlong_as_double((long long)(((unsigned long long)h << 32) | l));
+  };
+  const auto l16 = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  const auto h16 = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+  const double s = join(l16[0], h16[0]) + join(l16[1], h16[1]);
+  const unsigned long long bs = (unsigned long long)__double_as_longlong(s);
+  const unsigned slo = (unsigned)bs, shi = (unsigned)(bs >> 32);
+  const auto l32 = __builtin_amdgcn_permlane32_swap(slo, slo, false, false);
+  const auto h32 = __builtin_amdgcn_permlane32_swap(shi, shi, false, false);
+  return join(l32[0], h32[0]) + join(l32[1], h32[1]);
+}
+
 __device__ __forceinline__ float sum16(float v) {
   v += row_ror<8>(v);
   v += row_ror<4>(v);
@@ -467,7 +511,9 @@ __host__ __device__ constexpr bool strip_width(int D) {
 // element r: G[16 I + 4 kq + r][16 (T - 1) + c], taken from lane 4 kq + c of the summed
 // strip), and write the right-hand side (per-lane partials in rhs) into lane column aug_c
 // of the same tiles (element r: b[16 I + 4 kq + r], from lane 4 kq + r of the summed rhs).
-// The other lane columns of these tiles become zero.
+// The other lane columns of these tiles become zero. (Here the row-group sums stay LDS
+// shuffles: with seven or eight tiles their latency overlaps, and the lane swaps of
+// sum_row_groups measured slower.)
 template <int DP>
 __device__ __forceinline__ void strip_finish(floatx4 (&acc)[RowCfg<DP>::NT],
                                              float (&rhs)[DP / 16], int aug_c) {

@@ -91,30 +91,25 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   if constexpr (!AUG || STRIP) {
 #pragma unroll
     for (int X = 0; X < T; ++X) {
-      rhs[X] += __shfl_xor(rhs[X], 16);
-      rhs[X] += __shfl_xor(rhs[X], 32);
+      rhs[X] = sum_row_groups(rhs[X]);
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
+  sse = sum_wave_f64(sse);
   float *__restrict__ out = ((int64_t)blockIdx.x < n_chunk_items ? ws : ne) + it.slot * NES;
   if constexpr (CORNER && !TS) {
     // the corner block (tile (1, 1) accumulator) and the right-hand side of features
     // 16..19, summed over the four rating groups: lane c < 4 holds G[16 + r][16 + c] in
     // element r and b[16 + c]
-    corner += __shfl_xor(corner, 16);
-    corner += __shfl_xor(corner, 32);
+    corner = sum_row_groups(corner);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float v = acc[tidx<T>(1, 1)][r];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
+      v = sum_row_groups(v);
       if (kq == 0 && c < 4 && r <= c) out[tri<LD>(16 + r, 16 + c)] = v;
     }
     if (kq == 0 && c < 4) out[NTRI + 16 + c] = corner;
   } else if constexpr (CORNER) {
-    corner += __shfl_xor(corner, 16);
-    corner += __shfl_xor(corner, 32);
+    corner = sum_row_groups(corner);
     if (kq == 0 && c < 15) {
       const int a = 16 + cp, b = 16 + cq;
       if (b < LD) out[tri<LD>(a, b)] = corner;
@@ -128,8 +123,7 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float v = acc[tidx<T>(0, 1)][r];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
+      v = sum_row_groups(v);
       if (kq == 0) out[tri<LD>(4 * (c >> 2) + r, 16 + (c & 3))] = v;
     }
     if (kq == 0) out[NTRI + c] = rhs[0];

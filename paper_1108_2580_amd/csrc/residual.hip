@@ -58,8 +58,7 @@ __global__ __launch_bounds__(64) void k_resid(const WorkItem *__restrict__ items
     wave_sync();  // the buffer is restaged by the next group
     gv = gn;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) sse += __shfl_xor(sse, o);
+  sse = sum_wave_f64(sse);
   if (lane == 0) sse_items[blockIdx.x] = sse;
 }
 
