@@ -32,6 +32,39 @@ namespace als {
 // the elementwise products Fp[idx] * hd.Tp[hd.idx2].
 // Waves per SIMD: six for plain ALS (79 registers), five for weighted and four for tensor
 // ALS, which gather more per rating; the bound keeps the allocator within each budget.
+// Record of the corner widths (LD = 20) staged in LDS: the tile (0, 0) accumulators
+// [lane][element], the summed strip of tile (0, 1) [lane column][element], the summed
+// corner block [lane column][element], the right-hand side b[0..19], a zero for the
+// padding entries, and a sink for the stores of lanes without an entry.
+constexpr int kImgTile = 0, kImgStrip = 256, kImgCorner = 320, kImgRhs = 336, kImgZero = 356,
+              kImgSink = 360, kImgFloats = 364;
+constexpr int kRecordEntries20 = ne_floats(20);
+static_assert(sizeof(GroupStage) >= sizeof(float) * kImgFloats, "the record image fits");
+// Source in the image of every record entry (packed upper triangle of G, then b).
+struct __attribute__((aligned(8))) RecordMap20 {
+  uint16_t src[kRecordEntries20];
+};
+constexpr RecordMap20 make_record_map20() {
+  RecordMap20 m{};
+  constexpr int LD = 20, NTRI = LD * (LD + 1) / 2;
+  for (int a = 0; a < LD; ++a) {
+    for (int b = a; b < LD; ++b) {
+      int src;
+      if (b < 16)
+        src = kImgTile + 4 * (16 * (a >> 2) + b) + (a & 3);  // lane (a >> 2, b), element a & 3
+      else if (a < 16)
+        src = kImgStrip + 4 * (4 * (a >> 2) + (b - 16)) + (a & 3);
+      else
+        src = kImgCorner + 4 * (b - 16) + (a - 16);
+      m.src[tri<LD>(a, b)] = (uint16_t)src;
+    }
+  }
+  for (int d = 0; d < LD; ++d) m.src[NTRI + d] = (uint16_t)(kImgRhs + d);
+  for (int e = NTRI + LD; e < kRecordEntries20; ++e) m.src[e] = (uint16_t)kImgZero;
+  return m;
+}
+__constant__ RecordMap20 kRecordMap20 = make_record_map20();
+
 template <int DP, int LD, bool AUG, bool WT, bool TS>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(TS ? 4 : WT ? 5 : 6)))
 void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
@@ -49,7 +82,7 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   // the tile above it, which holds four used features, goes to 4 x 4 strips (STRIP)
   constexpr bool CORNER = AUG && T == 2 && LD == 20;
   constexpr bool STRIP = CORNER;
-  __shared__ GroupStage s_stage;
+  __shared__ __attribute__((aligned(16))) GroupStage s_stage;
   const WorkItem it = items[blockIdx.x];
   const int lane = threadIdx.x, kq = lane >> 4, c = lane & 15;
   floatx4 acc[NT];
@@ -96,6 +129,36 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
   }
   sse = sum_wave_f64(sse);
   float *__restrict__ out = ((int64_t)blockIdx.x < n_chunk_items ? ws : ne) + it.slot * NES;
+  if constexpr (CORNER && !TS) {
+    // The record is assembled in LDS (the staging area is free once the accumulation has
+    // ended) with unmasked stores of each lane's values, then written with one coalesced
+    // 16-byte store per lane, whose four entries come from the record map.
+    static_assert(NES == kRecordEntries20 && LD == 20, "record map of the corner widths");
+    float *const img = reinterpret_cast<float *>(&s_stage);
+    *reinterpret_cast<floatx4 *>(img + kImgTile + 4 * lane) = acc[tidx<T>(0, 0)];
+    floatx4 sv, cv;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sv[r] = sum_row_groups(acc[tidx<T>(0, 1)][r]);
+      cv[r] = sum_row_groups(acc[tidx<T>(1, 1)][r]);
+    }
+    corner = sum_row_groups(corner);
+    // every row group holds the same sums: their stores to one address agree
+    *reinterpret_cast<floatx4 *>(img + kImgStrip + 4 * c) = sv;
+    *reinterpret_cast<floatx4 *>(c < 4 ? img + kImgCorner + 4 * c : img + kImgSink) = cv;
+    img[kImgRhs + c] = rhs[0];
+    img[c < 4 ? kImgRhs + 16 + c : kImgSink] = corner;
+    img[kImgZero] = 0.f;
+    wave_sync();
+    if (lane < NES / 4) {
+      const uint2 sp = *reinterpret_cast<const uint2 *>(&kRecordMap20.src[4 * lane]);
+      const float4 o = make_float4(img[sp.x & 0xFFFF], img[sp.x >> 16], img[sp.y & 0xFFFF],
+                                   img[sp.y >> 16]);
+      *reinterpret_cast<float4 *>(out + 4 * lane) = o;
+    }
+    if (lane == 0) sse_out[blockIdx.x] = sse;
+    return;
+  }
   if constexpr (CORNER && !TS) {
     // the corner block (tile (1, 1) accumulator) and the right-hand side of features
     // 16..19, summed over the four rating groups: lane c < 4 holds G[16 + r][16 + c] in
