@@ -146,8 +146,8 @@ def small_matrix(seed=0, M=400, N=300):
     return workload.make_custom(M, N, deg, seed=seed + 1, item_weights=w)
 
 
-@pytest.mark.parametrize("D", [1, 7, 10, 16, 17, 19, 20, 31, 32, 33, 36, 42, 48, 52, 64, 65, 84, 97,
-                               98, 100, 116, 124, 128])
+@pytest.mark.parametrize("D", [1, 7, 10, 16, 17, 18, 19, 20, 31, 32, 33, 36, 42, 48, 52, 64, 65, 84,
+                               97, 98, 99, 100, 116, 124, 128])
 def test_widths_with_split_rows_and_batches(D):
     M, N = 400, 300
     ptr, col, val = small_matrix(D)
