@@ -30,8 +30,8 @@ namespace als {
 // tile) and the per-rating right-hand-side FMAs disappear. WT: weighted ALS, with the
 // per-rating weights wts aligned with idx / val. TS: tensor ALS, whose fixed vectors are
 // the elementwise products Fp[idx] * hd.Tp[hd.idx2].
-// Waves per SIMD: six for plain ALS (79 registers), five for weighted and four for tensor
-// ALS, which gather more per rating; the bound keeps the allocator within each budget.
+// Waves per SIMD: six for plain ALS (under 80 registers), five for weighted and four for
+// tensor ALS, which gather more per rating; the bound keeps the allocator within each budget.
 // Record of the corner widths (LD = 20) staged in LDS: the tile (0, 0) accumulators
 // [lane][element], the summed strip of tile (0, 1) [lane column][element], the summed
 // corner block [lane column][element], the right-hand side b[0..19], a zero for the
@@ -159,19 +159,9 @@ void k_gram_ne(const WorkItem *__restrict__ items, int64_t n_chunk_items,
     if (lane == 0) sse_out[blockIdx.x] = sse;
     return;
   }
-  if constexpr (CORNER && !TS) {
-    // the corner block (tile (1, 1) accumulator) and the right-hand side of features
-    // 16..19, summed over the four rating groups: lane c < 4 holds G[16 + r][16 + c] in
-    // element r and b[16 + c]
-    corner = sum_row_groups(corner);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float v = acc[tidx<T>(1, 1)][r];
-      v = sum_row_groups(v);
-      if (kq == 0 && c < 4 && r <= c) out[tri<LD>(16 + r, 16 + c)] = v;
-    }
-    if (kq == 0 && c < 4) out[NTRI + 16 + c] = corner;
-  } else if constexpr (CORNER) {
+  if constexpr (CORNER) {
+    // (tensor ALS) lane c < 15 of a row group holds one corner product, summed over the
+    // four rating groups
     corner = sum_row_groups(corner);
     if (kq == 0 && c < 15) {
       const int a = 16 + cp, b = 16 + cq;
