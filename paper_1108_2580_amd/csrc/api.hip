@@ -94,10 +94,13 @@ struct als_ctx {
   double *d_sse_total = nullptr; // SSE of the last residual pass
   int32_t *d_flag = nullptr;
   double *h_sse = nullptr;    // pinned
-  double *h_sse_in = nullptr; // pinned [2]: the entering-state SSE of the last half-sweep,
-                              // in one part, or two for the time chain's even and odd passes
+  double *h_sse_in = nullptr; // pinned, mapped [2]: the entering-state SSE of the last
+                              // half-sweep, in one part, or two for the time chain's even and
+                              // odd passes
   int sse_in_parts = 1;
-  int32_t *h_flag = nullptr;  // pinned
+  int32_t *h_flag = nullptr;  // pinned, mapped
+  double *hd_sse_in = nullptr; // device addresses of h_sse_in and h_flag
+  int32_t *hd_flag = nullptr;
   int last_side = -1;
   std::string err;
   bool profiling = false;
@@ -676,8 +679,13 @@ als_status als_create(als_ctx **out, int64_t n_users, int64_t n_items, int64_t n
   CK(dalloc(&c->d_sse_total, 1));
   CK(dalloc(&c->d_flag, 1));
   CK(hipHostMalloc((void **)&c->h_sse, sizeof(double), hipHostMallocDefault));
-  CK(hipHostMalloc((void **)&c->h_sse_in, 2 * sizeof(double), hipHostMallocDefault));
-  CK(hipHostMalloc((void **)&c->h_flag, sizeof(int32_t), hipHostMallocDefault));
+  // written by the half-sweep's last reduction kernel, so coherent and mapped
+  CK(hipHostMalloc((void **)&c->h_sse_in, 2 * sizeof(double),
+                   hipHostMallocMapped | hipHostMallocCoherent));
+  CK(hipHostMalloc((void **)&c->h_flag, sizeof(int32_t),
+                   hipHostMallocMapped | hipHostMallocCoherent));
+  CK(hipHostGetDevicePointer((void **)&c->hd_sse_in, c->h_sse_in, 0));
+  CK(hipHostGetDevicePointer((void **)&c->hd_flag, c->h_flag, 0));
   *c->h_flag = 0;
   *c->h_sse = 0.0;
   c->h_sse_in[0] = c->h_sse_in[1] = 0.0;
@@ -798,12 +806,10 @@ als_status run_sweep(als_ctx *ctx, const SweepSpec &sp, float lambda, float *out
   {
     PhaseTimer t(ctx, 4);
     HIP_OR_FAIL(ctx, als::launch_reduce(ctx->d_sse_items, (int64_t)P.gitems.size(),
-                                        ctx->d_partials, ctx->d_sse_in, ctx->stream));
+                                        ctx->d_partials, ctx->d_sse_in, ctx->stream,
+                                        ctx->hd_sse_in + sp.sse_in_part, ctx->d_flag,
+                                        ctx->hd_flag));
   }
-  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_sse_in + sp.sse_in_part, ctx->d_sse_in, sizeof(double),
-                                  hipMemcpyDeviceToHost, ctx->stream));
-  HIP_OR_FAIL(ctx, hipMemcpyAsync(ctx->h_flag, ctx->d_flag, sizeof(int32_t),
-                                  hipMemcpyDeviceToHost, ctx->stream));
   ctx->last_side = side;
   ctx->sse_in_parts = sp.sse_in_part + 1;
   if (ctx->phase_timing && !ctx->lane_solve && !P.rows.empty() && side < 2) {

@@ -142,10 +142,13 @@ hipError_t launch_solve_lane(int D, const RowTask *rows, int64_t n_rows, int64_t
                              int64_t base, const float *ws, float *ne, float lam, float *X,
                              int32_t *flag, const RowPrior &pr, hipStream_t s);
 
-// Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)].
+// Fixed-order sum of n doubles into *out; partials: double[reduce_partials(n)]. host_out, if
+// given, is the device address of mapped, coherent pinned host memory that receives the total
+// as well; flag and host_flag (both or neither) copy one device int32 to such memory.
 int64_t reduce_partials(int64_t n);
 hipError_t launch_reduce(const double *v, int64_t n, double *partials, double *out,
-                         hipStream_t s);
+                         hipStream_t s, double *host_out = nullptr,
+                         const int32_t *flag = nullptr, int32_t *host_flag = nullptr);
 
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 

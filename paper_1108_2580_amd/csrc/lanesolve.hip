@@ -49,13 +49,9 @@ constexpr RecordMap20 make_record_map20() {
   constexpr int LD = 20, NTRI = LD * (LD + 1) / 2;
   for (int a = 0; a < LD; ++a) {
     for (int b = a; b < LD; ++b) {
-      int src;
-      if (b < 16)
-        src = kImgTile + 4 * (16 * (a >> 2) + b) + (a & 3);  // lane (a >> 2, b), element a & 3
-      else if (a < 16)
-        src = kImgStrip + 4 * (4 * (a >> 2) + (b - 16)) + (a & 3);
-      else
-        src = kImgCorner + 4 * (b - 16) + (a - 16);
+      const int src = b < 16   ? kImgTile + 4 * (16 * (a >> 2) + b) + (a & 3)  // lane (a >> 2, b), element a & 3
+                      : a < 16 ? kImgStrip + 4 * (4 * (a >> 2) + (b - 16)) + (a & 3)
+                               : kImgCorner + 4 * (b - 16) + (a - 16);
       m.src[tri<LD>(a, b)] = (uint16_t)src;
     }
   }
@@ -216,7 +212,10 @@ __global__ __launch_bounds__(256) void k_sum_records(const RowTask *__restrict__
   constexpr int NES = ne_floats(LD);
   const RowTask rt = rows[blockIdx.x];
   for (int e = threadIdx.x; e < NES; e += 256) {
+    // unrolled so that several slots' loads are in flight before their additions, which
+    // stay in slot order
     float v = 0.f;
+#pragma unroll 8
     for (int s = 0; s < rt.nslots; ++s) v += ws[(rt.slot0 + s) * (int64_t)NES + e];
     ne[(base + blockIdx.x) * (int64_t)NES + e] = v;
   }

@@ -211,28 +211,38 @@ __global__ __launch_bounds__(kRedBlock) void k_reduce_partial(const double *__re
   if (threadIdx.x == 0) partial[blockIdx.x] = tot;
 }
 
-// One block: thread t sums partials t, t+256, ... in order, then a fixed tree.
+// One block: thread t sums partials t, t+256, ... in order, then a fixed tree. On request
+// thread 0 also stores the total, and a copy of *flag, into mapped host memory, in place of
+// two device-to-host copies after the kernel.
 __global__ __launch_bounds__(kRedBlock) void k_reduce_final(const double *__restrict__ partial,
-                                                            int64_t np, double *__restrict__ out) {
+                                                            int64_t np, double *__restrict__ out,
+                                                            double *host_out,
+                                                            const int32_t *__restrict__ flag,
+                                                            int32_t *host_flag) {
   __shared__ double sh[kRedBlock];
   double s = 0.0;
   for (int64_t i = threadIdx.x; i < np; i += kRedBlock) s += partial[i];
   const double tot = block_tree_sum(s, sh);
-  if (threadIdx.x == 0) *out = tot;
+  if (threadIdx.x == 0) {
+    *out = tot;
+    if (host_out) *host_out = tot;
+    if (host_flag) *host_flag = *flag;
+  }
 }
 
 hipError_t launch_reduce(const double *v, int64_t n, double *partials, double *out,
-                         hipStream_t s) {
-  const int64_t np = reduce_partials(n);
+                         hipStream_t s, double *host_out, const int32_t *flag,
+                         int32_t *host_flag) {
+  if ((flag == nullptr) != (host_flag == nullptr)) return hipErrorInvalidValue;
+  const int64_t np = n > 0 ? reduce_partials(n) : 0;
   if (n > 0) {
     hipLaunchKernelGGL(k_reduce_partial, dim3((unsigned)np), dim3(kRedBlock), 0, s, v, n,
                        partials);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_reduce_final, dim3(1), dim3(kRedBlock), 0, s, partials, np, out);
-  } else {
-    hipLaunchKernelGGL(k_reduce_final, dim3(1), dim3(kRedBlock), 0, s, partials, (int64_t)0, out);
   }
+  hipLaunchKernelGGL(k_reduce_final, dim3(1), dim3(kRedBlock), 0, s, partials, np, out, host_out,
+                     flag, host_flag);
   return hipGetLastError();
 }
 
