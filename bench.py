@@ -14,9 +14,10 @@ Default workload: the full-scale synthetic stand-in for the paper's data set
 lambda = 0.065 weighted by n_s. --config 4 selects the same matrix at D = 100.
 
 Besides the JSON line's throughput, the script reports the roofline position
-of the dominant kernel (HIP-event timing of every launch over the timed
-region) and the fp64 CPU oracle's throughput on a bounded sample of the same
-half-sweep on this host's cores.
+of the dominant kernel (HIP-event timing of each of its launches over the timed
+region; the other phases are timed on two extra untimed sweeps, so that their
+event records stay out of the timed region) and the fp64 CPU oracle's throughput
+on a bounded sample of the same half-sweep on this host's cores.
 """
 import argparse
 import hashlib
@@ -47,6 +48,9 @@ def parse():
                     help="target duration of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for HBM counter scaling)")
+    ap.add_argument("--phase-sweeps", type=int, default=2,
+                    help="untimed sweeps with every phase timed, after the timed ones (0: none; "
+                         "phases_ms_per_step is then null)")
     ap.add_argument("--heldout-share", type=int, default=64,
                     help="held-out prediction leg on 1/K of the stored positions (0 disables)")
     ap.add_argument("--weighted", action="store_true",
@@ -449,7 +453,9 @@ def run_workload(args, k):
         torch.cuda.synchronize()
         log(f"warmup {w + 1}/{args.warmup} done")
     torch.cuda.synchronize()
-    als.set_profiling(True)
+    # the timed sweeps carry event records only around the kernels that build the normal
+    # equations (the roofline's kernels); each record costs about 3 us of stream time
+    als.set_profiling(True, gram_only=True)
     # HIP events around each half-sweep on the stream the library enqueues on
     ev = {side: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                  for _ in range(args.steps)] for side in sides}
@@ -471,6 +477,15 @@ def run_workload(args, k):
     elapsed = t1 - t0
     rmse_in = als.rmse_in()
     rmse = als.tensor_rmse(U, V, T) if (args.tensor or args.bptf) else als.rmse(U, V)
+    # every phase's time, on extra untimed sweeps with events around every launch
+    prof_all = None
+    if args.phase_sweeps > 0:
+        als.set_profiling(True)
+        for _ in range(args.phase_sweeps):
+            for side in sides:
+                half(side, args.warmup + args.steps - 1)
+        prof_all = als.profile()
+        als.set_profiling(False)
     gram_share = phase_cycles = None
     if r.D > 20 and not (args.tensor or args.bptf):
         # one extra, untimed half-sweep per side with the row kernel's phase clocks on
@@ -486,7 +501,8 @@ def run_workload(args, k):
         # mean wavefront clock cycles per row in each phase (both waves of a SIMD share it)
         phase_cycles = {"items": {"gram": gi / max(rows_i, 1), "solve": si / max(rows_i, 1)},
                         "users": {"gram": gu / max(rows_u, 1), "solve": su / max(rows_u, 1)}}
-    log(f"timed {args.steps} sweeps in {elapsed:.3f} s; phases (ms total, launches): {prof}; "
+    log(f"timed {args.steps} sweeps in {elapsed:.3f} s; timed kernels (ms total, launches): "
+        f"{prof}; phases of {args.phase_sweeps} extra sweeps: {prof_all}; "
         f"rmse entering last half-sweep {rmse_in}, final {rmse:.6f}")
 
     value = len(sides) * r.nnz * args.steps / elapsed
@@ -502,7 +518,7 @@ def run_workload(args, k):
     workload_name = r.name + ("_wals" if args.weighted else "_bpmf" if args.gibbs else
                               "_tensor" if args.tensor else "_bptf" if args.bptf else "")
     tensor_like = args.tensor or args.bptf
-    dominant = max(prof, key=lambda k: prof[k][0])
+    dominant = max(prof_all or prof, key=lambda k: (prof_all or prof)[k][0])
     # per rating: a weight (weighted ALS); the second index and second gathered row, and
     # the product of the two rows (tensor ALS)
     wbytes = 4 if args.weighted else (4 + 4 * D) if tensor_like else 0
@@ -560,7 +576,7 @@ def run_workload(args, k):
     # D <= 20; at D > 20 the fused row kernel's time scaled by the share of its wavefront
     # cycles from the factorisation on (phase clocks; plain ALS and BPMF)
     if D <= 20:
-        chol_ms = prof["solve"][0] / args.steps
+        chol_ms = prof_all["solve"][0] / args.phase_sweeps if prof_all else None
     elif gram_share is not None:
         chol_ms = (1.0 - gram_share) * prof["solve"][0] / args.steps
     else:
@@ -617,7 +633,8 @@ def run_workload(args, k):
         "per_side": per_side,
         "gram_phase": gram_phase,
         "chol_ms_per_step": chol_ms,
-        "phases_ms_per_step": {k: v[0] / args.steps for k, v in prof.items()},
+        "phases_ms_per_step": ({k: v[0] / args.phase_sweeps for k, v in prof_all.items()}
+                               if prof_all else None),
         "rmse": rmse,
         "rmse_entering_last_half_sweep": rmse_in,
         "heldout": heldout,

@@ -162,9 +162,12 @@ als_status als_plan_stats(als_ctx *ctx, als_side side, int64_t *out, int32_t n);
  * equations of every row and chunk; D > 20: those of split-row chunks);
  * 2 = solve kernels (D <= 20: one row per lane; D > 20: the fused row kernel,
  * which also builds the normal equations of unsplit rows); 3 = new-state
- * residual pass; 4 = reductions. als_set_profiling(ctx, 1) resets the totals;
- * als_get_profile synchronises the stream, folds the recorded events into the
- * totals and returns the summed milliseconds and launch count of one phase.
+ * residual pass; 4 = reductions. enable: 0 = off; 1 = every phase; 2 = only the
+ * launches that build the normal equations (phase 1, and phase 2 above D = 20), so
+ * that no event record sits between the other launches. Other values:
+ * ALS_ERR_INVALID_ARG. Enabling (1 or 2) resets the totals; als_get_profile
+ * synchronises the stream, folds the recorded events into the totals and returns the
+ * summed milliseconds and launch count of one phase.
  */
 als_status als_set_profiling(als_ctx *ctx, int32_t enable);
 als_status als_get_profile(als_ctx *ctx, int32_t phase, double *total_ms, int64_t *launches);

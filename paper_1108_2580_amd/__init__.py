@@ -11,6 +11,10 @@ import ctypes
 import os
 
 import numpy as np
+# torch first: its bundled HIP runtime (soname libamdhip64.so.7) then satisfies libals.so's
+# dependency, so the process holds one HIP runtime. Opened before torch, libals.so would load
+# the system's runtime, torch would load its own beside it, and the library would see no device.
+import torch  # noqa: F401
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libals.so")
@@ -218,8 +222,10 @@ class ALS:
                 "workspace_bytes", "slot_bytes")
         return dict(zip(keys, (int(v) for v in out)))
 
-    def set_profiling(self, on=True):
-        self._check(lib.als_set_profiling(self._h, 1 if on else 0))
+    def set_profiling(self, on=True, gram_only=False):
+        """Per-phase HIP event timing; ``gram_only`` times only the launches that build the
+        normal equations (mode 2 of ``als_set_profiling``)."""
+        self._check(lib.als_set_profiling(self._h, (2 if gram_only else 1) if on else 0))
 
     def profile(self):
         res = {}

@@ -104,6 +104,7 @@ struct als_ctx {
   int last_side = -1;
   std::string err;
   bool profiling = false;
+  int prof_mode = 0;  // 1: every phase; 2: the launches that build the normal equations
   std::vector<ProfEvent> prof_pending;
   std::vector<hipEvent_t> ev_pool;
   double prof_ms[kPhases] = {0, 0, 0, 0, 0};
@@ -425,7 +426,9 @@ struct PhaseTimer {
   int phase;
   hipEvent_t a = nullptr;
   PhaseTimer(als_ctx *ctx, int ph) : c(ctx), phase(ph) {
-    if (c->profiling && (a = take_event(c))) (void)hipEventRecord(a, c->stream);
+    // mode 2 times only the gather kernels and, above D = 20, the fused row kernel
+    const bool on = c->profiling && (c->prof_mode == 1 || ph == 1 || (ph == 2 && !c->lane_solve));
+    if (on && (a = take_event(c))) (void)hipEventRecord(a, c->stream);
   }
   ~PhaseTimer() {
     if (!a) return;
@@ -1651,9 +1654,12 @@ als_status als_pair_rmse_noalloc(als_ctx *ctx, const float *U, const float *V, i
 
 als_status als_set_profiling(als_ctx *ctx, int32_t enable) {
   if (!ctx) return fail(nullptr, ALS_ERR_INVALID_ARG, "NULL context");
+  if (enable < 0 || enable > 2)
+    return fail(ctx, ALS_ERR_INVALID_ARG, "profiling mode %d is not 0, 1 or 2", (int)enable);
   als_status st = collect_profile(ctx);
   if (st != ALS_OK) return st;
   ctx->profiling = enable != 0;
+  ctx->prof_mode = enable;
   if (enable) {
     for (int i = 0; i < kPhases; ++i) {
       ctx->prof_ms[i] = 0.0;
